@@ -1,0 +1,451 @@
+"""Plain float64 oracle of the spectral spin-weighted spherical convolution layer.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring): slow, obviously correct
+numpy code that the GPU library is compared against.  Nothing here is tuned.
+
+What it computes (Esteves, Slotine, Makadia, "Scaling Spherical CNNs",
+ICML 2023):
+
+* the forward spin-weighted spherical Fourier transform, eq. (2) of the
+  Background section, evaluated by Driscoll--Healy quadrature on the
+  equiangular grid (the paper's "Computing generalized convolutions"
+  paragraph cites Driscoll--Healy and Kostelec--Rockmore for it);
+* the inverse transform, eq. (3);
+* the convolution as per-degree products of coefficients with filters shared
+  across the order m ("Spherical CNNs" paragraph: spin-weighted convolutions
+  are products of spin-weighted harmonic coefficients; Fig. 2's "*K");
+* the phase-collapse nonlinearity (Method, "Phase collapse nonlinearity");
+* the Funk--Hecke projection of isotropic bumps used to synthesise the
+  molecule-shaped inputs.
+
+Conventions (the paper fixes them only through eqs. (4) and (6); the readings
+are listed in the design doc):
+
+* grid: theta_j = pi (2j+1) / (2H), phi_k = 2 pi k / W;
+* Wigner d: d^1_{10}(beta) = -sin(beta)/sqrt(2);
+* spin harmonics: sY_lm(theta, phi) = (-1)^s N_l d^l_{m,-s}(theta) e^{i m phi},
+  N_l = sqrt((2l+1)/(4 pi)); 0Y_lm is the Condon--Shortley Y_lm;
+* coefficient layout: row l^2 + l + m of a [L^2, ...] array; rows with
+  l < |s| do not exist and hold 0;
+* filter layout: K[l, t, c_out, s, c_in] (output spin/channel first).
+
+Parity: every function here is pinned by tests/test_oracle_*.py against
+closed forms, exact rational arithmetic, library routines, invariants or
+brute force (see each docstring's "Pinned by").
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+__all__ = [
+    "grid",
+    "dh_weights",
+    "wigner_d",
+    "wigner_d_sum_exact",
+    "spin_harmonic",
+    "coef_index",
+    "forward",
+    "forward_direct",
+    "inverse",
+    "evaluate",
+    "mix",
+    "conv",
+    "phase_collapse",
+    "bump_coefficients",
+]
+
+
+# --------------------------------------------------------------------------
+# Grid and quadrature
+# --------------------------------------------------------------------------
+
+def grid(H: int, W: int):
+    """Equiangular sample points: colatitudes theta_j and longitudes phi_k.
+
+    The paper only requires an equiangular grid with the same number of
+    samples on both axes (appendix, WeatherBench details); we take the
+    pole-free Driscoll--Healy / Kostelec--Rockmore offset grid
+    theta_j = pi (2j+1)/(2H), phi_k = 2 pi k / W.
+    Pinned by: tests/test_oracle_quadrature.py (exactness of the rule built
+    on it).
+    """
+    j = np.arange(H, dtype=np.float64)
+    k = np.arange(W, dtype=np.float64)
+    theta = np.pi * (2.0 * j + 1.0) / (2.0 * H)
+    phi = 2.0 * np.pi * k / W
+    return theta, phi
+
+
+def dh_weights(H: int) -> np.ndarray:
+    """Driscoll--Healy latitude weights on the offset grid (H even).
+
+    w_j = (4/H) sin(theta_j) sum_{p=0}^{H/2-1} sin((2p+1) theta_j) / (2p+1),
+    so that (2 pi / W) sum_{j,k} w_j g(theta_j, phi_k) integrates g over the
+    sphere exactly when g is band-limited to degree < H in latitude and
+    |order| < W in longitude.
+    Pinned by: Fejer's first-rule closed form, exact integrals of cos^q,
+    orthogonality of Legendre polynomials (tests/test_oracle_quadrature.py).
+    """
+    if H % 2:
+        raise ValueError("H must be even")
+    theta, _ = grid(H, 1)
+    p = np.arange(H // 2, dtype=np.float64)
+    s = np.sin(np.outer(theta, 2.0 * p + 1.0)) / (2.0 * p + 1.0)
+    return (4.0 / H) * np.sin(theta) * s.sum(axis=1)
+
+
+# --------------------------------------------------------------------------
+# Wigner small-d functions
+# --------------------------------------------------------------------------
+
+def _wigner_seed(j: int, m: int, n: int, c: np.ndarray, sg: np.ndarray) -> np.ndarray:
+    """d^j_{mn} at the lowest degree j = max(|m|, |n|), where the textbook
+    sum has a single term.  c = cos(beta/2), sg = sin(beta/2)."""
+    if m == j:
+        return math.sqrt(math.comb(2 * j, j + n)) * c ** (j + n) * (-sg) ** (j - n)
+    if m == -j:
+        return math.sqrt(math.comb(2 * j, j - n)) * c ** (j - n) * sg ** (j + n)
+    if n == j:
+        return math.sqrt(math.comb(2 * j, j + m)) * c ** (j + m) * sg ** (j - m)
+    # n == -j
+    return math.sqrt(math.comb(2 * j, j - m)) * c ** (j - m) * (-sg) ** (j + m)
+
+
+def wigner_d(L: int, m: int, n: int, beta) -> np.ndarray:
+    """d^l_{mn}(beta) for l = 0..L-1 (rows), zero where l < max(|m|, |n|).
+
+    The paper uses Wigner Delta = d(pi/2) in eqs. (4)-(6); we evaluate d at
+    the grid colatitudes directly.  Seed at l0 = max(|m|,|n|) from the
+    single-term textbook sum, then the standard three-term recurrence in l:
+
+      d^{l+1} = (l+1)(2l+1) / sqrt(((l+1)^2-m^2)((l+1)^2-n^2))
+                * [ (cos b - m n/(l(l+1))) d^l
+                    - sqrt((l^2-m^2)(l^2-n^2)) / (l(2l+1)) d^{l-1} ]
+
+    (the m n/(l(l+1)) term is absent at l = 0).
+    Pinned by: exact rational evaluation of the full textbook sum, scipy's
+    associated Legendre functions at n = 0, orthogonality, symmetries,
+    d(0) = I, and the paper's Delta identity of eqs. (4)/(6)
+    (tests/test_oracle_wigner.py).
+    """
+    beta = np.atleast_1d(np.asarray(beta, dtype=np.float64))
+    out = np.zeros((L, beta.size), dtype=np.float64)
+    l0 = max(abs(m), abs(n))
+    if l0 >= L:
+        return out
+    c = np.cos(beta / 2.0)
+    sg = np.sin(beta / 2.0)
+    cb = np.cos(beta)
+    out[l0] = _wigner_seed(l0, m, n, c, sg)
+    prev = np.zeros_like(beta)
+    cur = out[l0].copy()
+    for l in range(l0, L - 1):
+        lp = l + 1
+        a = lp * (2 * l + 1) / math.sqrt((lp * lp - m * m) * (lp * lp - n * n))
+        if l == 0:
+            t1 = cb * cur
+        else:
+            t1 = (cb - m * n / (l * (l + 1.0))) * cur
+        if l > l0:
+            t2 = math.sqrt((l * l - m * m) * (l * l - n * n)) / (l * (2 * l + 1.0)) * prev
+        else:
+            t2 = 0.0
+        nxt = a * (t1 - t2)
+        out[lp] = nxt
+        prev, cur = cur, nxt
+    return out
+
+
+def wigner_d_sum_exact(l: int, m: int, n: int, cos_half, sin_half) -> float:
+    """Full textbook sum for d^l_{mn}(beta) in exact rational arithmetic.
+
+    d^l_{mn} = sqrt((l+m)!(l-m)!(l+n)!(l-n)!) *
+               sum_k (-1)^(k-n+m) c^(2l-2k+n-m) s^(2k-n+m)
+                     / ((l+n-k)! k! (l-k-m)! (k-n+m)!)
+    with c = cos(beta/2), s = sin(beta/2) given as fractions.Fraction, so the
+    sum (which cancels badly in floating point) is exact; only the final
+    square-root factor is rounded.  Used only as a pin for wigner_d.
+    """
+    from fractions import Fraction
+
+    c = Fraction(cos_half)
+    s = Fraction(sin_half)
+    total = Fraction(0)
+    for k in range(0, 2 * l + 1):
+        a1, a2, a3, a4 = l + n - k, k, l - k - m, k - n + m
+        if min(a1, a2, a3, a4) < 0:
+            continue
+        den = (math.factorial(a1) * math.factorial(a2) * math.factorial(a3)
+               * math.factorial(a4))
+        term = c ** (2 * l - 2 * k + n - m) * s ** (2 * k - n + m) / den
+        total += -term if (k - n + m) % 2 else term
+    pref = (math.factorial(l + m) * math.factorial(l - m)
+            * math.factorial(l + n) * math.factorial(l - n))
+    # sqrt(pref) * total, with the irrational factor rounded once at the end
+    return float(total) * math.sqrt(pref) if pref < 2 ** 1000 else \
+        float(total * math.isqrt(pref * 10 ** 40)) / 1e20
+
+
+# --------------------------------------------------------------------------
+# Spin-weighted spherical harmonics
+# --------------------------------------------------------------------------
+
+def _norm(l):
+    return np.sqrt((2.0 * np.asarray(l, dtype=np.float64) + 1.0) / (4.0 * np.pi))
+
+
+def spin_harmonic(s: int, l: int, m: int, theta, phi) -> np.ndarray:
+    """sY_lm(theta, phi) = (-1)^s sqrt((2l+1)/(4pi)) d^l_{m,-s}(theta) e^{i m phi}.
+
+    Zero for l < max(|m|, |s|).  This is the convention under which the
+    paper's eqs. (4) and (6) hold and 0Y_lm is the standard harmonic
+    (Background, after eqs. (2)-(3)).
+    Pinned by: scipy's sph_harm_y at s = 0, closed forms for l <= 2, spin
+    raising by finite differences, eqs. (4)/(6) (tests/test_oracle_wigner.py).
+    """
+    theta = np.asarray(theta, dtype=np.float64)
+    phi = np.asarray(phi, dtype=np.float64)
+    if l < max(abs(m), abs(s)):
+        return np.zeros(np.broadcast(theta, phi).shape, dtype=np.complex128)
+    d = wigner_d(l + 1, m, -s, theta.ravel())[l].reshape(theta.shape)
+    return ((-1.0) ** s) * _norm(l) * d * np.exp(1j * m * phi)
+
+
+def coef_index(l: int, m: int) -> int:
+    """Row of coefficient (l, m) in the packed [L^2] layout."""
+    return l * l + l + m
+
+
+# --------------------------------------------------------------------------
+# Forward / inverse transforms, eqs. (2) and (3)
+# --------------------------------------------------------------------------
+
+def _orders(L: int) -> np.ndarray:
+    return np.arange(-(L - 1), L)
+
+
+def _lon_dft_matrix(W: int, L: int, sign: int) -> np.ndarray:
+    """e^{sign * 2 pi i (m k mod W)/W}, shape [W, 2L-1]; phases are reduced
+    exactly in integers before the float64 exponential."""
+    k = np.arange(W)
+    m = _orders(L)
+    r = np.mod(np.outer(k, m), W).astype(np.float64)
+    return np.exp(sign * 2j * np.pi * r / W)
+
+
+def forward(x: np.ndarray, L: int, spins) -> np.ndarray:
+    """Forward SWSFT, eq. (2), by separable Driscoll--Healy quadrature.
+
+    x: complex [B, S, C, H, W] on the grid of `grid`; returns complex
+    coefficients [L^2, B, S, C] with
+      a[l^2+l+m, b, s, c] = (2pi/W) sum_j w_j sum_k x[b,s,c,j,k] conj(sY_lm(theta_j, phi_k)),
+    evaluated as a longitude DFT with exactly reduced phases followed by the
+    latitude sum.  Rows with l < |s| are zero.
+    Pinned by: forward_direct on tiny grids, orthonormality, Parseval,
+    round trip, the mean, longitude-shift equivariance
+    (tests/test_oracle_transform.py).
+    """
+    x = np.asarray(x, dtype=np.complex128)
+    B, S, C, H, W = x.shape
+    spins = list(spins)
+    assert S == len(spins)
+    theta, _ = grid(H, W)
+    w = dh_weights(H)
+    E = _lon_dft_matrix(W, L, -1)
+    # X[b, s, c, j, mi] = (2pi/W) sum_k x[b,s,c,j,k] e^{-i m phi_k}
+    X = (2.0 * np.pi / W) * (x.reshape(-1, W) @ E).reshape(B, S, C, H, 2 * L - 1)
+    coef = np.zeros((L * L, B, S, C), dtype=np.complex128)
+    lvals = np.arange(L)
+    for si, s in enumerate(spins):
+        for mi, m in enumerate(_orders(L)):
+            lo = max(abs(m), abs(s))
+            if lo >= L:
+                continue
+            d = wigner_d(L, m, -s, theta)  # [L, H]
+            tab = ((-1.0) ** s) * _norm(lvals)[:, None] * d * w[None, :]
+            # [L, H] x [H, B*C]
+            Xm = X[:, si, :, :, mi].transpose(2, 0, 1).reshape(H, B * C)
+            a = (tab @ Xm).reshape(L, B, C)
+            for l in range(lo, L):
+                coef[coef_index(l, m), :, si, :] = a[l]
+    return coef
+
+
+def forward_direct(x: np.ndarray, L: int, spins) -> np.ndarray:
+    """Eq. (2) as one unseparated double sum over every grid point, with the
+    harmonics evaluated by `spin_harmonic` and np.exp of the raw angle.
+    O(H W L^2) per map: tiny grids only."""
+    x = np.asarray(x, dtype=np.complex128)
+    B, S, C, H, W = x.shape
+    theta, phi = grid(H, W)
+    w = dh_weights(H)
+    TH, PH = np.meshgrid(theta, phi, indexing="ij")
+    q = (2.0 * np.pi / W) * w[:, None] * np.ones((H, W))
+    coef = np.zeros((L * L, B, S, C), dtype=np.complex128)
+    for si, s in enumerate(spins):
+        for l in range(abs(s), L):
+            for m in range(-l, l + 1):
+                Y = spin_harmonic(s, l, m, TH, PH)
+                coef[coef_index(l, m), :, si, :] = np.einsum(
+                    "bcjk,jk->bc", x[:, si], q * np.conj(Y))
+    return coef
+
+
+def inverse(coef: np.ndarray, H: int, W: int, spins) -> np.ndarray:
+    """Inverse SWSFT, eq. (3): y = sum_{l >= |s|} sum_{|m| <= l} a_lm sY_lm.
+
+    coef: complex [L^2, B, S, C]; returns complex [B, S, C, H, W].  Separable:
+    first G[j, m] = sum_l a_lm (-1)^s N_l d^l_{m,-s}(theta_j), then the
+    longitude sum over m with exactly reduced phases.  Rows with l < |s| are
+    ignored.
+    Pinned by: evaluate (direct sum at arbitrary points), round trip,
+    orthonormality (tests/test_oracle_transform.py).
+    """
+    coef = np.asarray(coef, dtype=np.complex128)
+    L2, B, S, C = coef.shape
+    L = int(round(math.sqrt(L2)))
+    assert L * L == L2
+    spins = list(spins)
+    theta, _ = grid(H, W)
+    lvals = np.arange(L)
+    G = np.zeros((B, S, C, H, 2 * L - 1), dtype=np.complex128)
+    for si, s in enumerate(spins):
+        for mi, m in enumerate(_orders(L)):
+            lo = max(abs(m), abs(s))
+            if lo >= L:
+                continue
+            d = wigner_d(L, m, -s, theta)
+            tab = ((-1.0) ** s) * _norm(lvals)[:, None] * d  # [L, H]
+            a = np.zeros((L, B, C), dtype=np.complex128)
+            for l in range(lo, L):
+                a[l] = coef[coef_index(l, m), :, si, :]
+            # [H, L] x [L, B*C]
+            g = tab.T @ a.reshape(L, B * C)
+            G[:, si, :, :, mi] = g.reshape(H, B, C).transpose(1, 2, 0)
+    E = _lon_dft_matrix(W, L, +1)  # [W, 2L-1]
+    y = G.reshape(-1, 2 * L - 1) @ E.T
+    return y.reshape(B, S, C, H, W)
+
+
+def evaluate(coef: np.ndarray, spins, theta, phi) -> np.ndarray:
+    """Direct sum of eq. (3) at arbitrary points (theta, phi) (same shape);
+    returns complex [B, S, C, *theta.shape].  Slow; tiny cases only."""
+    coef = np.asarray(coef, dtype=np.complex128)
+    L2, B, S, C = coef.shape
+    L = int(round(math.sqrt(L2)))
+    theta = np.asarray(theta, dtype=np.float64)
+    phi = np.asarray(phi, dtype=np.float64)
+    out = np.zeros((B, S, C) + theta.shape, dtype=np.complex128)
+    for si, s in enumerate(spins):
+        for l in range(abs(s), L):
+            for m in range(-l, l + 1):
+                Y = spin_harmonic(s, l, m, theta, phi)
+                out[:, si] += np.multiply.outer(coef[coef_index(l, m), :, si, :], Y)
+    return out
+
+
+# --------------------------------------------------------------------------
+# Convolution: per-degree products with filters shared across m
+# --------------------------------------------------------------------------
+
+def mix(coef: np.ndarray, K: np.ndarray, spins_in, spins_out) -> np.ndarray:
+    """a'[l^2+l+m, b, t, c'] = sum_{s, |s|<=l} sum_c K[l, t, c', s, c] a[l^2+l+m, b, s, c]
+    for |t| <= l, else 0.
+
+    The spin-weighted convolution is a product of coefficients per degree l
+    with filters shared across the order m (Background, "Spherical CNNs";
+    Fig. 2's "*K"); spins are mixed as channels.
+    coef: [L^2, B, S_in, C_in]; K: [L, S_out, C_out, S_in, C_in]; returns
+    [L^2, B, S_out, C_out].
+    Pinned by: an explicit loop over (l, m) on small cases, identity and
+    scalar filters, the spin-raising filter, brute-force SO(3) convolution
+    (tests/test_oracle_conv.py).
+    """
+    coef = np.asarray(coef, dtype=np.complex128)
+    K = np.asarray(K, dtype=np.complex128)
+    L2, B, S, C = coef.shape
+    L = K.shape[0]
+    assert L * L == L2
+    T, Co = K.shape[1], K.shape[2]
+    out = np.zeros((L2, B, T, Co), dtype=np.complex128)
+    sin_ = np.abs(np.asarray(list(spins_in)))
+    sout = np.abs(np.asarray(list(spins_out)))
+    for l in range(L):
+        Kl = K[l] * (sout[:, None, None, None] <= l) * (sin_[None, None, :, None] <= l)
+        rows = slice(l * l, (l + 1) * (l + 1))
+        a = coef[rows].reshape(-1, S * C)                    # [(2l+1) B, S C]
+        out[rows] = (a @ Kl.reshape(T * Co, S * C).T).reshape(2 * l + 1, B, T, Co)
+    return out
+
+
+def conv(x: np.ndarray, K: np.ndarray, L: int, spins_in, spins_out) -> np.ndarray:
+    """The layer: inverse(mix(forward(x))).  x: [B, S_in, C_in, H, W];
+    returns [B, S_out, C_out, H, W]."""
+    H, W = x.shape[-2:]
+    a = forward(x, L, spins_in)
+    return inverse(mix(a, K, spins_in, spins_out), H, W, spins_out)
+
+
+# --------------------------------------------------------------------------
+# Phase collapse (Method, "Phase collapse nonlinearity")
+# --------------------------------------------------------------------------
+
+def phase_collapse(x: np.ndarray, spins, W1: np.ndarray, W2: np.ndarray,
+                   bias: np.ndarray) -> np.ndarray:
+    """At every grid point, x0 <- W1 x0 + W2 |x| + b; other spins unchanged.
+
+    x: complex [B, S, C, H, W]; x0 = x[:, spins.index(0)] (C channels);
+    |x| stacks the moduli of all S*C channels in (spin, channel) order;
+    W1: complex [C, C]; W2: complex [C, S*C]; bias: complex [C].
+    Pinned by: invariants and selector-matrix cases
+    (tests/test_oracle_conv.py).
+    """
+    x = np.asarray(x, dtype=np.complex128)
+    B, S, C, H, W = x.shape
+    spins = list(spins)
+    s0 = spins.index(0)
+    y = x.copy()
+    z0 = x[:, s0]                                   # [B, C, H, W]
+    mag = np.abs(x).reshape(B, S * C, H, W)         # [B, S*C, H, W]
+    y[:, s0] = (np.einsum("oc,bchw->bohw", W1, z0)
+                + np.einsum("oc,bchw->bohw", W2, mag)
+                + bias[None, :, None, None])
+    return y
+
+
+# --------------------------------------------------------------------------
+# Input synthesis helper: isotropic bumps projected to a bandlimit
+# --------------------------------------------------------------------------
+
+def bump_coefficients(centres: np.ndarray, amps: np.ndarray, width: float,
+                      L: int, spin_raise: bool = False) -> np.ndarray:
+    """Coefficients of f(x) = sum_i A_i exp(-psi_i(x)^2 / (2 width^2)),
+    psi_i the geodesic angle from centre u_i, truncated to l < L.
+
+    Funk--Hecke: f_lm = sum_i A_i g_l conj(Y_lm(u_i)),
+    g_l = 2 pi int_{-1}^{1} exp(-arccos(t)^2/(2 width^2)) P_l(t) dt
+    (Gauss--Legendre, 400 nodes).  With spin_raise, returns the spin-1
+    coefficients sqrt(l(l+1)) f_lm of eth f.
+    centres: unit vectors [n, 3]; amps: [n, ...] (trailing dims kept).
+    Returns [L^2, ...].
+    """
+    from numpy.polynomial import legendre
+
+    centres = np.asarray(centres, dtype=np.float64)
+    amps = np.asarray(amps, dtype=np.float64)
+    t, wq = legendre.leggauss(400)
+    g = np.exp(-np.arccos(np.clip(t, -1.0, 1.0)) ** 2 / (2.0 * width ** 2))
+    gl = np.array([2.0 * np.pi * np.sum(wq * g * legendre.legval(t, [0] * l + [1]))
+                   for l in range(L)])
+    th = np.arccos(np.clip(centres[:, 2], -1.0, 1.0))
+    ph = np.arctan2(centres[:, 1], centres[:, 0])
+    out = np.zeros((L * L,) + amps.shape[1:], dtype=np.complex128)
+    for l in range(L):
+        fac = gl[l] * (math.sqrt(l * (l + 1.0)) if spin_raise else 1.0)
+        for m in range(-l, l + 1):
+            Yc = np.conj(spin_harmonic(0, l, m, th, ph))        # [n]
+            out[coef_index(l, m)] = fac * np.tensordot(Yc, amps, axes=(0, 0))
+    return out

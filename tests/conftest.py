@@ -1,0 +1,16 @@
+"""Shared pytest configuration.
+
+Markers: ``gpu`` — needs an MI355X and the built HIP library; every other
+test runs on the CPU.
+"""
+
+import os
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an AMD GPU (gfx950) and the built library")
