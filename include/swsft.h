@@ -1,0 +1,205 @@
+/*
+ * swsft.h — C ABI of the MI355X (gfx950) spectral spin-weighted spherical
+ * convolution library.
+ *
+ * The layer (Esteves, Slotine, Makadia, "Scaling Spherical CNNs", ICML 2023)
+ * is: forward spin-weighted spherical Fourier transform (Background, eq. (2)),
+ * per-degree mixing of spins and channels by filters shared across the order
+ * m (Background, "Spherical CNNs": convolution as products of spin-weighted
+ * harmonic coefficients; Fig. 2, "*K"), inverse transform (eq. (3)).  The
+ * phase-collapse nonlinearity of the Method section ("Phase collapse
+ * nonlinearity") is provided for stacking layers.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  Grid       H x W equiangular, H == W, H even: colatitude
+ *             theta_j = pi (2j+1) / (2H), longitude phi_k = 2 pi k / W.
+ *             Quadrature: Driscoll--Healy weights on that grid.
+ *  Bandlimit  degrees 0 <= l < L, 1 <= L <= H/2; orders |m| <= l.
+ *  Harmonics  sY_lm(theta, phi) = (-1)^s sqrt((2l+1)/(4 pi)) d^l_{m,-s}(theta)
+ *             e^{i m phi}, with d^1_{10}(b) = -sin(b)/sqrt(2).  This is the
+ *             convention in which the paper's eqs. (4) and (6) hold.
+ *  Complex    every complex array is interleaved (re, im) pairs of the plan's
+ *             storage type: float for SWSFT_F32, bfloat16 for SWSFT_BF16.
+ *  Layouts    (all C-contiguous, device memory)
+ *    spatial       x, y     [B][S][C][H][W]       complex
+ *    coefficients  coef     [L*L][B][S][C]        complex, row l*l + l + m;
+ *                  rows with l < |s| are written as 0 and ignored on input
+ *    filters       K        [L][S_out][C_out][S_in][C_in]   complex;
+ *                  output spin/channel first, like a dense-layer weight;
+ *                  entries with l < max(|s_in|, |s_out|) are ignored
+ *  S is the number of spins of the side concerned; spins are the plan's
+ *  spins_in (forward transform, conv input) or spins_out (inverse transform,
+ *  conv output, phase collapse), in the order given to swsft_plan_create.
+ *
+ * Ownership and streams
+ *  The plan owns its device tables (allocated by swsft_plan_create on the
+ *  current device, freed by swsft_plan_destroy).  The caller owns every
+ *  per-call buffer, including a workspace of at least swsft_workspace_bytes.
+ *  Calls never allocate, never synchronize and enqueue all work on `stream`
+ *  (a hipStream_t; NULL is the null stream) of the plan's device; results are
+ *  ready when the stream reaches them.  A plan is immutable after creation;
+ *  calls on different streams may run concurrently if their workspaces and
+ *  outputs are distinct.
+ *
+ * Errors
+ *  Every call validates its arguments on the host before enqueuing
+ *  anything; on SWSFT_E_INVALID / SWSFT_E_WORKSPACE / SWSFT_E_UNSUPPORTED
+ *  nothing was enqueued.  SWSFT_E_HIP reports a failed HIP call (text in
+ *  swsft_last_error()).  Nothing aborts and no C++ exception crosses the ABI.
+ */
+#ifndef SWSFT_H
+#define SWSFT_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct swsft_plan_s* swsft_plan;
+
+typedef enum {
+  SWSFT_OK = 0,
+  SWSFT_E_INVALID = 1,     /* bad argument; nothing enqueued                  */
+  SWSFT_E_UNSUPPORTED = 2, /* valid in the paper's terms, not implemented here */
+  SWSFT_E_ALLOC = 3,       /* device allocation failed in swsft_plan_create   */
+  SWSFT_E_HIP = 4,         /* a HIP call failed                               */
+  SWSFT_E_WORKSPACE = 5    /* workspace NULL or smaller than required         */
+} swsft_status;
+
+typedef enum {
+  SWSFT_F32 = 0,  /* float storage, float accumulation                   */
+  SWSFT_BF16 = 1  /* bfloat16 storage, float accumulation (MFMA bf16)    */
+} swsft_dtype;
+
+typedef enum {
+  SWSFT_OP_FORWARD = 0, /* swsft_forward          */
+  SWSFT_OP_INVERSE = 1, /* swsft_inverse          */
+  SWSFT_OP_CONV = 2     /* spin_sph_conv_forward  */
+} swsft_op;
+
+/*
+ * Create a plan for H x W grids with bandlimit L (Background, eqs. (2)-(3)).
+ *  H, W        grid size; H == W (the transform needs equal sample counts on
+ *              both axes, appendix "WeatherBench"), H even.  This build
+ *              implements W a power of two in [2, 512]; other even sizes
+ *              return SWSFT_E_UNSUPPORTED.
+ *  L           bandlimit, 1 <= L <= H/2 (L < H/2 is spectral pooling:
+ *              Method, "Spectral pooling").
+ *  spins_in    host array of n_spins_in distinct spins, |s| < L, 1..8 of them.
+ *  spins_out   host array of n_spins_out distinct spins, |s| < L, 1..8.
+ *  dtype       a swsft_dtype.
+ *  out         receives the plan (unchanged on error).
+ * Builds, on the current device, the Wigner-d tables of every spin in float64
+ * (recursion in l) rounded once to the storage type, and the DFT twiddles.
+ * Synchronizes the device before returning.
+ */
+swsft_status swsft_plan_create(int H, int W, int L, const int* spins_in, int n_spins_in,
+                               const int* spins_out, int n_spins_out, int dtype,
+                               swsft_plan* out);
+
+/* Free the plan's device tables.  NULL-safe.  The caller must make sure no
+ * enqueued call still uses the plan. */
+void swsft_plan_destroy(swsft_plan p);
+
+/* Workspace bytes needed by one call of `op` (a swsft_op) with batch B and
+ * channel counts C_in, C_out (C_out is ignored for SWSFT_OP_FORWARD, C_in
+ * for SWSFT_OP_INVERSE).  Returns 0 for invalid arguments. */
+size_t swsft_workspace_bytes(swsft_plan p, int op, int B, int C_in, int C_out);
+
+/*
+ * Forward transform, eq. (2), of every (b, s, c) map on spins_in:
+ *  coef[l*l+l+m][b][s][c] = int f conj(sY_lm) dx, by Driscoll--Healy
+ *  quadrature (exact for fields band-limited to l < L).
+ *  x     [B][S_in][C][H][W] complex, read only.
+ *  coef  [L*L][B][S_in][C] complex, written (rows l < |s| set to 0).
+ *  ws    workspace of ws_bytes >= swsft_workspace_bytes(p, SWSFT_OP_FORWARD, B, C, 0).
+ */
+swsft_status swsft_forward(swsft_plan p, int B, int C, const void* x, void* coef, void* ws,
+                           size_t ws_bytes, void* stream);
+
+/*
+ * Inverse transform, eq. (3), on spins_out:
+ *  y[b][s][c](theta_j, phi_k) = sum_{l>=|s|} sum_{|m|<=l} coef[l*l+l+m][b][s][c] sY_lm.
+ *  coef  [L*L][B][S_out][C] complex, read only (rows l < |s| ignored).
+ *  y     [B][S_out][C][H][W] complex, written.
+ *  ws    workspace of ws_bytes >= swsft_workspace_bytes(p, SWSFT_OP_INVERSE, B, 0, C).
+ */
+swsft_status swsft_inverse(swsft_plan p, int B, int C, const void* coef, void* y, void* ws,
+                           size_t ws_bytes, void* stream);
+
+/*
+ * The spectral spin-weighted spherical convolution layer (Background,
+ * "Spherical CNNs"; Fig. 2's FT -> *K -> IFT):
+ *  a  = forward(x)                                   on spins_in
+ *  a'[l*l+l+m][b][t][c'] = sum_{s: |s|<=l} sum_c K[l][t][c'][s][c] a[l*l+l+m][b][s][c]
+ *                          for |t| <= l (else 0)
+ *  y  = inverse(a')                                  on spins_out
+ *  x        [B][S_in][C_in][H][W] complex, read only.
+ *  filters  [L][S_out][C_out][S_in][C_in] complex, read only.
+ *  y        [B][S_out][C_out][H][W] complex, written; must not overlap x.
+ *  ws       workspace of ws_bytes >= swsft_workspace_bytes(p, SWSFT_OP_CONV, B, C_in, C_out).
+ */
+swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, const void* x,
+                                   const void* filters, void* y, void* ws, size_t ws_bytes,
+                                   void* stream);
+
+/*
+ * Phase-collapse nonlinearity (Method, "Phase collapse nonlinearity") on a
+ * spatial feature map with the plan's spins_out, which must contain spin 0:
+ * at every grid point, x0 <- W1 x0 + W2 |x| + b, where x0 are the C spin-0
+ * channels and |x| the moduli of all S_out*C channels stacked in (spin,
+ * channel) order; channels of other spins are passed through unchanged.
+ *  x     [B][S_out][C][H][W] complex (storage type), read only.
+ *  W1    [C][C] complex float (interleaved), row = output channel.
+ *  W2    [C][S_out*C] complex float, row = output channel.
+ *  bias  [C] complex float.
+ *  y     [B][S_out][C][H][W] complex, written; y == x (in place) is allowed,
+ *        any other overlap is not.
+ * Returns SWSFT_E_INVALID if spin 0 is not in spins_out.
+ */
+swsft_status spin_sph_phase_collapse(swsft_plan p, int B, int C, const void* x,
+                                     const void* W1, const void* W2, const void* bias,
+                                     void* y, void* stream);
+
+/* Static text for a status code. */
+const char* swsft_status_string(int status);
+
+/* Detail of the last non-OK status returned on this thread ("" if none). */
+const char* swsft_last_error(void);
+
+/*
+ * Stage timing for measurement.  When enabled on a plan, each kernel launch
+ * of the calls above is bracketed by HIP events recorded on the call's
+ * stream.  swsft_stage_times synchronizes those events, adds each stage's
+ * elapsed milliseconds and launch count into ms[i] and launches[i] for
+ * i < n (stage i is named by swsft_stage_name(i)), clears the record and
+ * returns the number of stages.  Disabled by default; enabling costs two
+ * event records per launch.  At most 4096 launches are recorded between
+ * reads; later ones are not timed.
+ */
+swsft_status swsft_stage_timing(swsft_plan p, int enable);
+int swsft_stage_times(swsft_plan p, double* ms, long long* launches, int n);
+const char* swsft_stage_name(int stage);
+
+/*
+ * Copy a plan table to host memory (synchronous; for tests).
+ *  which 0: forward table, [2L-1][L][Hp] per spins_in entry `spin_index`:
+ *           (2 pi / W) w_j (-1)^s sqrt((2l+1)/(4 pi)) d^l_{m,-s}(theta_j),
+ *           row (m + L - 1, l), zero for l < max(|m|, |s|), Hp = H rounded
+ *           up to a multiple of 8 (padding columns are 0).
+ *  which 1: inverse table, [2L-1][H][Lp] per spins_out entry:
+ *           (-1)^s sqrt((2l+1)/(4 pi)) d^l_{m,-s}(theta_j), Lp = L rounded
+ *           up to a multiple of 8.
+ *  Elements are of the plan's storage type.  `bytes` must equal the table
+ *  size; returns SWSFT_E_INVALID otherwise.
+ */
+swsft_status swsft_plan_table(swsft_plan p, int which, int spin_index, void* host_dst,
+                              size_t bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SWSFT_H */

@@ -1,0 +1,414 @@
+// C ABI: argument validation, plan ownership, workspace layout and the
+// sequence of kernel launches of each call.  Every call checks its
+// arguments on the host before it touches HIP; on an error nothing is
+// enqueued.
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+
+#include "swsft_internal.h"
+
+struct swsft_plan_s : swsft::Plan {};
+
+namespace {
+
+using swsft::Plan;
+
+thread_local char g_last_error[512] = "";
+
+swsft_status fail(swsft_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+swsft_status hip_fail(hipError_t e, const char* what) {
+  return fail(SWSFT_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool is_pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+swsft_status check_spins(const int* s, int n, int L, const char* which) {
+  if (s == nullptr) return fail(SWSFT_E_INVALID, "%s is NULL", which);
+  if (n < 1 || n > swsft::kMaxSpins)
+    return fail(SWSFT_E_INVALID, "%s: count %d not in [1, %d]", which, n, swsft::kMaxSpins);
+  for (int i = 0; i < n; ++i) {
+    if (s[i] <= -L || s[i] >= L)
+      return fail(SWSFT_E_INVALID, "%s[%d] = %d: need |s| < L = %d", which, i, s[i], L);
+    for (int j = 0; j < i; ++j)
+      if (s[j] == s[i]) return fail(SWSFT_E_INVALID, "%s: spin %d repeated", which, s[i]);
+  }
+  return SWSFT_OK;
+}
+
+// Batch and channel bounds keep every index computed in 32 bits inside the
+// kernels (n' = 2 B C, rows (2l+1) B, grid dimensions) in range.
+swsft_status check_bc(int B, int C, const char* cname) {
+  if (B < 1 || B > 65535) return fail(SWSFT_E_INVALID, "B = %d not in [1, 65535]", B);
+  if (C < 1 || C > (1 << 20)) return fail(SWSFT_E_INVALID, "%s = %d not in [1, 2^20]", cname, C);
+  if ((long long)B * C > (1LL << 26))
+    return fail(SWSFT_E_INVALID, "B * %s = %lld exceeds 2^26", cname, (long long)B * C);
+  return SWSFT_OK;
+}
+
+size_t ws_need(const Plan& p, int op, int B, int Cin, int Cout) {
+  const size_t e = p.elem;
+  switch (op) {
+    case SWSFT_OP_FORWARD:
+      return align_up(swsft::xy_elems(p, p.n_in, B, Cin) * e);
+    case SWSFT_OP_INVERSE:
+      return align_up(swsft::xy_elems(p, p.n_out, B, Cout) * e);
+    case SWSFT_OP_CONV: {
+      size_t xin = swsft::xy_elems(p, p.n_in, B, Cin), xout = swsft::xy_elems(p, p.n_out, B, Cout);
+      return align_up((xin > xout ? xin : xout) * e) +
+             align_up(swsft::coef_elems(p, p.n_in, B, Cin) * e) +
+             align_up(swsft::coef_elems(p, p.n_out, B, Cout) * e);
+    }
+    default:
+      return 0;
+  }
+}
+
+swsft_status check_ws(const Plan& p, int op, int B, int Cin, int Cout, const void* ws,
+                      size_t ws_bytes) {
+  const size_t need = ws_need(p, op, B, Cin, Cout);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(SWSFT_E_WORKSPACE, "workspace %s: %zu bytes given, %zu needed",
+                ws == nullptr ? "NULL" : "too small", ws == nullptr ? (size_t)0 : ws_bytes,
+                need);
+  if (reinterpret_cast<uintptr_t>(ws) % 16 != 0)
+    return fail(SWSFT_E_INVALID, "workspace must be 16-byte aligned");
+  return SWSFT_OK;
+}
+
+swsft_status check_ptr(const void* ptr, const char* name) {
+  if (ptr == nullptr) return fail(SWSFT_E_INVALID, "%s is NULL", name);
+  if (reinterpret_cast<uintptr_t>(ptr) % 16 != 0)
+    return fail(SWSFT_E_INVALID, "%s must be 16-byte aligned", name);
+  return SWSFT_OK;
+}
+
+swsft_status check_device(const Plan& p) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != p.device)
+    return fail(SWSFT_E_INVALID, "plan belongs to device %d, current device is %d", p.device, dev);
+  return SWSFT_OK;
+}
+
+// Launch one stage, bracketed by timing events when enabled.
+template <class F>
+swsft_status run_stage(Plan& p, int stage, hipStream_t st, const char* name, F&& launch) {
+  const bool timed = p.timing && p.ev != nullptr && p.n_timed < swsft::kMaxTimedLaunches;
+  if (timed) {
+    hipError_t e = hipEventRecord(p.ev[2 * p.n_timed], st);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+  }
+  hipError_t e = launch();
+  if (e != hipSuccess) return hip_fail(e, name);
+  if (timed) {
+    e = hipEventRecord(p.ev[2 * p.n_timed + 1], st);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    p.ev_stage[p.n_timed] = stage;
+    ++p.n_timed;
+  }
+  return SWSFT_OK;
+}
+
+#define SWSFT_TRY(expr)                  \
+  do {                                   \
+    swsft_status _st = (expr);           \
+    if (_st != SWSFT_OK) return _st;     \
+  } while (0)
+
+void free_plan(Plan* p) {
+  if (p == nullptr) return;
+  if (p->tab_fwd) (void)hipFree(p->tab_fwd);
+  if (p->tab_inv) (void)hipFree(p->tab_inv);
+  if (p->twiddle) (void)hipFree(p->twiddle);
+  if (p->ev) {
+    for (int i = 0; i < 2 * swsft::kMaxTimedLaunches; ++i)
+      if (p->ev[i]) (void)hipEventDestroy(p->ev[i]);
+    std::free(p->ev);
+  }
+  std::free(p->ev_stage);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* swsft_status_string(int status) {
+  switch (status) {
+    case SWSFT_OK: return "SWSFT_OK";
+    case SWSFT_E_INVALID: return "SWSFT_E_INVALID: invalid argument";
+    case SWSFT_E_UNSUPPORTED: return "SWSFT_E_UNSUPPORTED: not implemented for these sizes";
+    case SWSFT_E_ALLOC: return "SWSFT_E_ALLOC: device allocation failed";
+    case SWSFT_E_HIP: return "SWSFT_E_HIP: HIP call failed";
+    case SWSFT_E_WORKSPACE: return "SWSFT_E_WORKSPACE: workspace missing or too small";
+    default: return "unknown swsft status";
+  }
+}
+
+const char* swsft_last_error(void) { return g_last_error; }
+
+const char* swsft_stage_name(int stage) {
+  static const char* names[swsft::kNumStages] = {"dft_fwd", "lat_fwd", "mix", "lat_inv",
+                                                 "dft_inv", "phase_collapse", "tables"};
+  if (stage < 0 || stage >= swsft::kNumStages) return "";
+  return names[stage];
+}
+
+swsft_status swsft_plan_create(int H, int W, int L, const int* spins_in, int n_spins_in,
+                               const int* spins_out, int n_spins_out, int dtype,
+                               swsft_plan* out) {
+  g_last_error[0] = 0;
+  if (out == nullptr) return fail(SWSFT_E_INVALID, "out is NULL");
+  if (H != W) return fail(SWSFT_E_INVALID, "H = %d != W = %d (square grids only)", H, W);
+  if (H < 2 || H % 2) return fail(SWSFT_E_INVALID, "H = %d must be even and >= 2", H);
+  if (L < 1 || L > H / 2) return fail(SWSFT_E_INVALID, "L = %d not in [1, H/2 = %d]", L, H / 2);
+  if (dtype != SWSFT_F32 && dtype != SWSFT_BF16)
+    return fail(SWSFT_E_INVALID, "dtype %d is not a swsft_dtype", dtype);
+  SWSFT_TRY(check_spins(spins_in, n_spins_in, L, "spins_in"));
+  SWSFT_TRY(check_spins(spins_out, n_spins_out, L, "spins_out"));
+  if (!is_pow2(W) || W > 512)
+    return fail(SWSFT_E_UNSUPPORTED, "W = %d: this build implements powers of two up to 512", W);
+
+  Plan* p = new (std::nothrow) swsft_plan_s();
+  if (p == nullptr) return fail(SWSFT_E_ALLOC, "host allocation of the plan failed");
+  p->H = H;
+  p->W = W;
+  p->L = L;
+  p->Hp = swsft::round_up(H, 8);
+  p->Lp = swsft::round_up(L, 8);
+  p->M = 2 * L - 1;
+  p->n_in = n_spins_in;
+  p->n_out = n_spins_out;
+  for (int i = 0; i < n_spins_in; ++i) p->spins_in[i] = spins_in[i];
+  for (int i = 0; i < n_spins_out; ++i) p->spins_out[i] = spins_out[i];
+  p->dtype = dtype;
+  p->elem = dtype == SWSFT_BF16 ? 2 : 4;
+
+  hipError_t e = hipGetDevice(&p->device);
+  if (e != hipSuccess) {
+    free_plan(p);
+    delete static_cast<swsft_plan_s*>(p);
+    return hip_fail(e, "hipGetDevice");
+  }
+  const size_t fb = (size_t)p->n_in * p->fwd_table_elems() * p->elem;
+  const size_t ib = (size_t)p->n_out * p->inv_table_elems() * p->elem;
+  if (hipMalloc(&p->tab_fwd, fb) != hipSuccess || hipMalloc(&p->tab_inv, ib) != hipSuccess ||
+      hipMalloc((void**)&p->twiddle, (size_t)W * sizeof(float2)) != hipSuccess) {
+    (void)hipGetLastError();
+    free_plan(p);
+    delete static_cast<swsft_plan_s*>(p);
+    return fail(SWSFT_E_ALLOC, "hipMalloc of %zu + %zu table bytes failed", fb, ib);
+  }
+  // zero padding and the rows below max(|m|, |s|); the table kernel fills the rest
+  if ((e = hipMemset(p->tab_fwd, 0, fb)) != hipSuccess ||
+      (e = hipMemset(p->tab_inv, 0, ib)) != hipSuccess ||
+      (e = swsft::launch_tables(*p, nullptr)) != hipSuccess ||
+      (e = hipDeviceSynchronize()) != hipSuccess) {
+    free_plan(p);
+    delete static_cast<swsft_plan_s*>(p);
+    return hip_fail(e, "table generation");
+  }
+  *out = static_cast<swsft_plan_s*>(p);
+  return SWSFT_OK;
+}
+
+void swsft_plan_destroy(swsft_plan p) {
+  if (p == nullptr) return;
+  free_plan(p);
+  delete p;
+}
+
+size_t swsft_workspace_bytes(swsft_plan p, int op, int B, int C_in, int C_out) {
+  if (p == nullptr) return 0;
+  if (op == SWSFT_OP_FORWARD) C_out = 1;
+  if (op == SWSFT_OP_INVERSE) C_in = 1;
+  if (check_bc(B, C_in, "C_in") != SWSFT_OK || check_bc(B, C_out, "C_out") != SWSFT_OK) return 0;
+  return ws_need(*p, op, B, C_in, C_out);
+}
+
+swsft_status swsft_forward(swsft_plan p, int B, int C, const void* x, void* coef, void* ws,
+                           size_t ws_bytes, void* stream) {
+  g_last_error[0] = 0;
+  if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
+  SWSFT_TRY(check_bc(B, C, "C"));
+  SWSFT_TRY(check_ptr(x, "x"));
+  SWSFT_TRY(check_ptr(coef, "coef"));
+  SWSFT_TRY(check_ws(*p, SWSFT_OP_FORWARD, B, C, 1, ws, ws_bytes));
+  SWSFT_TRY(check_device(*p));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void* X = ws;
+  SWSFT_TRY(run_stage(*p, swsft::kStageDftFwd, st, "dft_fwd",
+                      [&] { return swsft::launch_dft_fwd(*p, p->n_in, B, C, x, X, st); }));
+  SWSFT_TRY(run_stage(*p, swsft::kStageLatFwd, st, "lat_fwd",
+                      [&] { return swsft::launch_lat_fwd(*p, B, C, X, coef, st); }));
+  return SWSFT_OK;
+}
+
+swsft_status swsft_inverse(swsft_plan p, int B, int C, const void* coef, void* y, void* ws,
+                           size_t ws_bytes, void* stream) {
+  g_last_error[0] = 0;
+  if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
+  SWSFT_TRY(check_bc(B, C, "C"));
+  SWSFT_TRY(check_ptr(coef, "coef"));
+  SWSFT_TRY(check_ptr(y, "y"));
+  SWSFT_TRY(check_ws(*p, SWSFT_OP_INVERSE, B, 1, C, ws, ws_bytes));
+  SWSFT_TRY(check_device(*p));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void* Y = ws;
+  SWSFT_TRY(run_stage(*p, swsft::kStageLatInv, st, "lat_inv",
+                      [&] { return swsft::launch_lat_inv(*p, B, C, coef, Y, st); }));
+  SWSFT_TRY(run_stage(*p, swsft::kStageDftInv, st, "dft_inv",
+                      [&] { return swsft::launch_dft_inv(*p, p->n_out, B, C, Y, y, st); }));
+  return SWSFT_OK;
+}
+
+swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, const void* x,
+                                   const void* filters, void* y, void* ws, size_t ws_bytes,
+                                   void* stream) {
+  g_last_error[0] = 0;
+  if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
+  SWSFT_TRY(check_bc(B, C_in, "C_in"));
+  SWSFT_TRY(check_bc(B, C_out, "C_out"));
+  SWSFT_TRY(check_ptr(x, "x"));
+  SWSFT_TRY(check_ptr(filters, "filters"));
+  SWSFT_TRY(check_ptr(y, "y"));
+  SWSFT_TRY(check_ws(*p, SWSFT_OP_CONV, B, C_in, C_out, ws, ws_bytes));
+  {
+    const char* xb = static_cast<const char*>(x);
+    const char* yb = static_cast<const char*>(y);
+    const size_t xs = (size_t)B * p->n_in * C_in * p->H * p->W * 2 * p->elem;
+    const size_t ys = (size_t)B * p->n_out * C_out * p->H * p->W * 2 * p->elem;
+    if (xb < yb + ys && yb < xb + xs) return fail(SWSFT_E_INVALID, "x and y overlap");
+  }
+  SWSFT_TRY(check_device(*p));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const size_t xin = swsft::xy_elems(*p, p->n_in, B, C_in);
+  const size_t xout = swsft::xy_elems(*p, p->n_out, B, C_out);
+  char* w = static_cast<char*>(ws);
+  void* XY = w;
+  w += align_up((xin > xout ? xin : xout) * p->elem);
+  void* coef = w;
+  w += align_up(swsft::coef_elems(*p, p->n_in, B, C_in) * p->elem);
+  void* coef2 = w;
+  SWSFT_TRY(run_stage(*p, swsft::kStageDftFwd, st, "dft_fwd",
+                      [&] { return swsft::launch_dft_fwd(*p, p->n_in, B, C_in, x, XY, st); }));
+  SWSFT_TRY(run_stage(*p, swsft::kStageLatFwd, st, "lat_fwd",
+                      [&] { return swsft::launch_lat_fwd(*p, B, C_in, XY, coef, st); }));
+  SWSFT_TRY(run_stage(*p, swsft::kStageMix, st, "mix", [&] {
+    return swsft::launch_mix(*p, B, C_in, C_out, coef, filters, coef2, st);
+  }));
+  SWSFT_TRY(run_stage(*p, swsft::kStageLatInv, st, "lat_inv",
+                      [&] { return swsft::launch_lat_inv(*p, B, C_out, coef2, XY, st); }));
+  SWSFT_TRY(run_stage(*p, swsft::kStageDftInv, st, "dft_inv", [&] {
+    return swsft::launch_dft_inv(*p, p->n_out, B, C_out, XY, y, st);
+  }));
+  return SWSFT_OK;
+}
+
+swsft_status spin_sph_phase_collapse(swsft_plan p, int B, int C, const void* x, const void* W1,
+                                     const void* W2, const void* bias, void* y, void* stream) {
+  g_last_error[0] = 0;
+  if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
+  SWSFT_TRY(check_bc(B, C, "C"));
+  SWSFT_TRY(check_ptr(x, "x"));
+  SWSFT_TRY(check_ptr(y, "y"));
+  if (W1 == nullptr || W2 == nullptr || bias == nullptr)
+    return fail(SWSFT_E_INVALID, "W1, W2 and bias must not be NULL");
+  if ((reinterpret_cast<uintptr_t>(W1) | reinterpret_cast<uintptr_t>(W2) |
+       reinterpret_cast<uintptr_t>(bias)) % 8 != 0)
+    return fail(SWSFT_E_INVALID, "W1, W2 and bias must be 8-byte aligned");
+  bool has0 = false;
+  for (int i = 0; i < p->n_out; ++i) has0 |= p->spins_out[i] == 0;
+  if (!has0) return fail(SWSFT_E_INVALID, "spins_out does not contain spin 0");
+  if (C > swsft::phase_collapse_max_channels(p->n_out))
+    return fail(SWSFT_E_UNSUPPORTED, "C = %d exceeds %d channels for %d spins", C,
+                swsft::phase_collapse_max_channels(p->n_out), p->n_out);
+  if (x != y) {
+    const char* xb = static_cast<const char*>(x);
+    const char* yb = static_cast<const char*>(y);
+    const size_t sz = (size_t)B * p->n_out * C * p->H * p->W * 2 * p->elem;
+    if (xb < yb + sz && yb < xb + sz)
+      return fail(SWSFT_E_INVALID, "x and y overlap without being equal");
+  }
+  SWSFT_TRY(check_device(*p));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return run_stage(*p, swsft::kStagePhaseCollapse, st, "phase_collapse", [&] {
+    return swsft::launch_phase_collapse(*p, B, C, x, static_cast<const float2*>(W1),
+                                        static_cast<const float2*>(W2),
+                                        static_cast<const float2*>(bias), y, st);
+  });
+}
+
+swsft_status swsft_stage_timing(swsft_plan p, int enable) {
+  g_last_error[0] = 0;
+  if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
+  if (enable && p->ev == nullptr) {
+    const int n = 2 * swsft::kMaxTimedLaunches;
+    p->ev = static_cast<hipEvent_t*>(std::calloc(n, sizeof(hipEvent_t)));
+    p->ev_stage = static_cast<int*>(std::calloc(swsft::kMaxTimedLaunches, sizeof(int)));
+    if (p->ev == nullptr || p->ev_stage == nullptr) return fail(SWSFT_E_ALLOC, "event pool");
+    for (int i = 0; i < n; ++i) {
+      hipError_t e = hipEventCreate(&p->ev[i]);
+      if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+    }
+  }
+  p->timing = enable != 0;
+  p->n_timed = 0;
+  return SWSFT_OK;
+}
+
+int swsft_stage_times(swsft_plan p, double* ms, long long* launches, int n) {
+  if (p == nullptr) return 0;
+  for (int i = 0; i < p->n_timed; ++i) {
+    const int s = p->ev_stage[i];
+    if (hipEventSynchronize(p->ev[2 * i + 1]) != hipSuccess) continue;
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, p->ev[2 * i], p->ev[2 * i + 1]) != hipSuccess) continue;
+    if (s < n) {
+      if (ms) ms[s] += t;
+      if (launches) launches[s] += 1;
+    }
+  }
+  p->n_timed = 0;
+  return swsft::kNumStages;
+}
+
+swsft_status swsft_plan_table(swsft_plan p, int which, int spin_index, void* host_dst,
+                              size_t bytes) {
+  g_last_error[0] = 0;
+  if (p == nullptr || host_dst == nullptr) return fail(SWSFT_E_INVALID, "NULL argument");
+  size_t elems;
+  const char* base;
+  if (which == 0) {
+    if (spin_index < 0 || spin_index >= p->n_in) return fail(SWSFT_E_INVALID, "spin index");
+    elems = p->fwd_table_elems();
+    base = static_cast<const char*>(p->tab_fwd) + spin_index * elems * p->elem;
+  } else if (which == 1) {
+    if (spin_index < 0 || spin_index >= p->n_out) return fail(SWSFT_E_INVALID, "spin index");
+    elems = p->inv_table_elems();
+    base = static_cast<const char*>(p->tab_inv) + spin_index * elems * p->elem;
+  } else {
+    return fail(SWSFT_E_INVALID, "which = %d", which);
+  }
+  if (bytes != elems * p->elem)
+    return fail(SWSFT_E_INVALID, "bytes = %zu, table has %zu", bytes, elems * p->elem);
+  SWSFT_TRY(check_device(*p));
+  hipError_t e = hipMemcpy(host_dst, base, bytes, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
+  return SWSFT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,87 @@
+// Internal declarations shared by the host API and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "../../include/swsft.h"
+
+namespace swsft {
+
+constexpr int kMaxSpins = 8;
+constexpr int kMaxTimedLaunches = 4096;
+
+enum Stage : int {
+  kStageDftFwd = 0,
+  kStageLatFwd = 1,
+  kStageMix = 2,
+  kStageLatInv = 3,
+  kStageDftInv = 4,
+  kStagePhaseCollapse = 5,
+  kStageTables = 6,
+  kNumStages = 7
+};
+
+inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+struct Plan {
+  int device = 0;
+  int H = 0, W = 0, L = 0;
+  int Hp = 0;  // H rounded up to a multiple of 8 (row pitch of tables, X and Y)
+  int Lp = 0;  // L rounded up to a multiple of 8 (row pitch of inverse tables)
+  int M = 0;   // number of orders, 2L - 1
+  int n_in = 0, n_out = 0;
+  int spins_in[kMaxSpins] = {0};
+  int spins_out[kMaxSpins] = {0};
+  int dtype = SWSFT_F32;
+  size_t elem = 4;  // bytes of one real of the storage type
+  // device tables
+  void* tab_fwd = nullptr;  // [n_in][M][L][Hp]
+  void* tab_inv = nullptr;  // [n_out][M][Hp][Lp]   (rows j < H used)
+  float2* twiddle = nullptr;  // [W]: exp(-2 pi i r / W)
+  // stage timing
+  bool timing = false;
+  int n_timed = 0;
+  hipEvent_t* ev = nullptr;  // 2 * kMaxTimedLaunches
+  int* ev_stage = nullptr;   // kMaxTimedLaunches
+
+  size_t fwd_table_elems() const { return (size_t)M * L * Hp; }
+  size_t inv_table_elems() const { return (size_t)M * Hp * Lp; }
+};
+
+// Sizes (in reals of the storage type) of the intermediate buffers.
+inline size_t xy_elems(const Plan& p, int S, int B, int C) {
+  return (size_t)S * p.M * (size_t)B * C * 2 * p.Hp;
+}
+inline size_t coef_elems(const Plan& p, int S, int B, int C) {
+  return (size_t)p.L * p.L * (size_t)B * S * C * 2;
+}
+
+// ---- kernel launchers (return hipGetLastError() of the launch) ----
+hipError_t launch_tables(const Plan& p, hipStream_t st);
+
+// x [B][S][C][H][W] -> X [S][M][B*C][2][Hp]
+hipError_t launch_dft_fwd(const Plan& p, int S, int B, int C, const void* x, void* X,
+                          hipStream_t st);
+// Y [S][M][B*C][2][Hp] -> y [B][S][C][H][W]
+hipError_t launch_dft_inv(const Plan& p, int S, int B, int C, const void* Y, void* y,
+                          hipStream_t st);
+// X (spins_in) -> coef [L^2][B][S_in][C]
+hipError_t launch_lat_fwd(const Plan& p, int B, int C, const void* X, void* coef,
+                          hipStream_t st);
+// coef' [L^2][B][S_out][C] -> Y (spins_out)
+hipError_t launch_lat_inv(const Plan& p, int B, int C, const void* coef, void* Y,
+                          hipStream_t st);
+// coef [L^2][B][S_in][C_in] x K -> coef' [L^2][B][S_out][C_out]
+hipError_t launch_mix(const Plan& p, int B, int C_in, int C_out, const void* coef,
+                      const void* K, void* coef_out, hipStream_t st);
+// Largest channel count the phase-collapse kernel stages in LDS for n_spins.
+int phase_collapse_max_channels(int n_spins);
+hipError_t launch_phase_collapse(const Plan& p, int B, int C, const void* x,
+                                 const float2* W1, const float2* W2, const float2* bias,
+                                 void* y, hipStream_t st);
+
+}  // namespace swsft

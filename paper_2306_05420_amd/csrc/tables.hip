@@ -1,0 +1,126 @@
+// Plan-time tables: Wigner-d / spin-weighted Legendre tables in float64,
+// rounded once to the storage type.
+//
+// Forward table  Tf[s][m][l][j] = (2 pi / W) w_j (-1)^s N_l d^l_{m,-s}(theta_j)
+// Inverse table  Ti[s][m][j][l] = (-1)^s N_l d^l_{m,-s}(theta_j)
+// with N_l = sqrt((2l+1)/(4 pi)), theta_j = pi (2j+1)/(2H), w_j the
+// Driscoll--Healy weights.  These are the latitude factors of the spin
+// harmonics of eqs. (2)-(3); the paper factors the same d^l(theta) through
+// Wigner Delta = d(pi/2) and a torus FFT (eqs. (4)-(6)), which we evaluate
+// directly instead.
+//
+// One thread per (spin, m, j) runs the three-term recurrence in l from the
+// single-term seed at l0 = max(|m|, |s|).
+#include "swsft_internal.h"
+
+namespace swsft {
+namespace {
+
+template <typename T>
+__device__ __forceinline__ T to_storage(double v);
+template <>
+__device__ __forceinline__ float to_storage<float>(double v) { return (float)v; }
+template <>
+__device__ __forceinline__ __bf16 to_storage<__bf16>(double v) {
+  // double -> float is exact enough here (|v| <= 1, relative 2^-24), then
+  // round-to-nearest-even to bfloat16.
+  return (__bf16)(float)v;
+}
+
+// d^{l0}_{m n}(theta) at l0 = max(|m|, |n|): sqrt(C(2 l0, a)) c^a s^b times a
+// sign, c = cos(theta/2), s = sin(theta/2), a + b = 2 l0.  Evaluated as a
+// running product so no factorial or power is formed on its own.
+__device__ double wigner_seed(int m, int n, double c, double s) {
+  const int am = m < 0 ? -m : m, an = n < 0 ? -n : n;
+  const int l0 = am > an ? am : an;
+  int a, b;
+  bool neg;
+  if (am >= an) {
+    if (m == l0) { a = l0 + n; b = l0 - n; neg = (b & 1); }   // d_{l,n}
+    else         { a = l0 - n; b = l0 + n; neg = false; }     // d_{-l,n}
+  } else {
+    if (n == l0) { a = l0 + m; b = l0 - m; neg = false; }     // d_{m,l}
+    else         { a = l0 - m; b = l0 + m; neg = (b & 1); }   // d_{m,-l}
+  }
+  double v = 1.0;
+  for (int i = 1; i <= a; ++i) v *= c * sqrt((double)(b + i) / (double)i);
+  for (int i = 0; i < b; ++i) v *= s;
+  return neg ? -v : v;
+}
+
+template <typename T>
+__global__ void tables_kernel(T* __restrict__ tab_fwd, T* __restrict__ tab_inv,
+                              const int* __restrict__ spins_dummy, int s, int si, bool fwd,
+                              int H, int W, int L, int Hp, int Lp) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  const int mi = blockIdx.y;
+  if (j >= H) return;
+  const int M = 2 * L - 1;
+  const int m = mi - (L - 1);
+  const int n = -s;
+  const int am = m < 0 ? -m : m, an = n < 0 ? -n : n;
+  const int l0 = am > an ? am : an;
+  if (l0 >= L) return;
+  const double pi = 3.14159265358979323846;
+  const double theta = pi * (2.0 * j + 1.0) / (2.0 * H);
+  const double c = cos(0.5 * theta), sn = sin(0.5 * theta), cb = cos(theta);
+  double scale = (s & 1) ? -1.0 : 1.0;
+  if (fwd) {
+    // Driscoll--Healy weight on the offset grid, times the longitude step
+    double acc = 0.0;
+    for (int p = 0; p < H / 2; ++p) acc += sin((2.0 * p + 1.0) * theta) / (2.0 * p + 1.0);
+    const double w = (4.0 / H) * sin(theta) * acc;
+    scale *= (2.0 * pi / W) * w;
+  }
+  double dprev = 0.0, dcur = wigner_seed(m, n, c, sn);
+  for (int l = l0; l < L; ++l) {
+    const double Nl = sqrt((2.0 * l + 1.0) / (4.0 * pi));
+    const double v = scale * Nl * dcur;
+    if (fwd) tab_fwd[(((size_t)si * M + mi) * L + l) * Hp + j] = to_storage<T>(v);
+    else     tab_inv[(((size_t)si * M + mi) * Hp + j) * Lp + l] = to_storage<T>(v);
+    if (l + 1 < L) {
+      const double lp = l + 1.0;
+      const double a = lp * (2.0 * l + 1.0) / sqrt((lp * lp - (double)m * m) * (lp * lp - (double)n * n));
+      const double t1 = (l == 0) ? cb * dcur : (cb - (double)m * n / (l * (l + 1.0))) * dcur;
+      const double t2 = (l > l0) ? sqrt(((double)l * l - (double)m * m) * ((double)l * l - (double)n * n)) /
+                                       (l * (2.0 * l + 1.0)) * dprev
+                                 : 0.0;
+      const double dn = a * (t1 - t2);
+      dprev = dcur;
+      dcur = dn;
+    }
+  }
+}
+
+__global__ void twiddle_kernel(float2* tw, int W) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= W) return;
+  // exp(-2 pi i r / W), phase reduced exactly: r < W
+  const double a = -2.0 * 3.14159265358979323846 * (double)r / (double)W;
+  tw[r] = make_float2((float)cos(a), (float)sin(a));
+}
+
+template <typename T>
+hipError_t launch_tables_t(const Plan& p, hipStream_t st) {
+  const int M = p.M;
+  dim3 block(64);
+  dim3 grid((p.H + 63) / 64, M);
+  for (int si = 0; si < p.n_in; ++si)
+    hipLaunchKernelGGL(tables_kernel<T>, grid, block, 0, st, (T*)p.tab_fwd, (T*)nullptr,
+                       (const int*)nullptr, p.spins_in[si], si, true, p.H, p.W, p.L, p.Hp, p.Lp);
+  for (int si = 0; si < p.n_out; ++si)
+    hipLaunchKernelGGL(tables_kernel<T>, grid, block, 0, st, (T*)nullptr, (T*)p.tab_inv,
+                       (const int*)nullptr, p.spins_out[si], si, false, p.H, p.W, p.L, p.Hp,
+                       p.Lp);
+  hipLaunchKernelGGL(twiddle_kernel, dim3((p.W + 63) / 64), dim3(64), 0, st, p.twiddle, p.W);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_tables(const Plan& p, hipStream_t st) {
+  if (p.dtype == SWSFT_BF16) return launch_tables_t<__bf16>(p, st);
+  return launch_tables_t<float>(p, st);
+}
+
+}  // namespace swsft

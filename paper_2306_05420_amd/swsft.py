@@ -1,0 +1,269 @@
+"""Thin Python binding of libswsft.so (the C ABI in include/swsft.h).
+
+Argument marshalling only: every step of the transform and the layer runs in
+the library's HIP kernels.  Torch tensors supply device memory and the
+current stream.  There is no fallback: if the library is not built, or is
+called without a GPU, this module raises.
+
+Tensor conventions (see include/swsft.h):
+  * f32 plans take complex64 tensors (or float32 with a trailing dim of 2);
+  * bf16 plans take bfloat16 tensors with a trailing dim of 2 (re, im);
+  * spatial [B, S, C, H, W], coefficients [L*L, B, S, C],
+    filters [L, S_out, C_out, S_in, C_in], phase-collapse weights complex64.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libswsft.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "swsft.h")
+
+OK, E_INVALID, E_UNSUPPORTED, E_ALLOC, E_HIP, E_WORKSPACE = range(6)
+F32, BF16 = 0, 1
+OP_FORWARD, OP_INVERSE, OP_CONV = 0, 1, 2
+STAGES = ("dft_fwd", "lat_fwd", "mix", "lat_inv", "dft_inv", "phase_collapse", "tables")
+
+_lib = None
+
+
+class SwsftError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} (status {status})")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load libswsft.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2306_05420_amd.build` (hipcc, gfx950)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    ip = ctypes.POINTER(ctypes.c_int)
+    sigs = {
+        "swsft_plan_create": (i, [i, i, i, ip, i, ip, i, i, ctypes.POINTER(vp)]),
+        "swsft_plan_destroy": (None, [vp]),
+        "swsft_workspace_bytes": (sz, [vp, i, i, i, i]),
+        "swsft_forward": (i, [vp, i, i, vp, vp, vp, sz, vp]),
+        "swsft_inverse": (i, [vp, i, i, vp, vp, vp, sz, vp]),
+        "spin_sph_conv_forward": (i, [vp, i, i, i, vp, vp, vp, vp, sz, vp]),
+        "spin_sph_phase_collapse": (i, [vp, i, i, vp, vp, vp, vp, vp, vp]),
+        "swsft_status_string": (ctypes.c_char_p, [i]),
+        "swsft_last_error": (ctypes.c_char_p, []),
+        "swsft_stage_timing": (i, [vp, i]),
+        "swsft_stage_times": (i, [vp, ctypes.POINTER(ctypes.c_double),
+                                  ctypes.POINTER(ctypes.c_longlong), i]),
+        "swsft_stage_name": (ctypes.c_char_p, [i]),
+        "swsft_plan_table": (i, [vp, i, i, vp, sz]),
+    }
+    for name, (res, args) in sigs.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def header_functions() -> list:
+    """Names of the functions declared in include/swsft.h."""
+    text = open(HEADER_PATH).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return re.findall(r"^[A-Za-z_][\w \*]*?\b(\w+)\s*\(", text, flags=re.M)
+
+
+def _check(status: int, what: str):
+    if status != OK:
+        L = lib()
+        detail = L.swsft_last_error().decode()
+        raise SwsftError(status, f"{what}: {L.swsft_status_string(status).decode()}: {detail}")
+
+
+def _stream_handle(stream) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+class Plan:
+    """A transform plan: grid H x W, bandlimit L, input/output spins, dtype.
+
+    Owns the device tables built by swsft_plan_create; workspaces are cached
+    per call shape (allocated through torch, i.e. by the caller of the C ABI).
+    """
+
+    def __init__(self, H: int, W: int, L: int, spins_in, spins_out, dtype: str = "f32"):
+        self.H, self.W, self.L = int(H), int(W), int(L)
+        self.spins_in = tuple(int(s) for s in spins_in)
+        self.spins_out = tuple(int(s) for s in spins_out)
+        if dtype not in ("f32", "bf16"):
+            raise ValueError("dtype must be 'f32' or 'bf16'")
+        self.dtype = dtype
+        self._code = F32 if dtype == "f32" else BF16
+        si = (ctypes.c_int * len(self.spins_in))(*self.spins_in)
+        so = (ctypes.c_int * len(self.spins_out))(*self.spins_out)
+        h = ctypes.c_void_p()
+        _check(lib().swsft_plan_create(self.H, self.W, self.L, si, len(self.spins_in), so,
+                                       len(self.spins_out), self._code, ctypes.byref(h)),
+               "swsft_plan_create")
+        self._h = h
+        self._ws = {}
+        self.device = torch.device("cuda", torch.cuda.current_device())
+
+    # -- lifetime --------------------------------------------------------
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            torch.cuda.synchronize(self.device)
+            lib().swsft_plan_destroy(self._h)
+            self._h = ctypes.c_void_p()
+        self._ws = {}
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- helpers ---------------------------------------------------------
+    def real_view(self, t: torch.Tensor) -> torch.Tensor:
+        """Validate a complex tensor of this plan's storage type and return
+        its real (..., 2) view."""
+        if not t.is_cuda:
+            raise ValueError("tensor must be on the GPU")
+        if self.dtype == "f32":
+            if t.dtype == torch.complex64:
+                t = torch.view_as_real(t)
+            elif t.dtype != torch.float32 or t.shape[-1] != 2:
+                raise ValueError(f"f32 plan needs complex64 tensors, got {t.dtype}")
+        else:
+            if t.dtype != torch.bfloat16 or t.shape[-1] != 2:
+                raise ValueError("bf16 plan needs bfloat16 tensors with a trailing dim of 2")
+        if not t.is_contiguous():
+            raise ValueError("tensor must be contiguous")
+        return t
+
+    def empty(self, *shape) -> torch.Tensor:
+        """An uninitialised complex tensor of this plan's storage type."""
+        if self.dtype == "f32":
+            return torch.empty(*shape, dtype=torch.complex64, device=self.device)
+        return torch.empty(*shape, 2, dtype=torch.bfloat16, device=self.device)
+
+    def _shape(self, t, want, name):
+        got = tuple(t.shape[:-1])
+        if got != tuple(want):
+            raise ValueError(f"{name}: shape {got}, expected {tuple(want)}")
+
+    def workspace_bytes(self, op: int, B: int, C_in: int, C_out: int) -> int:
+        return int(lib().swsft_workspace_bytes(self._h, op, B, C_in, C_out))
+
+    def workspace(self, op: int, B: int, C_in: int, C_out: int) -> torch.Tensor:
+        key = (op, B, C_in, C_out)
+        ws = self._ws.get(key)
+        if ws is None:
+            n = self.workspace_bytes(op, B, C_in, C_out)
+            if n == 0:
+                raise ValueError("invalid workspace request")
+            ws = torch.empty(n, dtype=torch.uint8, device=self.device)
+            self._ws[key] = ws
+        return ws
+
+    # -- the calls ---------------------------------------------------------
+    def forward(self, x: torch.Tensor, coef: torch.Tensor = None, stream=None) -> torch.Tensor:
+        """Forward transform, eq. (2): x [B, S_in, C, H, W] -> coef [L*L, B, S_in, C]."""
+        xr = self.real_view(x)
+        B, S, C = xr.shape[:3]
+        self._shape(xr, (B, len(self.spins_in), C, self.H, self.W), "x")
+        if coef is None:
+            coef = self.empty(self.L * self.L, B, S, C)
+        cr = self.real_view(coef)
+        self._shape(cr, (self.L * self.L, B, S, C), "coef")
+        ws = self.workspace(OP_FORWARD, B, C, 1)
+        _check(lib().swsft_forward(self._h, B, C, xr.data_ptr(), cr.data_ptr(), ws.data_ptr(),
+                                   ws.numel(), _stream_handle(stream)), "swsft_forward")
+        return coef
+
+    def inverse(self, coef: torch.Tensor, y: torch.Tensor = None, stream=None) -> torch.Tensor:
+        """Inverse transform, eq. (3): coef [L*L, B, S_out, C] -> y [B, S_out, C, H, W]."""
+        cr = self.real_view(coef)
+        _, B, S, C = cr.shape[:4]
+        self._shape(cr, (self.L * self.L, B, len(self.spins_out), C), "coef")
+        if y is None:
+            y = self.empty(B, S, C, self.H, self.W)
+        yr = self.real_view(y)
+        self._shape(yr, (B, S, C, self.H, self.W), "y")
+        ws = self.workspace(OP_INVERSE, B, 1, C)
+        _check(lib().swsft_inverse(self._h, B, C, cr.data_ptr(), yr.data_ptr(), ws.data_ptr(),
+                                   ws.numel(), _stream_handle(stream)), "swsft_inverse")
+        return y
+
+    def conv(self, x: torch.Tensor, filters: torch.Tensor, y: torch.Tensor = None,
+             stream=None) -> torch.Tensor:
+        """The layer: x [B, S_in, C_in, H, W], filters [L, S_out, C_out, S_in, C_in]
+        -> y [B, S_out, C_out, H, W]."""
+        xr = self.real_view(x)
+        B, S, Cin = xr.shape[:3]
+        self._shape(xr, (B, len(self.spins_in), Cin, self.H, self.W), "x")
+        kr = self.real_view(filters)
+        Cout = kr.shape[2]
+        self._shape(kr, (self.L, len(self.spins_out), Cout, len(self.spins_in), Cin), "filters")
+        if y is None:
+            y = self.empty(B, len(self.spins_out), Cout, self.H, self.W)
+        yr = self.real_view(y)
+        self._shape(yr, (B, len(self.spins_out), Cout, self.H, self.W), "y")
+        ws = self.workspace(OP_CONV, B, Cin, Cout)
+        _check(lib().spin_sph_conv_forward(self._h, B, Cin, Cout, xr.data_ptr(), kr.data_ptr(),
+                                           yr.data_ptr(), ws.data_ptr(), ws.numel(),
+                                           _stream_handle(stream)), "spin_sph_conv_forward")
+        return y
+
+    def phase_collapse(self, x: torch.Tensor, W1: torch.Tensor, W2: torch.Tensor,
+                       bias: torch.Tensor, y: torch.Tensor = None, stream=None) -> torch.Tensor:
+        """x0 <- W1 x0 + W2 |x| + b on spins_out (in place if y is x)."""
+        xr = self.real_view(x)
+        B, S, C = xr.shape[:3]
+        self._shape(xr, (B, len(self.spins_out), C, self.H, self.W), "x")
+        for t, shp, nm in ((W1, (C, C), "W1"), (W2, (C, S * C), "W2"), (bias, (C,), "bias")):
+            if t.dtype != torch.complex64 or not t.is_cuda or not t.is_contiguous():
+                raise ValueError(f"{nm} must be a contiguous complex64 GPU tensor")
+            if tuple(t.shape) != shp:
+                raise ValueError(f"{nm}: shape {tuple(t.shape)}, expected {shp}")
+        if y is None:
+            y = self.empty(*xr.shape[:-1])
+        yr = self.real_view(y)
+        self._shape(yr, tuple(xr.shape[:-1]), "y")
+        _check(lib().spin_sph_phase_collapse(self._h, B, C, xr.data_ptr(), W1.data_ptr(),
+                                             W2.data_ptr(), bias.data_ptr(), yr.data_ptr(),
+                                             _stream_handle(stream)), "spin_sph_phase_collapse")
+        return y
+
+    # -- tables and timing -------------------------------------------------
+    def table(self, which: int, spin_index: int) -> torch.Tensor:
+        """Copy of a plan table on the host (float32 or bfloat16 tensor):
+        which 0: [2L-1, L, Hp] forward; which 1: [2L-1, Hp, Lp] inverse."""
+        Hp = (self.H + 7) // 8 * 8
+        Lp = (self.L + 7) // 8 * 8
+        M = 2 * self.L - 1
+        shape = (M, self.L, Hp) if which == 0 else (M, Hp, Lp)
+        dt = torch.float32 if self.dtype == "f32" else torch.bfloat16
+        out = torch.empty(shape, dtype=dt)
+        _check(lib().swsft_plan_table(self._h, which, spin_index, out.data_ptr(),
+                                      out.numel() * out.element_size()), "swsft_plan_table")
+        return out
+
+    def stage_timing(self, enable: bool = True):
+        _check(lib().swsft_stage_timing(self._h, 1 if enable else 0), "swsft_stage_timing")
+
+    def stage_times(self) -> dict:
+        """{stage: (total ms, launches)} since the last read (synchronizes)."""
+        n = len(STAGES)
+        ms = (ctypes.c_double * n)()
+        cnt = (ctypes.c_longlong * n)()
+        lib().swsft_stage_times(self._h, ms, cnt, n)
+        return {STAGES[i]: (ms[i], cnt[i]) for i in range(n) if cnt[i]}

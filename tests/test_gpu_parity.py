@@ -1,0 +1,229 @@
+"""GPU parity: the HIP library against the float64 oracle.
+
+Every comparison is element by element on the same seeded inputs (inputs
+rounded to the storage type first, so the tolerance covers the GPU's own
+rounding only): relative L2 <= 1e-5 for float32 storage, <= 2e-2 for
+bfloat16 storage with float32 accumulation.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2306_05420_amd import swsft as S
+from paper_2306_05420_amd import synthetic as syn
+from helpers import TOL, from_device, rel_l2, round_to, to_device, workload_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    S.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _plan(w, dtype=None):
+    return S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_out, dtype or w.dtype)
+
+
+def _ref_table(plan, which, spin):
+    """Oracle value of the plan's forward / inverse table for one spin."""
+    H, W, L = plan.H, plan.W, plan.L
+    theta, _ = O.grid(H, W)
+    w = O.dh_weights(H)
+    Hp, Lp = (H + 7) // 8 * 8, (L + 7) // 8 * 8
+    M = 2 * L - 1
+    N = np.sqrt((2 * np.arange(L) + 1) / (4 * np.pi))
+    if which == 0:
+        ref = np.zeros((M, L, Hp))
+        for mi in range(M):
+            d = O.wigner_d(L, mi - (L - 1), -spin, theta)
+            ref[mi, :, :H] = (2 * np.pi / W) * w[None, :] * (-1.0) ** spin * N[:, None] * d
+    else:
+        ref = np.zeros((M, Hp, Lp))
+        for mi in range(M):
+            d = O.wigner_d(L, mi - (L - 1), -spin, theta)
+            ref[mi, :H, :L] = ((-1.0) ** spin * N[:, None] * d).T
+    return ref
+
+
+@pytest.mark.parametrize("name", ["tiny", "wx256"])
+def test_tables_match_oracle(name):
+    w = syn.workload(name)
+    plan = _plan(w)
+    eps = 2.0 ** -24 if w.dtype == "f32" else 2.0 ** -8   # half an ulp, relative
+    for which, spins in ((0, w.spins_in), (1, w.spins_out)):
+        for si, s in enumerate(spins):
+            got = plan.table(which, si).to(torch.float64).numpy()
+            ref = _ref_table(plan, which, s)
+            # one rounding of a float64 value, plus float64 differences
+            bound = 2 * eps * np.abs(ref) + 1e-14 * np.abs(ref).max()
+            assert np.all(np.abs(got - ref) <= bound), (name, which, s)
+            assert np.all(got[ref == 0] == 0)
+    plan.close()
+
+
+def _x_and_plan(name):
+    w = syn.workload(name)
+    x, K, d = workload_inputs(w)
+    return w, x, K, d, _plan(w)
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "mol", "wx128"])
+def test_forward_parity(name):
+    w, x, K, d, plan = _x_and_plan(name)
+    got = from_device(plan.forward(to_device(x, w.dtype)))
+    ref = O.forward(x, w.L, w.spins_in)
+    err = rel_l2(got, ref)
+    print(f"{name} forward rel-L2 {err:.3e}")
+    assert err <= TOL[w.dtype]
+    # rows that do not exist for spin s (l < |s|) are exactly zero
+    for si, s in enumerate(w.spins_in):
+        assert np.all(got[: abs(s) ** 2, :, si] == 0)
+    plan.close()
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "mol", "wx128"])
+def test_inverse_parity(name):
+    w = syn.workload(name)
+    rng = np.random.default_rng(w.seed + 77)
+    a = round_to(syn.random_coefficients(rng, w.L, w.B, w.spins_out, w.C_out, 1.0), w.dtype)
+    plan = _plan(w)
+    got = from_device(plan.inverse(to_device(a, w.dtype)))
+    ref = O.inverse(a, w.H, w.W, w.spins_out)
+    err = rel_l2(got, ref)
+    print(f"{name} inverse rel-L2 {err:.3e}")
+    assert err <= TOL[w.dtype]
+    plan.close()
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "mol", "wx128"])
+def test_conv_parity(name):
+    w, x, K, d, plan = _x_and_plan(name)
+    got = from_device(plan.conv(to_device(x, w.dtype), to_device(K, w.dtype)))
+    ref = O.conv(x, K, w.L, w.spins_in, w.spins_out)
+    err = rel_l2(got, ref)
+    print(f"{name} conv rel-L2 {err:.3e}")
+    assert err <= TOL[w.dtype]
+    plan.close()
+
+
+def test_two_layer_stack_with_phase_collapse():
+    """The molecule-shaped workload's two stacked layers: conv -> phase
+    collapse -> conv."""
+    w, x, K, d, plan = _x_and_plan("mol")
+    K2 = round_to(d["filters2"], w.dtype)
+    W1, W2, b = (np.asarray(t, dtype=np.complex64) for t in d["pc"])
+    plan2 = S.Plan(w.H, w.W, w.L, w.spins_out, w.spins_out, w.dtype)
+    y1 = plan.conv(to_device(x, w.dtype), to_device(K, w.dtype))
+    tW1, tW2, tb = (torch.from_numpy(t).cuda() for t in (W1, W2, b))
+    z = plan.phase_collapse(y1, tW1, tW2, tb)
+    y2 = plan2.conv(z, to_device(K2, w.dtype))
+    r1 = O.conv(x, K, w.L, w.spins_in, w.spins_out)
+    rz = O.phase_collapse(r1, w.spins_out, W1.astype(complex), W2.astype(complex),
+                          b.astype(complex))
+    r2 = O.conv(rz, K2, w.L, w.spins_out, w.spins_out)
+    for got, ref, tag in ((y1, r1, "layer1"), (z, rz, "phase collapse"), (y2, r2, "layer2")):
+        err = rel_l2(from_device(got), ref)
+        print(f"mol stack {tag} rel-L2 {err:.3e}")
+        assert err <= TOL[w.dtype], tag
+    plan.close()
+    plan2.close()
+
+
+def test_phase_collapse_in_place_and_passthrough():
+    w = syn.workload("mol")
+    rng = np.random.default_rng(5)
+    x = round_to(syn.complex_normal(rng, (3, 2, 5, w.H, w.W)), "f32")
+    W1, W2, b = (np.asarray(t, np.complex64) for t in syn.phase_collapse_parameters(rng, 2, 5))
+    plan = S.Plan(w.H, w.W, w.L, (0,), (1, 0), "f32")   # spin 0 second in the list
+    xd = to_device(x, "f32")
+    tW = [torch.from_numpy(t).cuda() for t in (W1, W2, b)]
+    y = from_device(plan.phase_collapse(xd, *tW))
+    ref = O.phase_collapse(x, (1, 0), W1.astype(complex), W2.astype(complex), b.astype(complex))
+    assert np.array_equal(y[:, 0], x[:, 0])              # spin 1 bit-identical
+    assert rel_l2(y, ref) <= 1e-6
+    plan.phase_collapse(xd, *tW, y=xd)                     # in place
+    assert np.array_equal(from_device(xd), y)
+    plan.close()
+
+
+EDGE = [
+    # H, L, spins_in, spins_out, B, C_in, C_out, dtype
+    (16, 5, (0,), (0,), 1, 1, 1, "f32"),            # L < H/2, one channel
+    (16, 8, (-1, 2, 0), (1, 0, -2), 3, 3, 5, "f32"),  # odd channel counts, |s| = 2
+    (2, 1, (0,), (0,), 2, 2, 3, "f32"),            # smallest grid
+    (4, 2, (0, 1), (1,), 1, 4, 2, "f32"),
+    (8, 4, (0,), (0, 1), 5, 7, 9, "bf16"),
+    (32, 16, (0, 1), (0, 1), 2, 40, 24, "bf16"),
+    (64, 32, (1,), (0, -1), 1, 33, 17, "f32"),     # ragged tiles everywhere
+    (64, 20, (0,), (0,), 3, 8, 8, "f32"),          # spectral truncation L << H/2
+]
+
+
+@pytest.mark.parametrize("case", EDGE, ids=[f"H{c[0]}L{c[1]}{c[7]}" for c in EDGE])
+def test_edge_cases(case):
+    H, L, si, so, B, Ci, Co, dt = case
+    rng = np.random.default_rng(H * 1000 + L)
+    a = syn.random_coefficients(rng, L, B, si, Ci, 0.5)
+    x = round_to(O.inverse(a, H, H, si), dt)
+    K = round_to(syn.random_filters(rng, L, si, Ci, so, Co, 1.0 / Ci), dt)
+    plan = S.Plan(H, H, L, si, so, dt)
+    xd = to_device(x, dt)
+    tol = TOL[dt]
+    err_f = rel_l2(from_device(plan.forward(xd)), O.forward(x, L, si))
+    ac = round_to(syn.random_coefficients(rng, L, B, so, Co, 0.5), dt)
+    err_i = rel_l2(from_device(plan.inverse(to_device(ac, dt))), O.inverse(ac, H, H, so))
+    err_c = rel_l2(from_device(plan.conv(xd, to_device(K, dt))), O.conv(x, K, L, si, so))
+    print(f"edge {case}: fwd {err_f:.2e} inv {err_i:.2e} conv {err_c:.2e}")
+    assert err_f <= tol and err_i <= tol and err_c <= tol
+    plan.close()
+
+
+def test_non_bandlimited_input_matches_oracle_operator():
+    """The transform is the quadrature operator itself, aliasing included."""
+    H, L = 32, 16
+    rng = np.random.default_rng(9)
+    x = round_to(syn.complex_normal(rng, (2, 2, 3, H, H)), "f32")
+    plan = S.Plan(H, H, L, (0, 1), (0, 1), "f32")
+    err = rel_l2(from_device(plan.forward(to_device(x, "f32"))), O.forward(x, L, (0, 1)))
+    assert err <= 1e-5
+    plan.close()
+
+
+def test_deterministic():
+    w, x, K, d, plan = _x_and_plan("small")
+    xd, Kd = to_device(x, w.dtype), to_device(K, w.dtype)
+    y1 = plan.conv(xd, Kd).clone()
+    y2 = plan.conv(xd, Kd)
+    assert torch.equal(y1, y2)
+    plan.close()
+
+
+def test_call_validation_with_plan():
+    w = syn.workload("tiny")
+    plan = _plan(w)
+    L = S.lib()
+    x = plan.empty(1, 1, 4, 16, 16)
+    c = plan.empty(64, 1, 1, 4)
+    need = plan.workspace_bytes(S.OP_FORWARD, 1, 4, 1)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    xp = torch.view_as_real(x).data_ptr()
+    cp = torch.view_as_real(c).data_ptr()
+    assert L.swsft_forward(plan._h, 1, 4, xp, cp, ws.data_ptr(), need - 1, None) == S.E_WORKSPACE
+    assert L.swsft_forward(plan._h, 1, 4, xp, cp, None, need, None) == S.E_WORKSPACE
+    assert L.swsft_forward(plan._h, 0, 4, xp, cp, ws.data_ptr(), need, None) == S.E_INVALID
+    assert L.swsft_forward(plan._h, 1, 4, xp + 4, cp, ws.data_ptr(), need, None) == S.E_INVALID
+    assert L.swsft_forward(plan._h, 1, 4, xp, cp, ws.data_ptr(), need, None) == S.OK
+    # phase collapse needs spin 0 among the output spins
+    p1 = S.Plan(16, 16, 8, (0,), (1,), "f32")
+    assert L.spin_sph_phase_collapse(p1._h, 1, 4, xp, xp, xp, xp, xp, None) == S.E_INVALID
+    torch.cuda.synchronize()
+    plan.close()
+    p1.close()
