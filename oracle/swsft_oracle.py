@@ -257,6 +257,8 @@ def forward(x: np.ndarray, L: int, spins) -> np.ndarray:
     E = _lon_dft_matrix(W, L, -1)
     # X[b, s, c, j, mi] = (2pi/W) sum_k x[b,s,c,j,k] e^{-i m phi_k}
     X = (2.0 * np.pi / W) * (x.reshape(-1, W) @ E).reshape(B, S, C, H, 2 * L - 1)
+    # the same numbers laid out [s, mi, j, (b, c)] so each (s, m) slice is contiguous
+    X = np.ascontiguousarray(X.transpose(1, 4, 3, 0, 2)).reshape(S, 2 * L - 1, H, B * C)
     coef = np.zeros((L * L, B, S, C), dtype=np.complex128)
     lvals = np.arange(L)
     for si, s in enumerate(spins):
@@ -266,9 +268,7 @@ def forward(x: np.ndarray, L: int, spins) -> np.ndarray:
                 continue
             d = wigner_d(L, m, -s, theta)  # [L, H]
             tab = ((-1.0) ** s) * _norm(lvals)[:, None] * d * w[None, :]
-            # [L, H] x [H, B*C]
-            Xm = X[:, si, :, :, mi].transpose(2, 0, 1).reshape(H, B * C)
-            a = (tab @ Xm).reshape(L, B, C)
+            a = (tab @ X[si, mi]).reshape(L, B, C)     # [L, H] x [H, B*C]
             for l in range(lo, L):
                 coef[coef_index(l, m), :, si, :] = a[l]
     return coef
@@ -311,7 +311,7 @@ def inverse(coef: np.ndarray, H: int, W: int, spins) -> np.ndarray:
     spins = list(spins)
     theta, _ = grid(H, W)
     lvals = np.arange(L)
-    G = np.zeros((B, S, C, H, 2 * L - 1), dtype=np.complex128)
+    G = np.zeros((S, 2 * L - 1, H, B * C), dtype=np.complex128)
     for si, s in enumerate(spins):
         for mi, m in enumerate(_orders(L)):
             lo = max(abs(m), abs(s))
@@ -319,12 +319,12 @@ def inverse(coef: np.ndarray, H: int, W: int, spins) -> np.ndarray:
                 continue
             d = wigner_d(L, m, -s, theta)
             tab = ((-1.0) ** s) * _norm(lvals)[:, None] * d  # [L, H]
-            a = np.zeros((L, B, C), dtype=np.complex128)
+            a = np.zeros((L, B * C), dtype=np.complex128)
             for l in range(lo, L):
-                a[l] = coef[coef_index(l, m), :, si, :]
-            # [H, L] x [L, B*C]
-            g = tab.T @ a.reshape(L, B * C)
-            G[:, si, :, :, mi] = g.reshape(H, B, C).transpose(1, 2, 0)
+                a[l] = coef[coef_index(l, m), :, si, :].reshape(B * C)
+            G[si, mi] = tab.T @ a                              # [H, L] x [L, B*C]
+    # [s, mi, j, (b, c)] -> [b, s, c, j, mi], then the longitude sum over m
+    G = np.ascontiguousarray(G.reshape(S, 2 * L - 1, H, B, C).transpose(3, 0, 4, 2, 1))
     E = _lon_dft_matrix(W, L, +1)  # [W, 2L-1]
     y = G.reshape(-1, 2 * L - 1) @ E.T
     return y.reshape(B, S, C, H, W)

@@ -143,3 +143,39 @@ def draw(w: Workload):
         out["filters2"] = random_filters(rng, w.L, w.spins_out, w.C_out,
                                          w.spins_out, w.C_out, w.filter_var)
     return out
+
+
+# ---------------------------------------------------------------------------
+# The same recipes drawn on the GPU with torch's seeded generator, for
+# benchmarks that only need inputs of the right shape and distribution (not
+# the exact values the float64 oracle sees in the parity tests).
+# ---------------------------------------------------------------------------
+
+def torch_complex_normal(gen, shape, var: float = 1.0, device="cuda"):
+    import torch
+
+    sd = (var / 2.0) ** 0.5
+    re = torch.randn(shape, generator=gen, device=device, dtype=torch.float32) * sd
+    im = torch.randn(shape, generator=gen, device=device, dtype=torch.float32) * sd
+    return torch.complex(re, im)
+
+
+def torch_random_coefficients(gen, L: int, B: int, spins, C: int, decay: float = 0.0,
+                              device="cuda"):
+    """Complex64 [L^2, B, S, C]: CN(0,1) (l+1)^-decay, zero where l < |s|."""
+    import torch
+
+    spins = list(spins)
+    a = torch_complex_normal(gen, (L * L, B, len(spins), C), 1.0, device)
+    l_of_row = torch.arange(L * L, device=device).float().sqrt().floor()
+    a *= ((l_of_row + 1.0) ** (-decay)).to(a.dtype)[:, None, None, None]
+    for si, s in enumerate(spins):
+        a[l_of_row < abs(s), :, si, :] = 0
+    return a
+
+
+def torch_random_filters(gen, L: int, spins_in, C_in: int, spins_out, C_out: int,
+                         var: float, device="cuda"):
+    """Complex64 filters [L, S_out, C_out, S_in, C_in], each entry CN(0, var)."""
+    return torch_complex_normal(gen, (L, len(spins_out), C_out, len(spins_in), C_in), var,
+                                device)

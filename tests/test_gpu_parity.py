@@ -227,3 +227,62 @@ def test_call_validation_with_plan():
     torch.cuda.synchronize()
     plan.close()
     p1.close()
+
+
+# ---------------------------------------------------------------------------
+# The 256 x 256, C = 256, bfloat16 workload at its full size, in the launch
+# configuration the benchmark times.  The oracle computes batch item 0 (all
+# 512 input maps) and a sample of output channels one by one.
+# ---------------------------------------------------------------------------
+
+@pytest.fixture(scope="module")
+def wx256():
+    w = syn.workload("wx256")
+    x, K, d = workload_inputs(w)
+    plan = _plan(w)
+    xd, Kd = to_device(x, "bf16"), to_device(K, "bf16")
+    yield w, x, K, d, plan, xd, Kd
+    plan.close()
+
+
+def test_wx256_forward_and_conv_sampled(wx256):
+    w, x, K, d, plan, xd, Kd = wx256
+    y = from_device(plan.conv(xd, Kd)[:1])
+    coef = from_device(plan.forward(xd)[:, :1])
+    a0 = O.forward(x[:1], w.L, w.spins_in)
+    err_f = rel_l2(coef, a0)
+    cs = [0, 1, 37, 128, 255]
+    yr = O.inverse(O.mix(a0, K[:, :, cs], w.spins_in, w.spins_out), w.H, w.W, w.spins_out)
+    err_c = rel_l2(y[:, :, cs], yr)
+    print(f"wx256 forward rel-L2 {err_f:.3e}, conv (sampled channels) rel-L2 {err_c:.3e}")
+    assert err_f <= TOL["bf16"] and err_c <= TOL["bf16"]
+
+
+def test_wx256_inverse_sampled(wx256):
+    w, x, K, d, plan, xd, Kd = wx256
+    rng = np.random.default_rng(4242)
+    a = round_to(syn.random_coefficients(rng, w.L, w.B, w.spins_out, w.C_out, 1.0), "bf16")
+    y = from_device(plan.inverse(to_device(a, "bf16"))[1:2, :, 100:104])
+    ref = O.inverse(np.ascontiguousarray(a[:, 1:2, :, 100:104]), w.H, w.W, w.spins_out)
+    err = rel_l2(y, ref)
+    print(f"wx256 inverse (sampled maps) rel-L2 {err:.3e}")
+    assert err <= TOL["bf16"]
+
+
+def test_wx256_properties_at_full_size(wx256):
+    """Round trip and exact longitude-shift equivariance on every map."""
+    w, x, K, d, plan, xd, Kd = wx256
+    coef = plan.forward(xd)
+    back = plan.inverse(coef)
+    xr = torch.view_as_complex(xd.float())
+    br = torch.view_as_complex(back.float())
+    err_rt = (torch.linalg.vector_norm(br - xr) / torch.linalg.vector_norm(xr)).item()
+    r = 37
+    c1 = torch.view_as_complex(coef.float())
+    c2 = torch.view_as_complex(plan.forward(torch.roll(xd, r, dims=4)).float())
+    m = torch.tensor([mm for l in range(w.L) for mm in range(-l, l + 1)], device="cuda")
+    ph = torch.exp(-2j * math.pi * m.double() * r / w.W).to(torch.complex64)
+    err_sh = (torch.linalg.vector_norm(c2 - c1 * ph[:, None, None, None])
+              / torch.linalg.vector_norm(c1)).item()
+    print(f"wx256 round trip {err_rt:.3e}, shift equivariance {err_sh:.3e}")
+    assert err_rt <= TOL["bf16"] and err_sh <= TOL["bf16"]
