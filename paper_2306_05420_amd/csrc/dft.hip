@@ -16,6 +16,7 @@
 // GEMM that reads it.
 #include "fft_reg.h"
 #include "swsft_internal.h"
+#include "xcd.h"
 
 namespace swsft {
 namespace {
@@ -45,26 +46,115 @@ struct CplxIO<__bf16> {
   }
 };
 
+// Row pitch (elements) of the [m][re/im][j] staging buffer: a multiple of
+// 16 bytes so whole 16-byte vectors move between LDS and HBM, and an odd
+// multiple of 16 bytes so consecutive orders start in different banks.
 template <typename T>
 constexpr int stage_pitch(int JB) {
-  return sizeof(T) == 4 ? 2 * JB + 1 : 2 * JB + 2;  // odd number of dwords
+  return sizeof(T) == 4 ? 2 * JB + 4 : 2 * JB + 8;
+}
+
+// Raw register image of one complex input sample (loaded before any compute).
+template <typename T>
+struct Raw;
+template <>
+struct Raw<float> {
+  using type = float2;
+  static __device__ __forceinline__ type load(const float* p, size_t i) {
+    return reinterpret_cast<const float2*>(p)[i];
+  }
+  static __device__ __forceinline__ float2 unpack(type v) { return v; }
+};
+template <>
+struct Raw<__bf16> {
+  using type = uint32_t;
+  static __device__ __forceinline__ type load(const __bf16* p, size_t i) {
+    return reinterpret_cast<const uint32_t*>(p)[i];
+  }
+  static __device__ __forceinline__ float2 unpack(type u) {
+    return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
+  }
+};
+
+constexpr int kMaxPasses = 2;
+
+// Move the [M][2][JB] spectrum block between the LDS stage (pitch SP) and
+// global memory at X[((mi * NBC + n) * 2 + ri) * Hp + j0 + r] (base already
+// offset to this spin), in 16-byte vectors when JB allows.
+template <typename T, bool kToGlobal>
+__device__ __forceinline__ void stage_copy(T* stage, T* gbase, int M, int JB, int SP,
+                                           size_t mstride, size_t nbase, int Hp, int tid,
+                                           int nthreads) {
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int BATCH = 8;  // global loads in flight per thread before their LDS stores
+  if (JB % VEC == 0) {
+    const int vpr = JB / VEC;
+    const int total = M * 2 * vpr;
+    for (int base = tid; base < total; base += BATCH * nthreads) {
+      uint4 buf[BATCH];
+#pragma unroll
+      for (int u = 0; u < BATCH; ++u) {
+        const int idx = base + u * nthreads;
+        // no per-lane branch around a load: out-of-range lanes read vector 0
+        const int id = idx < total ? idx : 0;
+        const int vi = id % vpr;
+        const int ri = (id / vpr) & 1;
+        const int mi = id / (2 * vpr);
+        uint4* s = reinterpret_cast<uint4*>(stage + (size_t)mi * SP + ri * JB + vi * VEC);
+        uint4* g = reinterpret_cast<uint4*>(gbase + mi * mstride + (nbase * 2 + ri) * Hp + vi * VEC);
+        if (kToGlobal) {
+          if (idx < total) *g = *s;
+        } else {
+          buf[u] = *g;
+        }
+      }
+      if (!kToGlobal) {
+#pragma unroll
+        for (int u = 0; u < BATCH; ++u) {
+          const int idx = base + u * nthreads;
+          if (idx < total) {
+            const int vi = idx % vpr;
+            const int ri = (idx / vpr) & 1;
+            const int mi = idx / (2 * vpr);
+            *reinterpret_cast<uint4*>(stage + (size_t)mi * SP + ri * JB + vi * VEC) = buf[u];
+          }
+        }
+      }
+    }
+  } else {
+    const int total = M * 2 * JB;
+    for (int idx = tid; idx < total; idx += nthreads) {
+      const int r = idx % JB;
+      const int ri = (idx / JB) & 1;
+      const int mi = idx / (2 * JB);
+      T* s = stage + (size_t)mi * SP + ri * JB + r;
+      T* g = gbase + mi * mstride + (nbase * 2 + ri) * Hp + r;
+      if (kToGlobal) *g = *s;
+      else *s = *g;
+    }
+  }
 }
 
 template <typename Tin, typename Tout, int W1, int W2>
 __global__ void __launch_bounds__(256) dft_fwd_kernel(const Tin* __restrict__ x,
                                                       Tout* __restrict__ X,
                                                       const float2* __restrict__ tw, int S,
-                                                      int C, int NBC, int H, int Hp, int L,
-                                                      int JB) {
+                                                      int C, int NB, int NBC, int H, int Hp,
+                                                      int L, int JB) {
   constexpr int W = W1 * W2;
   extern __shared__ __align__(16) unsigned char smem[];
   const int RPP = blockDim.x / W1;
+  const int NP = JB / RPP;  // passes, <= kMaxPasses
   const int tid = threadIdx.x;
   const int t = tid % W1;
   const int rr = tid / W1;
   const int nJB = H / JB;
-  const int map = blockIdx.x / nJB;
-  const int j0 = (blockIdx.x % nJB) * JB;
+  // consecutive row blocks of a map (which share the 128-byte lines of the
+  // transposed spectrum) are numbered together, so they run on one XCD
+  const int lb = xcd_logical_block();
+  if (lb >= S * C * NB * nJB) return;
+  const int map = lb / nJB;
+  const int j0 = (lb % nJB) * JB;
   const int c = map % C;
   const int si = (map / C) % S;
   const int b = map / (C * S);
@@ -74,16 +164,28 @@ __global__ void __launch_bounds__(256) dft_fwd_kernel(const Tin* __restrict__ x,
   float2* ex = reinterpret_cast<float2*>(smem);  // [RPP][W2][W1+1]
   Tout* stage = reinterpret_cast<Tout*>(ex + (size_t)RPP * W2 * (W1 + 1));  // [M][SP]
 
+  // every load of the block's JB rows is issued before any arithmetic
   const size_t row_base = ((size_t)map * H + j0) * W;  // complex index of row j0
-  for (int r0 = 0; r0 < JB; r0 += RPP) {
-    const int r = r0 + rr;
+  typename Raw<Tin>::type raw[kMaxPasses][W2];
+#pragma unroll
+  for (int p = 0; p < kMaxPasses; ++p)
+    if (p < NP) {
+#pragma unroll
+      for (int q = 0; q < W2; ++q)
+        raw[p][q] = Raw<Tin>::load(x, row_base + (size_t)(p * RPP + rr) * W + t + W1 * q);
+    }
+  float2* exr = ex + (size_t)rr * W2 * (W1 + 1);
+#pragma unroll
+  for (int p = 0; p < kMaxPasses; ++p) {
+    if (p >= NP) break;
+    const int r = p * RPP + rr;
     float2 v[W2];
 #pragma unroll
-    for (int q = 0; q < W2; ++q) v[q] = CplxIO<Tin>::load(x, row_base + (size_t)r * W + t + W1 * q);
+    for (int q = 0; q < W2; ++q) v[q] = Raw<Tin>::unpack(raw[p][q]);
     fft_reg<W2, -1>(v);
 #pragma unroll
-    for (int k2 = 1; k2 < W2; ++k2) v[k2] = cmul(v[k2], tw[(t * k2) % W]);
-    float2* exr = ex + (size_t)rr * W2 * (W1 + 1);
+    for (int k2 = 1; k2 < W2; ++k2) v[k2] = cmul(v[k2], tw[t * k2]);
+    if (p > 0) __syncthreads();  // the previous pass has finished reading ex
 #pragma unroll
     for (int k2 = 0; k2 < W2; ++k2) exr[k2 * (W1 + 1) + t] = v[k2];
     __syncthreads();
@@ -105,33 +207,33 @@ __global__ void __launch_bounds__(256) dft_fwd_kernel(const Tin* __restrict__ x,
         }
       }
     }
-    __syncthreads();
   }
-  // X[si][mi][n][ri][j0 + r], r fastest
-  const int total = M * 2 * JB;
-  for (int idx = tid; idx < total; idx += blockDim.x) {
-    const int r = idx % JB;
-    const int ri = (idx / JB) & 1;
-    const int mi = idx / (2 * JB);
-    X[((((size_t)si * M + mi) * NBC + n) * 2 + ri) * Hp + j0 + r] = stage[(size_t)mi * SP + ri * JB + r];
-  }
+  __syncthreads();
+  // X[si][mi][n][ri][j0 + r]
+  stage_copy<Tout, true>(stage, X + (size_t)si * M * NBC * 2 * Hp + j0, M, JB, SP,
+                         (size_t)NBC * 2 * Hp, n, Hp, tid, blockDim.x);
 }
 
 template <typename Tin, typename Tout, int W1, int W2>
 __global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
                                                       Tout* __restrict__ y,
                                                       const float2* __restrict__ tw, int S,
-                                                      int C, int NBC, int H, int Hp, int L,
-                                                      int JB) {
+                                                      int C, int NB, int NBC, int H, int Hp,
+                                                      int L, int JB) {
   constexpr int W = W1 * W2;
   extern __shared__ __align__(16) unsigned char smem[];
   const int RPP = blockDim.x / W1;
+  const int NP = JB / RPP;
   const int tid = threadIdx.x;
   const int t = tid % W1;
   const int rr = tid / W1;
   const int nJB = H / JB;
-  const int map = blockIdx.x / nJB;
-  const int j0 = (blockIdx.x % nJB) * JB;
+  // consecutive row blocks of a map (which share the 128-byte lines of the
+  // transposed spectrum) are numbered together, so they run on one XCD
+  const int lb = xcd_logical_block();
+  if (lb >= S * C * NB * nJB) return;
+  const int map = lb / nJB;
+  const int j0 = (lb % nJB) * JB;
   const int c = map % C;
   const int si = (map / C) % S;
   const int b = map / (C * S);
@@ -141,18 +243,16 @@ __global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
   float2* ex = reinterpret_cast<float2*>(smem);
   Tin* stage = reinterpret_cast<Tin*>(ex + (size_t)RPP * W2 * (W1 + 1));
 
-  const int total = M * 2 * JB;
-  for (int idx = tid; idx < total; idx += blockDim.x) {
-    const int r = idx % JB;
-    const int ri = (idx / JB) & 1;
-    const int mi = idx / (2 * JB);
-    stage[(size_t)mi * SP + ri * JB + r] = Y[((((size_t)si * M + mi) * NBC + n) * 2 + ri) * Hp + j0 + r];
-  }
+  stage_copy<Tin, false>(stage, const_cast<Tin*>(Y) + (size_t)si * M * NBC * 2 * Hp + j0, M, JB,
+                         SP, (size_t)NBC * 2 * Hp, n, Hp, tid, blockDim.x);
   __syncthreads();
 
   const size_t row_base = ((size_t)map * H + j0) * W;
-  for (int r0 = 0; r0 < JB; r0 += RPP) {
-    const int r = r0 + rr;
+  float2* exr = ex + (size_t)rr * W2 * (W1 + 1);
+#pragma unroll
+  for (int p = 0; p < kMaxPasses; ++p) {
+    if (p >= NP) break;
+    const int r = p * RPP + rr;
     float2 v[W2];
 #pragma unroll
     for (int q = 0; q < W2; ++q) {
@@ -167,9 +267,8 @@ __global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
     }
     fft_reg<W2, +1>(v);
 #pragma unroll
-    for (int k2 = 1; k2 < W2; ++k2) v[k2] = cmulc(v[k2], tw[(t * k2) % W]);
-    float2* exr = ex + (size_t)rr * W2 * (W1 + 1);
-    // the previous pass's readers of ex are done: the barrier below orders them
+    for (int k2 = 1; k2 < W2; ++k2) v[k2] = cmulc(v[k2], tw[t * k2]);
+    if (p > 0) __syncthreads();  // the previous pass has finished reading ex
 #pragma unroll
     for (int k2 = 0; k2 < W2; ++k2) exr[k2 * (W1 + 1) + t] = v[k2];
     __syncthreads();
@@ -184,26 +283,26 @@ __global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
       for (int k1 = 0; k1 < W1; ++k1)
         CplxIO<Tout>::store(y, row_base + (size_t)r * W + k2 + W2 * k1, u[k1]);
     }
-    __syncthreads();
   }
 }
 
-// Rows per workgroup: 32 (64-byte bf16 / 128-byte f32 store runs) unless the
-// exchange + staging LDS would exceed 80 KiB (two workgroups per CU), then 16.
+// Rows per workgroup JB = NP * RPP: RPP rows are transformed at a time by
+// 256 / W1 threads (fewer for small grids), NP <= 2 passes.  JB = 32 gives
+// 64-byte (bf16) / 128-byte (f32) runs per order in the transposed layout.
 template <typename Ts, int W1, int W2>
 void dft_geometry(const Plan& p, int* JB, int* nthreads, size_t* lds) {
-  for (int jb = p.H < 32 ? p.H : 32;; jb /= 2) {
-    const int nt = jb * W1 < 256 ? jb * W1 : 256;
-    const int rpp = nt / W1;
-    const size_t l = (size_t)rpp * W2 * (W1 + 1) * sizeof(float2) +
-                     (size_t)p.M * stage_pitch<Ts>(jb) * sizeof(Ts);
-    if (l <= 80 * 1024 || jb <= 16 || jb <= rpp) {
-      *JB = jb;
-      *nthreads = nt;
-      *lds = l;
-      return;
-    }
-  }
+  int rpp = 256 / W1;
+  if (rpp > p.H) rpp = p.H;
+  int jb = rpp;
+  if (jb < 32 && 2 * jb <= p.H) jb *= 2;  // a second pass when rows allow
+  auto bytes = [&](int j) {
+    return (size_t)rpp * W2 * (W1 + 1) * sizeof(float2) +
+           (size_t)p.M * stage_pitch<Ts>(j) * sizeof(Ts);
+  };
+  if (bytes(jb) > 160 * 1024) jb = rpp;  // one pass if two do not fit the CU's LDS
+  *JB = jb;
+  *nthreads = rpp * W1;
+  *lds = bytes(jb);
 }
 
 template <typename Tin, typename Tout, int W1, int W2>
@@ -219,8 +318,8 @@ hipError_t launch_fwd_shape(const Plan& p, int S, int B, int C, const void* x, v
     if (e != hipSuccess) return e;
   }
   const long long blocks = (long long)B * S * C * (p.H / JB);
-  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(nthreads), lds, st, (const Tin*)x,
-                     (Tout*)X, p.twiddle, S, C, B * C, p.H, p.Hp, p.L, JB);
+  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(nthreads), lds, st, (const Tin*)x,
+                     (Tout*)X, p.twiddle, S, C, B, B * C, p.H, p.Hp, p.L, JB);
   return hipGetLastError();
 }
 
@@ -237,8 +336,8 @@ hipError_t launch_inv_shape(const Plan& p, int S, int B, int C, const void* Y, v
     if (e != hipSuccess) return e;
   }
   const long long blocks = (long long)B * S * C * (p.H / JB);
-  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(nthreads), lds, st, (const Tin*)Y,
-                     (Tout*)y, p.twiddle, S, C, B * C, p.H, p.Hp, p.L, JB);
+  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(nthreads), lds, st, (const Tin*)Y,
+                     (Tout*)y, p.twiddle, S, C, B, B * C, p.H, p.Hp, p.L, JB);
   return hipGetLastError();
 }
 

@@ -5,8 +5,8 @@
 //     real GEMM: rows l in [|m|, L), columns n' = 2n + re/im, K = j.
 //  mix      (per-degree products with filters shared across m), per l:
 //     coef'[l][(m,b)][(t,c')] = sum_(s,c) coef[l][(m,b)][(s,c)] K[l][(t,c')][(s,c)]
-//     complex GEMM written as a real GEMM with K doubled: the filter tile is
-//     expanded in LDS into 2x2 real blocks [[re, -im], [im, re]].
+//     complex GEMM written as a real GEMM with K doubled: each filter row is
+//     expanded in LDS into the two real rows (re, -im, ...) and (im, re, ...).
 //  lat_inv  (eq. (3), latitude sum), per (spin t, order m):
 //     Y[t][m][n'][j] = sum_l coef'[l*l+l+m][b][t][c'][re/im] Ti[t][m][j][l]
 //     real GEMM: rows n', columns j, K = l in [max(|m|,|t|), L).
@@ -15,13 +15,17 @@
 // intermediates are laid out so that their global rows already are, the
 // mixing filters are stored output-major for the same reason, and only the
 // coefficient operand of lat_inv is transposed on its way into LDS.
+//
+// Main loop: two LDS buffers and one barrier per K step; the global loads
+// of step k+2 are in flight while step k is multiplied.  Epilogue: the
+// accumulator tile goes through LDS so that results leave in 16-byte rows.
 #include "mfma_tile.h"
 #include "swsft_internal.h"
+#include "xcd.h"
 
 namespace swsft {
 namespace {
 
-constexpr int BK = 32;
 constexpr int NT = 256;
 
 struct SpinList {
@@ -30,77 +34,355 @@ struct SpinList {
 
 __device__ __forceinline__ int iabs(int v) { return v < 0 ? -v : v; }
 
+template <typename T>
+struct Vec16 {
+  static constexpr int N = 16 / sizeof(T);
+  union {
+    uint4 u;
+    T e[N];
+  };
+};
+
+// LDS bytes of one operand stage and of the epilogue tile.
+template <typename T, int BM, int BN, int BK>
+struct GemmLds {
+  static constexpr int LD = BK + LdsPad<T>::value;
+  static constexpr int LDC = BN + (sizeof(T) == 4 ? 4 : 8);
+  static constexpr size_t stage = (size_t)(BM + BN) * LD * sizeof(T);
+  static constexpr size_t mainloop = 2 * stage;
+  static constexpr size_t epilogue = (size_t)BM * LDC * sizeof(T);
+  static constexpr size_t bytes = mainloop > epilogue ? mainloop : epilogue;
+};
+
+// Double-buffered main loop over nk K-tiles.  la / lb: load(kt) issues the
+// global reads of K-tile kt into registers, store(lds) writes them to LDS.
+template <typename T, int BM, int BN, int BK, int WM, int WN, class LA, class LB>
+__device__ __forceinline__ void mainloop(MfmaTile<T, BM, BN, BK, WM, WN>& tile, LA& la, LB& lb,
+                                         T* smem, int nk, int wm, int wn, int lane) {
+  using G = GemmLds<T, BM, BN, BK>;
+  constexpr int kStage = (BM + BN) * G::LD;  // elements per buffer (A then B)
+  la.load(0);
+  lb.load(0);
+  la.store(smem);
+  lb.store(smem + BM * G::LD);
+  if (nk > 1) {
+    la.load(1);
+    lb.load(1);
+  }
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    T* cur = smem + (kt & 1) * kStage;
+    T* nxt = smem + ((kt & 1) ^ 1) * kStage;
+    if (kt + 1 < nk) {
+      la.store(nxt);
+      lb.store(nxt + BM * G::LD);
+      if (kt + 2 < nk) {
+        la.load(kt + 2);
+        lb.load(kt + 2);
+      }
+    }
+    tile.compute(cur, cur + BM * G::LD, wm, wn, lane);
+    __syncthreads();
+  }
+}
+
+// Epilogue: accumulators -> LDS tile [BM][LDC] of T -> `out(row, col, vec,
+// n)` with up to VEC consecutive columns per call (n valid values).
+template <typename T, int BM, int BN, int BK, int WM, int WN, class Out>
+__device__ __forceinline__ void epilogue(const MfmaTile<T, BM, BN, BK, WM, WN>& tile, T* smem,
+                                         int rows, int cols, int wm, int wn, int lane, int tid,
+                                         Out&& out) {
+  using G = GemmLds<T, BM, BN, BK>;
+  constexpr int VEC = 16 / sizeof(T);
+  tile.for_each(wm, wn, lane,
+                [&](int row, int col, float v) { smem[row * G::LDC + col] = (T)v; });
+  __syncthreads();
+  constexpr int VPR = BN / VEC;
+  for (int idx = tid; idx < BM * VPR; idx += NT) {
+    const int row = idx / VPR;
+    const int col = (idx % VPR) * VEC;
+    if (row >= rows || col >= cols) continue;
+    Vec16<T> v;
+    v.u = *reinterpret_cast<const uint4*>(&smem[row * G::LDC + col]);
+    out(row, col, v, cols - col < VEC ? cols - col : VEC);
+  }
+}
+
+// K-contiguous operand tile of R rows from global rows given by row_ptr(r)
+// (nullptr = zero row); columns >= K are zero.  kVec: 16-byte loads (rows
+// 16-byte aligned, K a multiple of the vector); else element loads.  The
+// choice is a template flag: as a runtime branch the compiler merges both
+// paths into element loads.
+//
+// Loads are never inside a per-lane branch: out-of-range lanes read a
+// clamped valid address and the zero mask is applied when the registers are
+// written to LDS, so the loads of a K step stay in flight together (a
+// divergent if/else writing the same registers would force a wait on each).
+template <typename T, int R, int BK, bool kVec>
+struct RowLoader {
+  static constexpr int VEC = 16 / sizeof(T);
+  static constexpr int VPR = BK / VEC;
+  static constexpr int NV = R * VPR;
+  static constexpr int PER = (NV + NT - 1) / NT;
+  static constexpr int LD = BK + LdsPad<T>::value;
+  Vec16<T> reg[PER];
+  const T* rows_[PER];
+  bool rowok_[PER];
+  unsigned ok_[PER];  // bit e: element e of reg[p] is in range
+  int kv_[PER];
+  int k_base, K;
+
+  template <class RowPtr>
+  __device__ __forceinline__ void init(RowPtr&& row_ptr, const T* fallback, int k_base_, int K_,
+                                       int tid) {
+    k_base = k_base_;
+    K = K_;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int v = tid + p * NT;
+      const T* r = (NV % NT == 0 || v < NV) ? row_ptr(v / VPR) : nullptr;
+      rowok_[p] = r != nullptr;
+      rows_[p] = r != nullptr ? r : fallback;
+      kv_[p] = (v % VPR) * VEC;
+    }
+  }
+  __device__ __forceinline__ void load(int kt) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int k = k_base + kt * BK + kv_[p];
+      if constexpr (kVec) {
+        const bool ok = rowok_[p] && k < K;
+        reg[p].u = *reinterpret_cast<const uint4*>(rows_[p] + (ok ? k : 0));
+        ok_[p] = ok ? 0xffu : 0u;
+      } else {
+        unsigned bits = 0;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const bool ok = rowok_[p] && k + e < K;
+          reg[p].e[e] = rows_[p][ok ? k + e : 0];
+          bits |= (ok ? 1u : 0u) << e;
+        }
+        ok_[p] = bits;
+      }
+    }
+  }
+  __device__ __forceinline__ void store(T* lds) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int v = tid + p * NT;
+      if (NV % NT != 0 && v >= NV) break;
+      const int r = v / VPR;
+      if constexpr (kVec) {
+        if (!ok_[p]) reg[p].u = make_uint4(0, 0, 0, 0);
+      } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+          if (!((ok_[p] >> e) & 1u)) reg[p].e[e] = (T)0.f;
+      }
+      if constexpr (sizeof(T) == 4) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) lds[r * LD + kv_[p] + e] = reg[p].e[e];
+      } else {
+        *reinterpret_cast<uint4*>(&lds[r * LD + kv_[p]]) = reg[p].u;
+      }
+    }
+  }
+};
+
 // --------------------------------------------------------------------------
-template <typename T, int BM, int BN, int WM, int WN>
+// lat_fwd
+// --------------------------------------------------------------------------
+template <typename T, int BM, int BN, int BK, int WM, int WN, bool kVec>
 __global__ void __launch_bounds__(NT) lat_fwd_kernel(const T* __restrict__ X,
                                                      const T* __restrict__ tab,
                                                      T* __restrict__ coef, int L, int H, int Hp,
-                                                     int B, int C, int S, int n_row_tiles) {
+                                                     int B, int C, int S, int n_row_tiles,
+                                                     int n_tiles_n) {
   using Tile = MfmaTile<T, BM, BN, BK, WM, WN>;
-  __shared__ __align__(16) T As[BM * Tile::LD];
-  __shared__ __align__(16) T Bs[BN * Tile::LD];
+  using G = GemmLds<T, BM, BN, BK>;
+  __shared__ __align__(16) T smem[G::bytes / sizeof(T)];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int M = 2 * L - 1;
-  const int mi = blockIdx.y, si = blockIdx.z;
+  // logical block = ((s, order, row tile), column tile): the column tiles of
+  // one (s, m, row tile) share its table tile and run on one XCD
+  int lbk = xcd_logical_block();
+  if (lbk >= S * M * n_row_tiles * n_tiles_n) return;
+  const int nt = lbk % n_tiles_n;
+  lbk /= n_tiles_n;
+  const int rt = lbk % n_row_tiles;
+  lbk /= n_row_tiles;
+  const int mi = mixed_order(lbk % M, L), si = lbk / M;
   const int m = mi - (L - 1);
-  const int rt = blockIdx.x % n_row_tiles, nt = blockIdx.x / n_row_tiles;
   const int l_begin = iabs(m) + rt * BM;
   if (l_begin >= L) return;
   const int Np = 2 * B * C;
   const int n0 = nt * BN;
   const T* A0 = tab + (size_t)(si * M + mi) * L * Hp;
   const T* B0 = X + (size_t)(si * M + mi) * Np * Hp;
-  auto arow = [&](int r) -> const T* {
-    const int l = l_begin + r;
-    return l < L ? A0 + (size_t)l * Hp : nullptr;
-  };
-  auto brow = [&](int r) -> const T* {
-    const int np = n0 + r;
-    return np < Np ? B0 + (size_t)np * Hp : nullptr;
-  };
+  RowLoader<T, BM, BK, kVec> la;
+  RowLoader<T, BN, BK, kVec> lb;
+  la.init([&](int r) -> const T* { const int l = l_begin + r; return l < L ? A0 + (size_t)l * Hp : nullptr; },
+          A0 + (size_t)l_begin * Hp, 0, H, tid);
+  lb.init([&](int r) -> const T* { const int np = n0 + r; return np < Np ? B0 + (size_t)np * Hp : nullptr; },
+          B0 + (size_t)n0 * Hp, 0, H, tid);
   Tile tile;
   tile.zero();
-  KTileLoader<T, BM, BK, NT> la;
-  KTileLoader<T, BN, BK, NT> lb;
-  la.load(arow, 0, H, tid, true);
-  lb.load(brow, 0, H, tid, true);
-  for (int k0 = 0; k0 < H; k0 += BK) {
-    __syncthreads();
-    la.store(As, tid);
-    lb.store(Bs, tid);
-    __syncthreads();
-    if (k0 + BK < H) {
-      la.load(arow, k0 + BK, H, tid, true);
-      lb.load(brow, k0 + BK, H, tid, true);
-    }
-    tile.compute(As, Bs, wm, wn, lane);
-  }
+  mainloop(tile, la, lb, smem, (H + BK - 1) / BK, wm, wn, lane);
   const int twoC = 2 * C;
-  tile.for_each(wm, wn, lane, [&](int row, int col, float v) {
-    const int l = l_begin + row;
-    const int np = n0 + col;
-    if (l < L && np < Np) {
-      const int b = np / twoC;
-      const int rem = np - b * twoC;
-      coef[(((size_t)(l * l + l + m) * B + b) * S + si) * twoC + rem] = (T)v;
-    }
-  });
+  epilogue(tile, smem, L - l_begin, Np - n0, wm, wn, lane, tid,
+           [&](int row, int col, const Vec16<T>& v, int n) {
+             const int l = l_begin + row;
+             const size_t rowbase = ((size_t)(l * l + l + m) * B) * S * twoC;
+             const int np = n0 + col;
+             if (kVec && n == Vec16<T>::N) {
+               const int b = np / twoC, rem = np - b * twoC;
+               *reinterpret_cast<uint4*>(&coef[rowbase + ((size_t)b * S + si) * twoC + rem]) = v.u;
+             } else {
+#pragma unroll
+               for (int e = 0; e < Vec16<T>::N; ++e) {
+                 if (e >= n) break;
+                 const int b = (np + e) / twoC, rem = np + e - b * twoC;
+                 coef[rowbase + ((size_t)b * S + si) * twoC + rem] = v.e[e];
+               }
+             }
+           });
 }
 
 // --------------------------------------------------------------------------
-template <typename T, int BM, int BN, int WM, int WN>
+// mix
+// --------------------------------------------------------------------------
+// Filter operand: BN/2 complex filter rows q (output (t, c')) become the BN
+// real rows (2q: re, -im pairs; 2q+1: im, re pairs) of the real GEMM.
+// Input spins that do not exist at degree l are zeroed: per K tile when a
+// tile lies inside one spin's channel block, else per element.
+template <typename T, int BN, int BK, bool kVec>
+struct FilterLoader {
+  static constexpr int VEC = 16 / sizeof(T);   // reals per vector
+  static constexpr int VPR = BK / VEC;
+  static constexpr int NV = (BN / 2) * VPR;
+  static constexpr int PER = (NV + NT - 1) / NT;
+  static constexpr int LD = BK + LdsPad<T>::value;
+  Vec16<T> reg[PER];
+  const T* rows_[PER];
+  bool rowok_[PER];
+  unsigned ok_[PER];
+  int kv_[PER];
+  int Kp, Cin, l;
+  bool tile_spin;
+  unsigned dead_;  // bit si: input spin si does not exist at degree l
+
+  __device__ __forceinline__ void init(const T* K0, int n0, int Nc, int Kp_, int Cin_, int Cout,
+                                       int l_, const SpinList& sin, const SpinList& sout,
+                                       int tid) {
+    Kp = Kp_;
+    Cin = Cin_;
+    l = l_;
+    tile_spin = ((2 * Cin) % BK) == 0;
+    dead_ = 0;
+    for (int i = 0; i < kMaxSpins; ++i)
+      if (i * Cin < Kp / 2 && iabs(sin.s[i]) > l) dead_ |= 1u << i;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int v = tid + p * NT;
+      const int q = n0 / 2 + v / VPR;
+      const bool ok = (NV % NT == 0 || v < NV) && q < Nc && iabs(sout.s[q < Nc ? q / Cout : 0]) <= l;
+      rowok_[p] = ok;
+      rows_[p] = ok ? K0 + (size_t)q * Kp : K0;
+      kv_[p] = (v % VPR) * VEC;
+    }
+  }
+  __device__ __forceinline__ void load(int kt) {
+    // tile-uniform spin test (scalar)
+    const bool tile_dead = tile_spin && ((dead_ >> ((kt * BK) / (2 * Cin))) & 1u);
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int k = kt * BK + kv_[p];
+      unsigned bits;
+      if constexpr (kVec) {
+        const bool ok = rowok_[p] && k < Kp;
+        reg[p].u = *reinterpret_cast<const uint4*>(rows_[p] + (ok ? k : 0));
+        bits = ok ? 0xffu : 0u;
+      } else {
+        bits = 0;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const bool ok = rowok_[p] && k + e < Kp;
+          reg[p].e[e] = rows_[p][ok ? k + e : 0];
+          bits |= (ok ? 1u : 0u) << e;
+        }
+      }
+      if (tile_spin) {
+        if (tile_dead) bits = 0;
+      } else {
+#pragma unroll
+        for (int e = 0; e < VEC; e += 2) {
+          const int pc = (k + e) >> 1;
+          if (pc < Kp / 2 && ((dead_ >> (pc / Cin)) & 1u)) bits &= ~(3u << e);
+        }
+      }
+      ok_[p] = bits;
+    }
+  }
+  __device__ __forceinline__ void store(T* lds) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int v = tid + p * NT;
+      if (NV % NT != 0 && v >= NV) break;
+      const int r = v / VPR;
+      if (ok_[p] == 0) {
+        reg[p].u = make_uint4(0, 0, 0, 0);
+      } else if (ok_[p] != 0xffu) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+          if (!((ok_[p] >> e) & 1u)) reg[p].e[e] = (T)0.f;
+      }
+      T* re_row = lds + (2 * r) * LD + kv_[p];
+      T* im_row = lds + (2 * r + 1) * LD + kv_[p];
+      if constexpr (sizeof(T) == 2) {
+        // packed (re, im) bf16 pairs: (re, -im) flips the sign bit of the high
+        // half, (im, re) swaps the halves
+        const uint4 a = reg[p].u;
+        const uint4 neg = make_uint4(a.x ^ 0x80000000u, a.y ^ 0x80000000u, a.z ^ 0x80000000u,
+                                     a.w ^ 0x80000000u);
+        const uint4 bsw = make_uint4((a.x >> 16) | (a.x << 16), (a.y >> 16) | (a.y << 16),
+                                     (a.z >> 16) | (a.z << 16), (a.w >> 16) | (a.w << 16));
+        *reinterpret_cast<uint4*>(re_row) = neg;
+        *reinterpret_cast<uint4*>(im_row) = bsw;
+      } else {
+#pragma unroll
+        for (int e = 0; e < VEC; e += 2) {
+          const T kr = reg[p].e[e], ki = reg[p].e[e + 1];
+          re_row[e] = kr;
+          re_row[e + 1] = -ki;
+          im_row[e] = ki;
+          im_row[e + 1] = kr;
+        }
+      }
+    }
+  }
+};
+
+template <typename T, int BM, int BN, int BK, int WM, int WN, bool kVec>
 __global__ void __launch_bounds__(NT) mix_kernel(const T* __restrict__ coef,
                                                  const T* __restrict__ K, T* __restrict__ out,
                                                  int L, int B, int Cin, int Cout, int Sin,
                                                  int Sout, SpinList sin_, SpinList sout_) {
   using Tile = MfmaTile<T, BM, BN, BK, WM, WN>;
-  __shared__ __align__(16) T As[BM * Tile::LD];
-  __shared__ __align__(16) T Bs[BN * Tile::LD];
+  using G = GemmLds<T, BM, BN, BK>;
+  __shared__ __align__(16) T smem[G::bytes / sizeof(T)];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  // work item -> (l, row tile); the largest degrees come first
-  int t = blockIdx.x;
+  // logical block = ((l, row tile), column tile), largest degrees first: all
+  // tiles of one degree (its filter block and coefficient rows) are numbered
+  // together and run on one XCD
+  const int Np_ = 2 * Sout * Cout;
+  const int n_tiles_n = (Np_ + BN - 1) / BN;
+  int lbk = xcd_logical_block();
+  const int ntile = lbk % n_tiles_n;
+  int t = lbk / n_tiles_n;
   int l = L - 1;
   for (; l >= 0; --l) {
     const int ntl = ((2 * l + 1) * B + BM - 1) / BM;
@@ -112,199 +394,178 @@ __global__ void __launch_bounds__(NT) mix_kernel(const T* __restrict__ coef,
   const int row0 = t * BM;
   const int Kc = Sin * Cin, Nc = Sout * Cout;  // complex sizes
   const int Kp = 2 * Kc, Np = 2 * Nc;          // real sizes
-  const int n0 = blockIdx.y * BN;
+  const int n0 = ntile * BN;
   const T* A0 = coef + (size_t)l * l * B * Kp;
   const T* K0 = K + (size_t)l * Nc * Kc * 2;
-  const bool avec = (Kp % (16 / (int)sizeof(T))) == 0;
-  auto arow = [&](int r) -> const T* {
-    const int i = row0 + r;
-    return i < Mrows ? A0 + (size_t)i * Kp : nullptr;
-  };
+  RowLoader<T, BM, BK, kVec> la;
+  la.init([&](int r) -> const T* { const int i = row0 + r; return i < Mrows ? A0 + (size_t)i * Kp : nullptr; },
+          A0 + (size_t)row0 * Kp, 0, Kp, tid);
+  FilterLoader<T, BN, BK, kVec> lb;
+  lb.init(K0, n0, Nc, Kp, Cin, Cout, l, sin_, sout_, tid);
   Tile tile;
   tile.zero();
-  KTileLoader<T, BM, BK, NT> la;
-
-  // filter operand: BN/2 complex rows x BK/2 complex columns per tile
-  constexpr int VEC = 16 / sizeof(T);      // reals per 16-byte vector
-  constexpr int VPR = BK / VEC;            // vectors per complex row of the tile
-  constexpr int NVB = (BN / 2) * VPR;
-  constexpr int PERB = (NVB + NT - 1) / NT;
-  union Vec {
-    uint4 u;
-    T e[VEC];
-  };
-  Vec breg[PERB];
-  const bool bvec = (Kp % VEC) == 0;
-  auto load_b = [&](int k0) {
+  mainloop(tile, la, lb, smem, (Kp + BK - 1) / BK, wm, wn, lane);
+  T* O0 = out + ((size_t)l * l * B + row0) * Np + n0;
+  epilogue(tile, smem, Mrows - row0, Np - n0, wm, wn, lane, tid,
+           [&](int row, int col, const Vec16<T>& v, int n) {
+             T* dst = O0 + (size_t)row * Np + col;
+             if (kVec && n == Vec16<T>::N) {
+               *reinterpret_cast<uint4*>(dst) = v.u;
+             } else {
 #pragma unroll
-    for (int p = 0; p < PERB; ++p) {
-      const int v = tid + p * NT;
-      if (NVB % NT != 0 && v >= NVB) break;
-      const int r = v / VPR;           // complex row within tile
-      const int kv = (v % VPR) * VEC;  // real column within tile
-      const int q = n0 / 2 + r;        // complex output index (t, c')
-      const int k = k0 + kv;           // real input index (s, c, re/im)
-      const bool qok = q < Nc && iabs(sout_.s[q < Nc ? q / Cout : 0]) <= l;
-      const T* src = K0 + (size_t)q * Kp;
-      if (qok && bvec && k + VEC <= Kp) {
-        breg[p].u = *reinterpret_cast<const uint4*>(src + k);
-      } else {
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) breg[p].e[e] = (qok && k + e < Kp) ? src[k + e] : (T)0.f;
-      }
-      // input spins that do not exist at this degree take no part
-#pragma unroll
-      for (int e = 0; e < VEC; e += 2) {
-        const int pc = (k + e) >> 1;
-        if (pc < Kc && iabs(sin_.s[pc / Cin]) > l) {
-          breg[p].e[e] = (T)0.f;
-          breg[p].e[e + 1] = (T)0.f;
-        }
-      }
-    }
-  };
-  auto store_b = [&]() {
-#pragma unroll
-    for (int p = 0; p < PERB; ++p) {
-      const int v = tid + p * NT;
-      if (NVB % NT != 0 && v >= NVB) break;
-      const int r = v / VPR;
-      const int kv = (v % VPR) * VEC;
-      T* re_row = Bs + (2 * r) * Tile::LD + kv;      // output real part
-      T* im_row = Bs + (2 * r + 1) * Tile::LD + kv;  // output imaginary part
-#pragma unroll
-      for (int e = 0; e < VEC; e += 2) {
-        const T kr = breg[p].e[e], ki = breg[p].e[e + 1];
-        re_row[e] = kr;
-        re_row[e + 1] = -ki;
-        im_row[e] = ki;
-        im_row[e + 1] = kr;
-      }
-    }
-  };
-
-  la.load(arow, 0, Kp, tid, avec);
-  load_b(0);
-  for (int k0 = 0; k0 < Kp; k0 += BK) {
-    __syncthreads();
-    la.store(As, tid);
-    store_b();
-    __syncthreads();
-    if (k0 + BK < Kp) {
-      la.load(arow, k0 + BK, Kp, tid, avec);
-      load_b(k0 + BK);
-    }
-    tile.compute(As, Bs, wm, wn, lane);
-  }
-  T* O0 = out + (size_t)l * l * B * Np;
-  tile.for_each(wm, wn, lane, [&](int row, int col, float v) {
-    const int i = row0 + row;
-    const int np = n0 + col;
-    if (i < Mrows && np < Np) O0[(size_t)i * Np + np] = (T)v;
-  });
+               for (int e = 0; e < Vec16<T>::N; ++e)
+                 if (e < n) dst[e] = v.e[e];
+             }
+           });
 }
 
 // --------------------------------------------------------------------------
-template <typename T, int BM, int BN, int WM, int WN>
+// lat_inv
+// --------------------------------------------------------------------------
+// Coefficient operand transposed into LDS: each thread reads 16-byte runs
+// of consecutive n' for two consecutive degrees and writes degree pairs;
+// consecutive lanes take consecutive degree pairs of the same n' run, so the
+// pair writes of a wave fall in distinct banks.  Loads use clamped
+// addresses; the zero mask is applied at the LDS store.
+template <typename T, int BM, int BK, bool kVec>
+struct CoefTLoader {
+  static constexpr int VEC = 16 / sizeof(T);
+  static constexpr int NV = (BK / 2) * (BM / VEC);
+  static constexpr int PER = (NV + NT - 1) / NT;
+  static constexpr int LD = BK + LdsPad<T>::value;
+  Vec16<T> reg[PER][2];
+  unsigned ok_[PER][2];
+  const T* coef;
+  int m, B, S, si, twoC, Np, n0, lo, L, k_base;
+
+  __device__ __forceinline__ size_t offset(int l, int n2) const {
+    const int b = n2 / twoC, rem = n2 - b * twoC;
+    return ((size_t)(l * l + l + m) * B + b) * S * twoC + (size_t)si * twoC + rem;
+  }
+  __device__ __forceinline__ void load(int kt) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int v = tid + p * NT;
+      const int kl = 2 * (v % (BK / 2));
+      const int np = n0 + (v / (BK / 2)) * VEC;
+      const bool vok = NV % NT == 0 || v < NV;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int l = k_base + kt * BK + kl + h;
+        const bool lok = vok && l >= lo && l < L;
+        if constexpr (kVec) {
+          const bool ok = lok && np < Np;
+          reg[p][h].u = *reinterpret_cast<const uint4*>(coef + (ok ? offset(l, np) : 0));
+          ok_[p][h] = ok ? 0xffu : 0u;
+        } else {
+          unsigned bits = 0;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            const bool ok = lok && np + e < Np;
+            reg[p][h].e[e] = coef[ok ? offset(l, np + e) : 0];
+            bits |= (ok ? 1u : 0u) << e;
+          }
+          ok_[p][h] = bits;
+        }
+      }
+    }
+  }
+  __device__ __forceinline__ void store(T* lds) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int v = tid + p * NT;
+      if (NV % NT != 0 && v >= NV) break;
+      const int kl = 2 * (v % (BK / 2));
+      const int nv = (v / (BK / 2)) * VEC;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        if (ok_[p][h] == 0) {
+          reg[p][h].u = make_uint4(0, 0, 0, 0);
+        } else if (ok_[p][h] != 0xffu) {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e)
+            if (!((ok_[p][h] >> e) & 1u)) reg[p][h].e[e] = (T)0.f;
+        }
+      }
+      if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const uint32_t lo16 = __builtin_bit_cast(uint16_t, reg[p][0].e[e]);
+          const uint32_t hi16 = __builtin_bit_cast(uint16_t, reg[p][1].e[e]);
+          *reinterpret_cast<uint32_t*>(&lds[(nv + e) * LD + kl]) = lo16 | (hi16 << 16);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          lds[(nv + e) * LD + kl] = reg[p][0].e[e];
+          lds[(nv + e) * LD + kl + 1] = reg[p][1].e[e];
+        }
+      }
+    }
+  }
+};
+
+template <typename T, int BM, int BN, int BK, int WM, int WN, bool kVec>
 __global__ void __launch_bounds__(NT) lat_inv_kernel(const T* __restrict__ coef,
                                                      const T* __restrict__ tab,
                                                      T* __restrict__ Y, int L, int H, int Hp,
                                                      int Lp, int B, int C, int S,
                                                      SpinList sout_, int n_tiles_n) {
   using Tile = MfmaTile<T, BM, BN, BK, WM, WN>;
-  __shared__ __align__(16) T As[BM * Tile::LD];
-  __shared__ __align__(16) T Bs[BN * Tile::LD];
+  using G = GemmLds<T, BM, BN, BK>;
+  __shared__ __align__(16) T smem[G::bytes / sizeof(T)];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int M = 2 * L - 1;
-  const int mi = blockIdx.y, si = blockIdx.z;
+  // logical block = ((s, order, j tile), n' tile): the n' tiles of one
+  // (s, m, j tile) share its table tile and run on one XCD
+  const int n_tiles_j = (H + BN - 1) / BN;
+  int lbk = xcd_logical_block();
+  if (lbk >= S * M * n_tiles_j * n_tiles_n) return;
+  const int nt = lbk % n_tiles_n;
+  lbk /= n_tiles_n;
+  const int jt = lbk % n_tiles_j;
+  lbk /= n_tiles_j;
+  const int mi = mixed_order(lbk % M, L), si = lbk / M;
   const int m = mi - (L - 1);
   const int spin = sout_.s[si];
   const int lo = iabs(m) > iabs(spin) ? iabs(m) : iabs(spin);
-  const int nt = blockIdx.x % n_tiles_n, jt = blockIdx.x / n_tiles_n;
   const int Np = 2 * B * C;
   const int n0 = nt * BM, j0 = jt * BN;
-  const int twoC = 2 * C;
   const int kb = (lo / 8) * 8;  // aligned start of the degree range
   const T* Tb = tab + (size_t)(si * M + mi) * Hp * Lp;
-  auto brow = [&](int r) -> const T* {
-    const int j = j0 + r;
-    return j < H ? Tb + (size_t)j * Lp : nullptr;
-  };
+  CoefTLoader<T, BM, BK, kVec> la;
+  la.coef = coef;
+  la.m = m;
+  la.B = B;
+  la.S = S;
+  la.si = si;
+  la.twoC = 2 * C;
+  la.Np = Np;
+  la.n0 = n0;
+  la.lo = lo;
+  la.L = L;
+  la.k_base = kb;
+  RowLoader<T, BN, BK, true> lb;  // table rows: Lp is a multiple of 8
+  lb.init([&](int r) -> const T* { const int j = j0 + r; return j < H ? Tb + (size_t)j * Lp : nullptr; },
+          Tb + (size_t)j0 * Lp, kb, Lp, tid);
   Tile tile;
   tile.zero();
-  KTileLoader<T, BN, BK, NT> lb;
-
-  // coefficient operand, transposed into LDS: VEC consecutive n' per thread
-  constexpr int VEC = 16 / sizeof(T);
-  constexpr int VPC = BM / VEC;  // vectors per degree column of the tile
-  constexpr int NVA = BK * VPC;
-  constexpr int PERA = (NVA + NT - 1) / NT;
-  union Vec {
-    uint4 u;
-    T e[VEC];
-  };
-  Vec areg[PERA];
-  const bool avec = (twoC % VEC) == 0;
-  auto load_a = [&](int k0) {
+  mainloop(tile, la, lb, smem, (L - kb + BK - 1) / BK, wm, wn, lane);
+  T* Y0 = Y + ((size_t)(si * M + mi) * Np + n0) * Hp + j0;
+  epilogue(tile, smem, Np - n0, H - j0, wm, wn, lane, tid,
+           [&](int row, int col, const Vec16<T>& v, int n) {
+             T* dst = Y0 + (size_t)row * Hp + col;
+             if (n == Vec16<T>::N) {  // Y rows have a pitch of Hp, a multiple of 8
+               *reinterpret_cast<uint4*>(dst) = v.u;
+             } else {
 #pragma unroll
-    for (int p = 0; p < PERA; ++p) {
-      const int v = tid + p * NT;
-      if (NVA % NT != 0 && v >= NVA) break;
-      const int kl = v / VPC;
-      const int nv = (v % VPC) * VEC;
-      const int l = k0 + kl;
-      const int np = n0 + nv;
-      const bool lok = l >= lo && l < L;
-      if (lok && avec && np + VEC <= Np) {
-        const int b = np / twoC, rem = np - b * twoC;
-        areg[p].u = *reinterpret_cast<const uint4*>(
-            coef + (((size_t)(l * l + l + m) * B + b) * S + si) * twoC + rem);
-      } else {
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          const int n2 = np + e;
-          if (lok && n2 < Np) {
-            const int b = n2 / twoC, rem = n2 - b * twoC;
-            areg[p].e[e] = coef[(((size_t)(l * l + l + m) * B + b) * S + si) * twoC + rem];
-          } else {
-            areg[p].e[e] = (T)0.f;
-          }
-        }
-      }
-    }
-  };
-  auto store_a = [&]() {
-#pragma unroll
-    for (int p = 0; p < PERA; ++p) {
-      const int v = tid + p * NT;
-      if (NVA % NT != 0 && v >= NVA) break;
-      const int kl = v / VPC;
-      const int nv = (v % VPC) * VEC;
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) As[(nv + e) * Tile::LD + kl] = areg[p].e[e];
-    }
-  };
-
-  load_a(kb);
-  lb.load(brow, kb, Lp, tid, true);
-  for (int k0 = kb; k0 < L; k0 += BK) {
-    __syncthreads();
-    store_a();
-    lb.store(Bs, tid);
-    __syncthreads();
-    if (k0 + BK < L) {
-      load_a(k0 + BK);
-      lb.load(brow, k0 + BK, Lp, tid, true);
-    }
-    tile.compute(As, Bs, wm, wn, lane);
-  }
-  T* Y0 = Y + (size_t)(si * M + mi) * Np * Hp;
-  tile.for_each(wm, wn, lane, [&](int row, int col, float v) {
-    const int np = n0 + row;
-    const int j = j0 + col;
-    if (np < Np && j < H) Y0[(size_t)np * Hp + j] = (T)v;
-  });
+               for (int e = 0; e < Vec16<T>::N; ++e)
+                 if (e < n) dst[e] = v.e[e];
+             }
+           });
 }
 
 SpinList make_spins(const int* s, int n) {
@@ -313,14 +574,21 @@ SpinList make_spins(const int* s, int n) {
   return r;
 }
 
+// K step (a larger one lowers occupancy, which these kernels need more).
+template <typename T>
+constexpr int kBK = 32;
+
 template <typename T, int BM, int BN, int WM, int WN>
 hipError_t lat_fwd_cfg(const Plan& p, int B, int C, const void* X, void* coef, hipStream_t st) {
   const int Np = 2 * B * C;
   const int nrt = (p.L + BM - 1) / BM;
   const int nnt = (Np + BN - 1) / BN;
-  dim3 grid(nrt * nnt, p.M, p.n_in);
-  hipLaunchKernelGGL((lat_fwd_kernel<T, BM, BN, WM, WN>), grid, dim3(NT), 0, st, (const T*)X,
-                     (const T*)p.tab_fwd, (T*)coef, p.L, p.H, p.Hp, B, C, p.n_in, nrt);
+  const long long blocks = (long long)nrt * nnt * p.M * p.n_in;
+  constexpr int VEC = 16 / sizeof(T);
+  auto kern = (p.H % VEC == 0 && (2 * C) % VEC == 0) ? lat_fwd_kernel<T, BM, BN, kBK<T>, WM, WN, true>
+                                                      : lat_fwd_kernel<T, BM, BN, kBK<T>, WM, WN, false>;
+  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(NT), 0, st, (const T*)X, (const T*)p.tab_fwd,
+                     (T*)coef, p.L, p.H, p.Hp, B, C, p.n_in, nrt, nnt);
   return hipGetLastError();
 }
 
@@ -336,11 +604,14 @@ hipError_t mix_cfg(const Plan& p, int B, int Cin, int Cout, const void* coef, co
                    void* out, hipStream_t st) {
   int tiles = 0;
   for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + BM - 1) / BM;
-  const int Np = 2 * p.n_out * Cout;
-  dim3 grid(tiles, (Np + BN - 1) / BN);
-  hipLaunchKernelGGL((mix_kernel<T, BM, BN, WM, WN>), grid, dim3(NT), 0, st, (const T*)coef,
-                     (const T*)K, (T*)out, p.L, B, Cin, Cout, p.n_in, p.n_out,
-                     make_spins(p.spins_in, p.n_in), make_spins(p.spins_out, p.n_out));
+  const int Np = 2 * p.n_out * Cout, Kp = 2 * p.n_in * Cin;
+  const long long blocks = (long long)tiles * ((Np + BN - 1) / BN);
+  constexpr int VEC = 16 / sizeof(T);
+  auto kern = (Kp % VEC == 0 && Np % VEC == 0) ? mix_kernel<T, BM, BN, kBK<T>, WM, WN, true>
+                                               : mix_kernel<T, BM, BN, kBK<T>, WM, WN, false>;
+  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(NT), 0, st, (const T*)coef, (const T*)K,
+                     (T*)out, p.L, B, Cin, Cout, p.n_in, p.n_out, make_spins(p.spins_in, p.n_in),
+                     make_spins(p.spins_out, p.n_out));
   return hipGetLastError();
 }
 
@@ -357,10 +628,13 @@ hipError_t lat_inv_cfg(const Plan& p, int B, int C, const void* coef, void* Y, h
   const int Np = 2 * B * C;
   const int nnt = (Np + BM - 1) / BM;
   const int njt = (p.H + BN - 1) / BN;
-  dim3 grid(nnt * njt, p.M, p.n_out);
-  hipLaunchKernelGGL((lat_inv_kernel<T, BM, BN, WM, WN>), grid, dim3(NT), 0, st,
-                     (const T*)coef, (const T*)p.tab_inv, (T*)Y, p.L, p.H, p.Hp, p.Lp, B, C,
-                     p.n_out, make_spins(p.spins_out, p.n_out), nnt);
+  const long long blocks = (long long)nnt * njt * p.M * p.n_out;
+  constexpr int VEC = 16 / sizeof(T);
+  auto kern = ((2 * C) % VEC == 0) ? lat_inv_kernel<T, BM, BN, kBK<T>, WM, WN, true>
+                                   : lat_inv_kernel<T, BM, BN, kBK<T>, WM, WN, false>;
+  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(NT), 0, st, (const T*)coef,
+                     (const T*)p.tab_inv, (T*)Y, p.L, p.H, p.Hp, p.Lp, B, C, p.n_out,
+                     make_spins(p.spins_out, p.n_out), nnt);
   return hipGetLastError();
 }
 

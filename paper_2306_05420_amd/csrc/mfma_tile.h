@@ -97,59 +97,4 @@ struct MfmaTile {
   }
 };
 
-// Global -> register -> LDS staging of a K-contiguous operand tile of
-// R rows x BK columns.  `row_ptr(r)` returns the global address of element
-// k = 0 of tile row r, or nullptr for a row outside the matrix (zero
-// filled); columns at or beyond K are zero filled.  With `vec` the global
-// rows are 16-byte aligned and 16-byte vectors are used where they fit.
-template <typename T, int R, int BK, int NT>
-struct KTileLoader {
-  static constexpr int VEC = 16 / sizeof(T);
-  static constexpr int VPR = BK / VEC;
-  static constexpr int NV = R * VPR;
-  static constexpr int PER = (NV + NT - 1) / NT;
-  static constexpr int LD = BK + LdsPad<T>::value;
-  union Vec {
-    uint4 u;
-    T e[VEC];
-  };
-  Vec reg[PER];
-
-  template <class RowPtr>
-  __device__ __forceinline__ void load(RowPtr&& row_ptr, int k0, int K, int tid, bool vec) {
-#pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int v = tid + p * NT;
-      if (NV % NT != 0 && v >= NV) break;
-      const int r = v / VPR;
-      const int kv = (v % VPR) * VEC;
-      const T* src = row_ptr(r);
-      const int k = k0 + kv;
-      if (src != nullptr && vec && k + VEC <= K) {
-        reg[p].u = *reinterpret_cast<const uint4*>(src + k);
-      } else {
-#pragma unroll
-        for (int e = 0; e < VEC; ++e)
-          reg[p].e[e] = (src != nullptr && k + e < K) ? src[k + e] : (T)0.f;
-      }
-    }
-  }
-
-  __device__ __forceinline__ void store(T* __restrict__ lds, int tid) const {
-#pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int v = tid + p * NT;
-      if (NV % NT != 0 && v >= NV) break;
-      const int r = v / VPR;
-      const int kv = (v % VPR) * VEC;
-      if constexpr (std::is_same<T, float>::value) {
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) lds[r * LD + kv + e] = reg[p].e[e];
-      } else {
-        *reinterpret_cast<uint4*>(&lds[r * LD + kv]) = reg[p].u;
-      }
-    }
-  }
-};
-
 }  // namespace swsft
