@@ -109,15 +109,17 @@ __device__ __forceinline__ void stage_copy(T* stage, T* gbase, int M, int JB, in
         }
       }
       if (!kToGlobal) {
+        // unconditional stores too (a lane past the end rewrites vector 0 with
+        // the same data): a conditional store lets the compiler sink each
+        // load next to it, which serializes the loads again
 #pragma unroll
         for (int u = 0; u < BATCH; ++u) {
           const int idx = base + u * nthreads;
-          if (idx < total) {
-            const int vi = idx % vpr;
-            const int ri = (idx / vpr) & 1;
-            const int mi = idx / (2 * vpr);
-            *reinterpret_cast<uint4*>(stage + (size_t)mi * SP + ri * JB + vi * VEC) = buf[u];
-          }
+          const int id = idx < total ? idx : 0;
+          const int vi = id % vpr;
+          const int ri = (id / vpr) & 1;
+          const int mi = id / (2 * vpr);
+          *reinterpret_cast<uint4*>(stage + (size_t)mi * SP + ri * JB + vi * VEC) = buf[u];
         }
       }
     }
@@ -256,14 +258,13 @@ __global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
     float2 v[W2];
 #pragma unroll
     for (int q = 0; q < W2; ++q) {
+      // branch-free: orders outside |m| < L read row 0 and are zeroed after
       const int f = t + W1 * q;
       const int m = f < L ? f : f - W;
-      if (m > -L && m < L) {
-        const Tin* sp = stage + (size_t)(m + L - 1) * SP;
-        v[q] = make_float2((float)sp[r], (float)sp[JB + r]);
-      } else {
-        v[q] = make_float2(0.f, 0.f);
-      }
+      const bool ok = m > -L && m < L;
+      const Tin* sp = stage + (size_t)(ok ? m + L - 1 : 0) * SP;
+      const float re = (float)sp[r], im = (float)sp[JB + r];
+      v[q] = make_float2(ok ? re : 0.f, ok ? im : 0.f);
     }
     fft_reg<W2, +1>(v);
 #pragma unroll
