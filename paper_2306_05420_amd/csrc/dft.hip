@@ -1,7 +1,7 @@
 // Longitude DFT stages of the transform.
 //
-// Forward:  X[s][m][n][re/im][j] = sum_k x[b][s][c][j][k] exp(-2 pi i m k / W)
-// Inverse:  y[b][s][c][j][k]     = sum_m Y[s][m][n][re/im][j] exp(+2 pi i m k / W)
+// Forward:  X[s][m][j][n][re/im] = sum_k x[b][s][c][j][k] exp(-2 pi i m k / W)
+// Inverse:  y[b][s][c][j][k]     = sum_m Y[s][m][j][n][re/im] exp(+2 pi i m k / W)
 // for orders |m| < L, n = b*C + c.  This is the e^{i m phi} factor of the
 // harmonics in eqs. (2)-(3); the paper evaluates it as a dense DFT matrix
 // product on TPU (Method, "Efficient TPU implementation"), here it is an
@@ -11,9 +11,11 @@
 // samples is split W = W1 * W2: W1 threads per row, each holding W2 samples
 // strided by W1 (coalesced loads), a length-W2 register FFT, a twiddle, an
 // LDS exchange, a length-W1 register FFT.  The spectrum is then staged in
-// LDS as [m][re/im][j] and written with j fastest, so the output layout has
-// the latitude index contiguous, which is the K dimension of the latitude
-// GEMM that reads it.
+// LDS as [m][re/im][j] and written with j fastest into the K-tiled layout
+// X[s][m][j/JT][n][re/im][JT] (JT = 32): the latitude index, the K dimension
+// of the latitude GEMM, is contiguous within a tile, and one tile of all
+// maps is one contiguous block, so the GEMM reads whole 8 KiB blocks per K
+// step and a block of rows of one map writes 128-byte runs.
 #include "fft_reg.h"
 #include "swsft_internal.h"
 #include "xcd.h"
@@ -79,11 +81,12 @@ struct Raw<__bf16> {
 constexpr int kMaxPasses = 2;
 
 // Move the [M][2][JB] spectrum block between the LDS stage (pitch SP) and
-// global memory at X[((mi * NBC + n) * 2 + ri) * Hp + j0 + r] (base already
-// offset to this spin), in 16-byte vectors when JB allows.
+// global memory at gbase[mi * mstride + (n * 2 + ri) * pitch + r] (gbase
+// already offset to the spin, latitude tile and row), in 16-byte vectors
+// when JB allows.
 template <typename T, bool kToGlobal>
 __device__ __forceinline__ void stage_copy(T* stage, T* gbase, int M, int JB, int SP,
-                                           size_t mstride, size_t nbase, int Hp, int tid,
+                                           size_t mstride, size_t nbase, int pitch, int tid,
                                            int nthreads) {
   constexpr int VEC = 16 / sizeof(T);
   constexpr int BATCH = 8;  // global loads in flight per thread before their LDS stores
@@ -101,7 +104,7 @@ __device__ __forceinline__ void stage_copy(T* stage, T* gbase, int M, int JB, in
         const int ri = (id / vpr) & 1;
         const int mi = id / (2 * vpr);
         uint4* s = reinterpret_cast<uint4*>(stage + (size_t)mi * SP + ri * JB + vi * VEC);
-        uint4* g = reinterpret_cast<uint4*>(gbase + mi * mstride + (nbase * 2 + ri) * Hp + vi * VEC);
+        uint4* g = reinterpret_cast<uint4*>(gbase + mi * mstride + (nbase * 2 + ri) * pitch + vi * VEC);
         if (kToGlobal) {
           if (idx < total) *g = *s;
         } else {
@@ -130,7 +133,7 @@ __device__ __forceinline__ void stage_copy(T* stage, T* gbase, int M, int JB, in
       const int ri = (idx / JB) & 1;
       const int mi = idx / (2 * JB);
       T* s = stage + (size_t)mi * SP + ri * JB + r;
-      T* g = gbase + mi * mstride + (nbase * 2 + ri) * Hp + r;
+      T* g = gbase + mi * mstride + (nbase * 2 + ri) * pitch + r;
       if (kToGlobal) *g = *s;
       else *s = *g;
     }
@@ -141,7 +144,7 @@ template <typename Tin, typename Tout, int W1, int W2>
 __global__ void __launch_bounds__(256) dft_fwd_kernel(const Tin* __restrict__ x,
                                                       Tout* __restrict__ X,
                                                       const float2* __restrict__ tw, int S,
-                                                      int C, int NB, int NBC, int H, int Hp,
+                                                      int C, int NB, int NBC, int H, int JT,
                                                       int L, int JB) {
   constexpr int W = W1 * W2;
   extern __shared__ __align__(16) unsigned char smem[];
@@ -212,15 +215,17 @@ __global__ void __launch_bounds__(256) dft_fwd_kernel(const Tin* __restrict__ x,
   }
   __syncthreads();
   // X[si][mi][n][ri][j0 + r]
-  stage_copy<Tout, true>(stage, X + (size_t)si * M * NBC * 2 * Hp + j0, M, JB, SP,
-                         (size_t)NBC * 2 * Hp, n, Hp, tid, blockDim.x);
+  // X[si][mi][j0 / JT][n][ri][j0 % JT + r]
+  const size_t tile = (size_t)NBC * 2 * JT;  // one latitude tile of one order
+  stage_copy<Tout, true>(stage, X + ((size_t)si * M * (H / JT) + j0 / JT) * tile + j0 % JT, M, JB,
+                         SP, (size_t)(H / JT) * tile, n, JT, tid, blockDim.x);
 }
 
 template <typename Tin, typename Tout, int W1, int W2>
 __global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
                                                       Tout* __restrict__ y,
                                                       const float2* __restrict__ tw, int S,
-                                                      int C, int NB, int NBC, int H, int Hp,
+                                                      int C, int NB, int NBC, int H, int JT,
                                                       int L, int JB) {
   constexpr int W = W1 * W2;
   extern __shared__ __align__(16) unsigned char smem[];
@@ -245,8 +250,10 @@ __global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
   float2* ex = reinterpret_cast<float2*>(smem);
   Tin* stage = reinterpret_cast<Tin*>(ex + (size_t)RPP * W2 * (W1 + 1));
 
-  stage_copy<Tin, false>(stage, const_cast<Tin*>(Y) + (size_t)si * M * NBC * 2 * Hp + j0, M, JB,
-                         SP, (size_t)NBC * 2 * Hp, n, Hp, tid, blockDim.x);
+  const size_t tile = (size_t)NBC * 2 * JT;  // one latitude tile of one order
+  stage_copy<Tin, false>(stage,
+                         const_cast<Tin*>(Y) + ((size_t)si * M * (H / JT) + j0 / JT) * tile + j0 % JT,
+                         M, JB, SP, (size_t)(H / JT) * tile, n, JT, tid, blockDim.x);
   __syncthreads();
 
   const size_t row_base = ((size_t)map * H + j0) * W;
@@ -290,12 +297,20 @@ __global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
 // Rows per workgroup JB = NP * RPP: RPP rows are transformed at a time by
 // 256 / W1 threads (fewer for small grids), NP <= 2 passes.  JB = 32 gives
 // 64-byte (bf16) / 128-byte (f32) runs per order in the transposed layout.
+#ifndef SWSFT_DFT_THREADS
+#define SWSFT_DFT_THREADS 256
+#endif
+#ifndef SWSFT_DFT_JB
+#define SWSFT_DFT_JB 32
+#endif
+
 template <typename Ts, int W1, int W2>
 void dft_geometry(const Plan& p, int* JB, int* nthreads, size_t* lds) {
-  int rpp = 256 / W1;
+  int rpp = SWSFT_DFT_THREADS / W1;
+  if (rpp < 1) rpp = 1;
   if (rpp > p.H) rpp = p.H;
   int jb = rpp;
-  if (jb < 32 && 2 * jb <= p.H) jb *= 2;  // a second pass when rows allow
+  if (jb < SWSFT_DFT_JB && 2 * jb <= p.H) jb *= 2;  // a second pass when rows allow
   auto bytes = [&](int j) {
     return (size_t)rpp * W2 * (W1 + 1) * sizeof(float2) +
            (size_t)p.M * stage_pitch<Ts>(j) * sizeof(Ts);
@@ -320,7 +335,7 @@ hipError_t launch_fwd_shape(const Plan& p, int S, int B, int C, const void* x, v
   }
   const long long blocks = (long long)B * S * C * (p.H / JB);
   hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(nthreads), lds, st, (const Tin*)x,
-                     (Tout*)X, p.twiddle, S, C, B, B * C, p.H, p.Hp, p.L, JB);
+                     (Tout*)X, p.twiddle, S, C, B, B * C, p.H, p.JT, p.L, JB);
   return hipGetLastError();
 }
 
@@ -338,7 +353,7 @@ hipError_t launch_inv_shape(const Plan& p, int S, int B, int C, const void* Y, v
   }
   const long long blocks = (long long)B * S * C * (p.H / JB);
   hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(nthreads), lds, st, (const Tin*)Y,
-                     (Tout*)y, p.twiddle, S, C, B, B * C, p.H, p.Hp, p.L, JB);
+                     (Tout*)y, p.twiddle, S, C, B, B * C, p.H, p.JT, p.L, JB);
   return hipGetLastError();
 }
 

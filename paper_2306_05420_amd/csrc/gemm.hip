@@ -1,18 +1,19 @@
 // The three contractions of the layer, as MFMA GEMMs.
 //
 //  lat_fwd  (eq. (2), latitude sum), per (spin s, order m):
-//     coef[l*l+l+m][b][s][c] = sum_j Tf[s][m][l][j] X[s][m][n][re/im][j]
+//     coef[l*l+l+m][b][s][c] = sum_j Tf[s][m][l][j] X[s][m][j][n][re/im]
 //     real GEMM: rows l in [|m|, L), columns n' = 2n + re/im, K = j.
 //  mix      (per-degree products with filters shared across m), per l:
 //     coef'[l][(m,b)][(t,c')] = sum_(s,c) coef[l][(m,b)][(s,c)] K[l][(t,c')][(s,c)]
 //     complex GEMM written as a real GEMM with K doubled: each filter row is
 //     expanded in LDS into the two real rows (re, -im, ...) and (im, re, ...).
 //  lat_inv  (eq. (3), latitude sum), per (spin t, order m):
-//     Y[t][m][n'][j] = sum_l coef'[l*l+l+m][b][t][c'][re/im] Ti[t][m][j][l]
+//     Y[t][m][j][n'] = sum_l coef'[l*l+l+m][b][t][c'][re/im] Ti[t][m][j][l]
 //     real GEMM: rows n', columns j, K = l in [max(|m|,|t|), L).
 //
-// Every operand is staged in LDS K-contiguous; the tables and the X / Y
-// intermediates are laid out so that their global rows already are, the
+// Every operand is staged in LDS K-contiguous; the tables and the K-tiled X /
+// Y spectra ([j/32][n'][32]) are laid out so that their global rows already
+// are, the
 // mixing filters are stored output-major for the same reason, and only the
 // coefficient operand of lat_inv is transposed on its way into LDS.
 //
@@ -109,7 +110,9 @@ __device__ __forceinline__ void epilogue(const MfmaTile<T, BM, BN, BK, WM, WN>& 
 }
 
 // K-contiguous operand tile of R rows from global rows given by row_ptr(r)
-// (nullptr = zero row); columns >= K are zero.  kVec: 16-byte loads (rows
+// (nullptr = zero row); columns >= K are zero.  Element k of a row is at
+// row + k_base + (k - k_base) / BK * kstride + (k - k_base) % BK: kstride = BK
+// for plain rows, the tile stride for K-tiled operands.  kVec: 16-byte loads (rows
 // 16-byte aligned, K a multiple of the vector); else element loads.  The
 // choice is a template flag: as a runtime branch the compiler merges both
 // paths into element loads.
@@ -131,12 +134,14 @@ struct RowLoader {
   unsigned ok_[PER];  // bit e: element e of reg[p] is in range
   int kv_[PER];
   int k_base, K;
+  size_t kstride;  // elements between consecutive K tiles of a row
 
   template <class RowPtr>
   __device__ __forceinline__ void init(RowPtr&& row_ptr, const T* fallback, int k_base_, int K_,
-                                       int tid) {
+                                       int tid, size_t kstride_ = BK) {
     k_base = k_base_;
     K = K_;
+    kstride = kstride_;
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int v = tid + p * NT;
@@ -150,16 +155,17 @@ struct RowLoader {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int k = k_base + kt * BK + kv_[p];
+      const size_t off = k_base + kt * kstride + kv_[p];  // address of element k
       if constexpr (kVec) {
         const bool ok = rowok_[p] && k < K;
-        reg[p].u = *reinterpret_cast<const uint4*>(rows_[p] + (ok ? k : 0));
+        reg[p].u = *reinterpret_cast<const uint4*>(rows_[p] + (ok ? off : 0));
         ok_[p] = ok ? 0xffu : 0u;
       } else {
         unsigned bits = 0;
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
           const bool ok = rowok_[p] && k + e < K;
-          reg[p].e[e] = rows_[p][ok ? k + e : 0];
+          reg[p].e[e] = rows_[p][ok ? off + e : 0];
           bits |= (ok ? 1u : 0u) << e;
         }
         ok_[p] = bits;
@@ -197,7 +203,7 @@ template <typename T, int BM, int BN, int BK, int WM, int WN, bool kVec>
 __global__ void __launch_bounds__(NT) lat_fwd_kernel(const T* __restrict__ X,
                                                      const T* __restrict__ tab,
                                                      T* __restrict__ coef, int L, int H, int Hp,
-                                                     int B, int C, int S, int n_row_tiles,
+                                                     int JT, int B, int C, int S, int n_row_tiles,
                                                      int n_tiles_n) {
   using Tile = MfmaTile<T, BM, BN, BK, WM, WN>;
   using G = GemmLds<T, BM, BN, BK>;
@@ -220,13 +226,13 @@ __global__ void __launch_bounds__(NT) lat_fwd_kernel(const T* __restrict__ X,
   const int Np = 2 * B * C;
   const int n0 = nt * BN;
   const T* A0 = tab + (size_t)(si * M + mi) * L * Hp;
-  const T* B0 = X + (size_t)(si * M + mi) * Np * Hp;
+  const T* B0 = X + (size_t)(si * M + mi) * Np * H;  // K-tiled: [H/JT][Np][JT]
   RowLoader<T, BM, BK, kVec> la;
   RowLoader<T, BN, BK, kVec> lb;
   la.init([&](int r) -> const T* { const int l = l_begin + r; return l < L ? A0 + (size_t)l * Hp : nullptr; },
           A0 + (size_t)l_begin * Hp, 0, H, tid);
-  lb.init([&](int r) -> const T* { const int np = n0 + r; return np < Np ? B0 + (size_t)np * Hp : nullptr; },
-          B0 + (size_t)n0 * Hp, 0, H, tid);
+  lb.init([&](int r) -> const T* { const int np = n0 + r; return np < Np ? B0 + (size_t)np * JT : nullptr; },
+          B0 + (size_t)n0 * JT, 0, H, tid, (size_t)Np * JT);
   Tile tile;
   tile.zero();
   mainloop(tile, la, lb, smem, (H + BK - 1) / BK, wm, wn, lane);
@@ -511,7 +517,7 @@ template <typename T, int BM, int BN, int BK, int WM, int WN, bool kVec>
 __global__ void __launch_bounds__(NT) lat_inv_kernel(const T* __restrict__ coef,
                                                      const T* __restrict__ tab,
                                                      T* __restrict__ Y, int L, int H, int Hp,
-                                                     int Lp, int B, int C, int S,
+                                                     int JT, int Lp, int B, int C, int S,
                                                      SpinList sout_, int n_tiles_n) {
   using Tile = MfmaTile<T, BM, BN, BK, WM, WN>;
   using G = GemmLds<T, BM, BN, BK>;
@@ -554,16 +560,18 @@ __global__ void __launch_bounds__(NT) lat_inv_kernel(const T* __restrict__ coef,
   Tile tile;
   tile.zero();
   mainloop(tile, la, lb, smem, (L - kb + BK - 1) / BK, wm, wn, lane);
-  T* Y0 = Y + ((size_t)(si * M + mi) * Np + n0) * Hp + j0;
+  // Y K-tiled: [H/JT][Np][JT]; element (n', j) at (j / JT) Np JT + n' JT + j % JT
+  T* Y0 = Y + (size_t)(si * M + mi) * Np * H;
+  const size_t tstride = (size_t)Np * JT;
   epilogue(tile, smem, Np - n0, H - j0, wm, wn, lane, tid,
            [&](int row, int col, const Vec16<T>& v, int n) {
-             T* dst = Y0 + (size_t)row * Hp + col;
-             if (n == Vec16<T>::N) {  // Y rows have a pitch of Hp, a multiple of 8
-               *reinterpret_cast<uint4*>(dst) = v.u;
+             const int np = n0 + row, j = j0 + col;
+             if (n == Vec16<T>::N) {  // 8 consecutive j inside one tile (JT is a multiple of 8)
+               *reinterpret_cast<uint4*>(Y0 + (j / JT) * tstride + (size_t)np * JT + j % JT) = v.u;
              } else {
 #pragma unroll
                for (int e = 0; e < Vec16<T>::N; ++e)
-                 if (e < n) dst[e] = v.e[e];
+                 if (e < n) Y0[((j + e) / JT) * tstride + (size_t)np * JT + (j + e) % JT] = v.e[e];
              }
            });
 }
@@ -574,9 +582,18 @@ SpinList make_spins(const int* s, int n) {
   return r;
 }
 
-// K step (a larger one lowers occupancy, which these kernels need more).
-template <typename T>
-constexpr int kBK = 32;
+// K step of each contraction for bf16 storage (float uses 32).
+#ifndef SWSFT_BK_LAT_FWD
+#define SWSFT_BK_LAT_FWD 32
+#endif
+#ifndef SWSFT_BK_MIX
+#define SWSFT_BK_MIX 32
+#endif
+#ifndef SWSFT_BK_LAT_INV
+#define SWSFT_BK_LAT_INV 32
+#endif
+template <typename T, int kBf16>
+constexpr int kBK = sizeof(T) == 2 ? kBf16 : 32;
 
 template <typename T, int BM, int BN, int WM, int WN>
 hipError_t lat_fwd_cfg(const Plan& p, int B, int C, const void* X, void* coef, hipStream_t st) {
@@ -585,16 +602,20 @@ hipError_t lat_fwd_cfg(const Plan& p, int B, int C, const void* X, void* coef, h
   const int nnt = (Np + BN - 1) / BN;
   const long long blocks = (long long)nrt * nnt * p.M * p.n_in;
   constexpr int VEC = 16 / sizeof(T);
-  auto kern = (p.H % VEC == 0 && (2 * C) % VEC == 0) ? lat_fwd_kernel<T, BM, BN, kBK<T>, WM, WN, true>
-                                                      : lat_fwd_kernel<T, BM, BN, kBK<T>, WM, WN, false>;
+  auto kern = (p.H % VEC == 0 && (2 * C) % VEC == 0) ? lat_fwd_kernel<T, BM, BN, kBK<T, SWSFT_BK_LAT_FWD>, WM, WN, true>
+                                                      : lat_fwd_kernel<T, BM, BN, kBK<T, SWSFT_BK_LAT_FWD>, WM, WN, false>;
   hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(NT), 0, st, (const T*)X, (const T*)p.tab_fwd,
-                     (T*)coef, p.L, p.H, p.Hp, B, C, p.n_in, nrt, nnt);
+                     (T*)coef, p.L, p.H, p.Hp, p.JT, B, C, p.n_in, nrt, nnt);
   return hipGetLastError();
 }
 
+#ifndef SWSFT_LAT_FWD_TILE
+#define SWSFT_LAT_FWD_TILE 128, 128, 2, 2
+#endif
+
 template <typename T>
 hipError_t lat_fwd_t(const Plan& p, int B, int C, const void* X, void* coef, hipStream_t st) {
-  if (p.L > 64) return lat_fwd_cfg<T, 128, 128, 2, 2>(p, B, C, X, coef, st);
+  if (p.L > 64) return lat_fwd_cfg<T, SWSFT_LAT_FWD_TILE>(p, B, C, X, coef, st);
   if (p.L > 32) return lat_fwd_cfg<T, 64, 128, 2, 2>(p, B, C, X, coef, st);
   return lat_fwd_cfg<T, 32, 128, 1, 4>(p, B, C, X, coef, st);
 }
@@ -607,19 +628,24 @@ hipError_t mix_cfg(const Plan& p, int B, int Cin, int Cout, const void* coef, co
   const int Np = 2 * p.n_out * Cout, Kp = 2 * p.n_in * Cin;
   const long long blocks = (long long)tiles * ((Np + BN - 1) / BN);
   constexpr int VEC = 16 / sizeof(T);
-  auto kern = (Kp % VEC == 0 && Np % VEC == 0) ? mix_kernel<T, BM, BN, kBK<T>, WM, WN, true>
-                                               : mix_kernel<T, BM, BN, kBK<T>, WM, WN, false>;
+  auto kern = (Kp % VEC == 0 && Np % VEC == 0) ? mix_kernel<T, BM, BN, kBK<T, SWSFT_BK_MIX>, WM, WN, true>
+                                               : mix_kernel<T, BM, BN, kBK<T, SWSFT_BK_MIX>, WM, WN, false>;
   hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(NT), 0, st, (const T*)coef, (const T*)K,
                      (T*)out, p.L, B, Cin, Cout, p.n_in, p.n_out, make_spins(p.spins_in, p.n_in),
                      make_spins(p.spins_out, p.n_out));
   return hipGetLastError();
 }
 
+// Tile of the large-channel mixing GEMM (rows x columns, waves per dim).
+#ifndef SWSFT_MIX_TILE
+#define SWSFT_MIX_TILE 128, 128, 2, 2
+#endif
+
 template <typename T>
 hipError_t mix_t(const Plan& p, int B, int Cin, int Cout, const void* coef, const void* K,
                  void* out, hipStream_t st) {
   const int Np = 2 * p.n_out * Cout;
-  if (Np >= 128) return mix_cfg<T, 128, 128, 2, 2>(p, B, Cin, Cout, coef, K, out, st);
+  if (Np >= 128) return mix_cfg<T, SWSFT_MIX_TILE>(p, B, Cin, Cout, coef, K, out, st);
   return mix_cfg<T, 128, 32, 4, 1>(p, B, Cin, Cout, coef, K, out, st);
 }
 
@@ -630,17 +656,21 @@ hipError_t lat_inv_cfg(const Plan& p, int B, int C, const void* coef, void* Y, h
   const int njt = (p.H + BN - 1) / BN;
   const long long blocks = (long long)nnt * njt * p.M * p.n_out;
   constexpr int VEC = 16 / sizeof(T);
-  auto kern = ((2 * C) % VEC == 0) ? lat_inv_kernel<T, BM, BN, kBK<T>, WM, WN, true>
-                                   : lat_inv_kernel<T, BM, BN, kBK<T>, WM, WN, false>;
+  auto kern = ((2 * C) % VEC == 0) ? lat_inv_kernel<T, BM, BN, kBK<T, SWSFT_BK_LAT_INV>, WM, WN, true>
+                                   : lat_inv_kernel<T, BM, BN, kBK<T, SWSFT_BK_LAT_INV>, WM, WN, false>;
   hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(NT), 0, st, (const T*)coef,
-                     (const T*)p.tab_inv, (T*)Y, p.L, p.H, p.Hp, p.Lp, B, C, p.n_out,
+                     (const T*)p.tab_inv, (T*)Y, p.L, p.H, p.Hp, p.JT, p.Lp, B, C, p.n_out,
                      make_spins(p.spins_out, p.n_out), nnt);
   return hipGetLastError();
 }
 
+#ifndef SWSFT_LAT_INV_TILE
+#define SWSFT_LAT_INV_TILE 128, 128, 2, 2
+#endif
+
 template <typename T>
 hipError_t lat_inv_t(const Plan& p, int B, int C, const void* coef, void* Y, hipStream_t st) {
-  if (p.H >= 128) return lat_inv_cfg<T, 128, 128, 2, 2>(p, B, C, coef, Y, st);
+  if (p.H >= 128) return lat_inv_cfg<T, SWSFT_LAT_INV_TILE>(p, B, C, coef, Y, st);
   if (p.H >= 64) return lat_inv_cfg<T, 128, 64, 2, 2>(p, B, C, coef, Y, st);
   return lat_inv_cfg<T, 128, 32, 4, 1>(p, B, C, coef, Y, st);
 }

@@ -30,7 +30,8 @@ inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 struct Plan {
   int device = 0;
   int H = 0, W = 0, L = 0;
-  int Hp = 0;  // H rounded up to a multiple of 8 (row pitch of tables, X and Y)
+  int Hp = 0;  // H rounded up to a multiple of 8 (row pitch of the forward tables)
+  int JT = 0;  // latitude tile of the X / Y spectra: min(H, 32), the latitude GEMMs' K step
   int Lp = 0;  // L rounded up to a multiple of 8 (row pitch of inverse tables)
   int M = 0;   // number of orders, 2L - 1
   int n_in = 0, n_out = 0;
@@ -53,8 +54,10 @@ struct Plan {
 };
 
 // Sizes (in reals of the storage type) of the intermediate buffers.
+// X / Y spectra, K-tiled: [S][2L-1][H/JT][B*C][re/im][JT], so that one
+// latitude tile of all maps is one contiguous block.
 inline size_t xy_elems(const Plan& p, int S, int B, int C) {
-  return (size_t)S * p.M * (size_t)B * C * 2 * p.Hp;
+  return (size_t)S * p.M * (size_t)B * C * 2 * p.H;
 }
 inline size_t coef_elems(const Plan& p, int S, int B, int C) {
   return (size_t)p.L * p.L * (size_t)B * S * C * 2;
@@ -63,10 +66,10 @@ inline size_t coef_elems(const Plan& p, int S, int B, int C) {
 // ---- kernel launchers (return hipGetLastError() of the launch) ----
 hipError_t launch_tables(const Plan& p, hipStream_t st);
 
-// x [B][S][C][H][W] -> X [S][M][B*C][2][Hp]
+// x [B][S][C][H][W] -> X [S][M][H/JT][B*C][2][JT]
 hipError_t launch_dft_fwd(const Plan& p, int S, int B, int C, const void* x, void* X,
                           hipStream_t st);
-// Y [S][M][B*C][2][Hp] -> y [B][S][C][H][W]
+// Y [S][M][H/JT][B*C][2][JT] -> y [B][S][C][H][W]
 hipError_t launch_dft_inv(const Plan& p, int S, int B, int C, const void* Y, void* y,
                           hipStream_t st);
 // X (spins_in) -> coef [L^2][B][S_in][C]

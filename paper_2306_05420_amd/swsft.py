@@ -21,7 +21,9 @@ import re
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libswsft.so")
+# SWSFT_LIBRARY may name another build of the same library (e.g. a tuning
+# variant); by default the in-tree build is used.
+LIB_PATH = os.environ.get("SWSFT_LIBRARY") or os.path.join(_PKG, "libswsft.so")
 HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "swsft.h")
 
 OK, E_INVALID, E_UNSUPPORTED, E_ALLOC, E_HIP, E_WORKSPACE = range(6)
