@@ -683,8 +683,14 @@ hipError_t launch_lat_fwd(const Plan& p, int B, int C, const void* X, void* coef
   return lat_fwd_t<float>(p, B, C, X, coef, st);
 }
 
+#ifndef SWSFT_MIX_DMA
+#define SWSFT_MIX_DMA 1
+#endif
+
 hipError_t launch_mix(const Plan& p, int B, int Cin, int Cout, const void* coef, const void* K,
                       void* out, hipStream_t st) {
+  if (SWSFT_MIX_DMA && mix_dma_supported(p, Cin, Cout))
+    return launch_mix_dma(p, B, Cin, Cout, coef, K, out, st);
   if (p.dtype == SWSFT_BF16) return mix_t<__bf16>(p, B, Cin, Cout, coef, K, out, st);
   return mix_t<float>(p, B, Cin, Cout, coef, K, out, st);
 }
