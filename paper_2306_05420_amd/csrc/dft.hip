@@ -166,8 +166,10 @@ __global__ void __launch_bounds__(256) dft_fwd_kernel(const Tin* __restrict__ x,
   const int n = b * C + c;
   const int M = 2 * L - 1;
   const int SP = stage_pitch<Tout>(JB);
-  float2* ex = reinterpret_cast<float2*>(smem);  // [RPP][W2][W1+1]
-  Tout* stage = reinterpret_cast<Tout*>(ex + (size_t)RPP * W2 * (W1 + 1));  // [M][SP]
+  // the exchange buffer [RPP][W2][W1+1] (during the FFTs) and the spectrum
+  // stage [M][SP] (after them) share one allocation
+  float2* ex = reinterpret_cast<float2*>(smem);
+  Tout* stage = reinterpret_cast<Tout*>(smem);
 
   // every load of the block's JB rows is issued before any arithmetic
   const size_t row_base = ((size_t)map * H + j0) * W;  // complex index of row j0
@@ -180,10 +182,12 @@ __global__ void __launch_bounds__(256) dft_fwd_kernel(const Tin* __restrict__ x,
         raw[p][q] = Raw<Tin>::load(x, row_base + (size_t)(p * RPP + rr) * W + t + W1 * q);
     }
   float2* exr = ex + (size_t)rr * W2 * (W1 + 1);
+  // spectra of all passes stay in registers until the exchange buffer is free:
+  // spec[p][i * W1 + k1] is frequency t + W1 * i + W2 * k1 of row p * RPP + rr
+  float2 spec[kMaxPasses][W2];
 #pragma unroll
   for (int p = 0; p < kMaxPasses; ++p) {
     if (p >= NP) break;
-    const int r = p * RPP + rr;
     float2 v[W2];
 #pragma unroll
     for (int q = 0; q < W2; ++q) v[q] = Raw<Tin>::unpack(raw[p][q]);
@@ -202,16 +206,26 @@ __global__ void __launch_bounds__(256) dft_fwd_kernel(const Tin* __restrict__ x,
       for (int tp = 0; tp < W1; ++tp) u[tp] = exr[k2 * (W1 + 1) + tp];
       fft_reg<W1, -1>(u);
 #pragma unroll
+      for (int k1 = 0; k1 < W1; ++k1) spec[p][i * W1 + k1] = u[k1];
+    }
+  }
+  __syncthreads();  // every read of ex is done before the stage overwrites it
+#pragma unroll
+  for (int p = 0; p < kMaxPasses; ++p) {
+    if (p >= NP) break;
+    const int r = p * RPP + rr;
+#pragma unroll
+    for (int i = 0; i < W2 / W1; ++i)
+#pragma unroll
       for (int k1 = 0; k1 < W1; ++k1) {
-        const int f = k2 + W2 * k1;
+        const int f = t + W1 * i + W2 * k1;
         const int m = f < L ? f : f - W;
         if (m > -L && m < L) {
           Tout* sp = stage + (size_t)(m + L - 1) * SP;
-          sp[r] = (Tout)u[k1].x;
-          sp[JB + r] = (Tout)u[k1].y;
+          sp[r] = (Tout)spec[p][i * W1 + k1].x;
+          sp[JB + r] = (Tout)spec[p][i * W1 + k1].y;
         }
       }
-    }
   }
   __syncthreads();
   // X[si][mi][n][ri][j0 + r]
@@ -247,8 +261,10 @@ __global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
   const int n = b * C + c;
   const int M = 2 * L - 1;
   const int SP = stage_pitch<Tin>(JB);
+  // the spectrum stage [M][SP] (first) and the exchange buffer
+  // [RPP][W2][W1+1] (during the FFTs) share one allocation
+  Tin* stage = reinterpret_cast<Tin*>(smem);
   float2* ex = reinterpret_cast<float2*>(smem);
-  Tin* stage = reinterpret_cast<Tin*>(ex + (size_t)RPP * W2 * (W1 + 1));
 
   const size_t tile = (size_t)NBC * 2 * JT;  // one latitude tile of one order
   stage_copy<Tin, false>(stage,
@@ -256,13 +272,13 @@ __global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
                          M, JB, SP, (size_t)(H / JT) * tile, n, JT, tid, blockDim.x);
   __syncthreads();
 
-  const size_t row_base = ((size_t)map * H + j0) * W;
-  float2* exr = ex + (size_t)rr * W2 * (W1 + 1);
+  // the spectra of all passes are read into registers before the exchange
+  // buffer overwrites the stage
+  float2 v[kMaxPasses][W2];
 #pragma unroll
   for (int p = 0; p < kMaxPasses; ++p) {
     if (p >= NP) break;
     const int r = p * RPP + rr;
-    float2 v[W2];
 #pragma unroll
     for (int q = 0; q < W2; ++q) {
       // branch-free: orders outside |m| < L read row 0 and are zeroed after
@@ -271,14 +287,23 @@ __global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
       const bool ok = m > -L && m < L;
       const Tin* sp = stage + (size_t)(ok ? m + L - 1 : 0) * SP;
       const float re = (float)sp[r], im = (float)sp[JB + r];
-      v[q] = make_float2(ok ? re : 0.f, ok ? im : 0.f);
+      v[p][q] = make_float2(ok ? re : 0.f, ok ? im : 0.f);
     }
-    fft_reg<W2, +1>(v);
+  }
+  __syncthreads();
+
+  const size_t row_base = ((size_t)map * H + j0) * W;
+  float2* exr = ex + (size_t)rr * W2 * (W1 + 1);
 #pragma unroll
-    for (int k2 = 1; k2 < W2; ++k2) v[k2] = cmulc(v[k2], tw[t * k2]);
+  for (int p = 0; p < kMaxPasses; ++p) {
+    if (p >= NP) break;
+    const int r = p * RPP + rr;
+    fft_reg<W2, +1>(v[p]);
+#pragma unroll
+    for (int k2 = 1; k2 < W2; ++k2) v[p][k2] = cmulc(v[p][k2], tw[t * k2]);
     if (p > 0) __syncthreads();  // the previous pass has finished reading ex
 #pragma unroll
-    for (int k2 = 0; k2 < W2; ++k2) exr[k2 * (W1 + 1) + t] = v[k2];
+    for (int k2 = 0; k2 < W2; ++k2) exr[k2 * (W1 + 1) + t] = v[p][k2];
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < W2 / W1; ++i) {
@@ -311,9 +336,10 @@ void dft_geometry(const Plan& p, int* JB, int* nthreads, size_t* lds) {
   if (rpp > p.H) rpp = p.H;
   int jb = rpp;
   if (jb < SWSFT_DFT_JB && 2 * jb <= p.H) jb *= 2;  // a second pass when rows allow
-  auto bytes = [&](int j) {
-    return (size_t)rpp * W2 * (W1 + 1) * sizeof(float2) +
-           (size_t)p.M * stage_pitch<Ts>(j) * sizeof(Ts);
+  auto bytes = [&](int j) {  // exchange buffer and stage alias
+    const size_t ex = (size_t)rpp * W2 * (W1 + 1) * sizeof(float2);
+    const size_t stage = (size_t)p.M * stage_pitch<Ts>(j) * sizeof(Ts);
+    return ex > stage ? ex : stage;
   };
   if (bytes(jb) > 160 * 1024) jb = rpp;  // one pass if two do not fit the CU's LDS
   *JB = jb;
