@@ -11,8 +11,13 @@
 // so the hardware copies them from HBM/L2 without passing through registers
 // and several K steps are in flight per workgroup.
 //
-// Preconditions (checked by the launcher): bf16, K' = 2 S_in C_in a multiple
-// of 32, each input spin's channel block a whole number of 32-wide K steps.
+// Tile geometry (template parameters): BK reals of every row per K step (64
+// = one whole 128-byte line per row and copy), RA coefficient rows (2 RA
+// expanded GEMM rows) x RB filter rows (complex outputs) per workgroup, ST
+// K steps resident in LDS.  Each wave owns 64 expanded rows x 64 outputs.
+//
+// Preconditions (checked by the launcher): bf16, K' = 2 S_in C_in with each
+// input spin's channel block a whole number of BK-wide K steps, C_out % 4 == 0.
 #include "mfma_tile.h"
 #include "swsft_internal.h"
 #include "xcd.h"
@@ -20,13 +25,7 @@
 namespace swsft {
 namespace {
 
-constexpr int kNT = 256;     // 4 waves
-constexpr int kBK = 32;      // bf16 per row per K step (64 bytes)
-constexpr int kRowsA = 64;   // coefficient rows per tile (128 expanded GEMM rows)
-constexpr int kRowsB = 128;  // filter rows (complex outputs) per tile
-constexpr int kStages = 4;
-constexpr int kStageBytes = (kRowsA + kRowsB) * kBK * 2;
-constexpr int kMaxKTiles = 256;  // K' <= 8192
+constexpr int kMaxKp = 8192;  // 2 S_in C_in
 
 struct Spins {
   int s[kMaxSpins];
@@ -34,9 +33,14 @@ struct Spins {
 
 __device__ __forceinline__ int iabs_(int v) { return v < 0 ? -v : v; }
 
-// LDS slot of 16-byte chunk c of tile row r: chunks are XOR-swizzled so that
-// the 32 rows one MFMA operand read touches fall in distinct banks.
-__device__ __forceinline__ int swz(int r, int c) { return c ^ (((r >> 1) ^ (r >> 3)) & 3); }
+// LDS slot of 16-byte chunk c of tile row r (CPR chunks per row): chunks are
+// XOR-swizzled so that the rows one MFMA operand read touches fall in
+// distinct banks, for 8- and for 16-lane groups of a 16-byte read.
+template <int CPR>
+__device__ __forceinline__ int swz(int r, int c) {
+  if constexpr (CPR == 4) return c ^ (((r >> 1) ^ (r >> 3)) & 3);
+  else return c ^ ((r & 7) ^ ((r >> 3) & 1));
+}
 
 // One direct global -> LDS copy of 16 bytes per lane: lane l writes
 // LDS[lds_base + 16 l].  M0 holds the wave-uniform LDS base (with the NOP
@@ -50,23 +54,54 @@ __device__ __forceinline__ void dma16(const void* g, unsigned lds_base) {
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 16, "vmcnt immediate");
+  static_assert(N >= 0 && N < 64, "vmcnt immediate");
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-__global__ void __launch_bounds__(kNT) mix_dma_kernel(const __bf16* __restrict__ coef,
-                                                      const __bf16* __restrict__ K,
-                                                      __bf16* __restrict__ out, int L, int B,
-                                                      int Cin, int Cout, int Sin, int Sout,
-                                                      Spins sin_, Spins sout_) {
-  __shared__ __align__(16) unsigned char ring[kStages * kStageBytes];
-  __shared__ int live[kMaxKTiles];
+// Wait until at most `ahead` groups of P copies are outstanding (ahead <= A).
+template <int A, int P>
+__device__ __forceinline__ void wait_groups(int ahead) {
+  if constexpr (A == 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (ahead >= A) wait_vmcnt<A * P>();
+    else wait_groups<A - 1, P>(ahead);
+  }
+}
+
+template <int BK, int RA, int RB, int ST>
+struct MixGeom {
+  static constexpr int WM = 2 * RA / 64, WN = RB / 64;
+  static constexpr int NW = WM * WN, NT = 64 * NW;  // waves, threads
+  static constexpr int PITCH = 2 * BK;               // bytes per tile row
+  static constexpr int CPR = PITCH / 16;             // 16-byte chunks per row
+  static constexpr int RPI = 1024 / PITCH;           // rows per 1 KiB copy
+  static constexpr int LPR = 64 / RPI;               // lanes per row
+  static constexpr int NI = (RA + RB) / RPI;         // copies per stage
+  static constexpr int PER_WAVE = NI / NW;
+  static constexpr int STAGE = (RA + RB) * PITCH;
+  static constexpr int LDC = 2 * RB + 8;  // bf16 per row of the epilogue tile
+  static constexpr int RING = ST * STAGE, CTILE = RA * LDC * 2;
+  static constexpr int SMEM = RING > CTILE ? RING : CTILE;
+  static constexpr int MAX_KT = kMaxKp / BK;
+  static_assert(RA % RPI == 0 && NI % NW == 0 && RA % 32 == 0 && RB % 64 == 0, "tile shape");
+  static_assert(ST >= 2 && (ST - 2) * PER_WAVE < 64, "stages");
+};
+
+template <int BK, int RA, int RB, int ST>
+__global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
+    mix_dma_kernel(const __bf16* __restrict__ coef, const __bf16* __restrict__ K,
+                   __bf16* __restrict__ out, int L, int B, int Cin, int Cout, int Sin, int Sout,
+                   Spins sin_, Spins sout_) {
+  using G = MixGeom<BK, RA, RB, ST>;
+  __shared__ __align__(16) unsigned char smem[G::SMEM];
+  __shared__ int live[G::MAX_KT];
   __shared__ int n_live_s;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;  // 2 x 2 waves, 64 expanded rows x 64 cols each
+  const int wm = wave / G::WN, wn = wave % G::WN;
   const int Kc = Sin * Cin, Nc = Sout * Cout;
   const int Kp = 2 * Kc;
-  const int n_tiles_n = (Nc + kRowsB - 1) / kRowsB;
+  const int n_tiles_n = (Nc + RB - 1) / RB;
 
   // logical block = ((l, row tile), column tile), largest degrees first
   int lbk = xcd_logical_block();
@@ -74,18 +109,18 @@ __global__ void __launch_bounds__(kNT) mix_dma_kernel(const __bf16* __restrict__
   int t = lbk / n_tiles_n;
   int l = L - 1;
   for (; l >= 0; --l) {
-    const int ntl = ((2 * l + 1) * B + kRowsA - 1) / kRowsA;
+    const int ntl = ((2 * l + 1) * B + RA - 1) / RA;
     if (t < ntl) break;
     t -= ntl;
   }
   if (l < 0) return;
   const int Mrows = (2 * l + 1) * B;
-  const int row0 = t * kRowsA;
-  const int q0 = ntile * kRowsB;
+  const int row0 = t * RA;
+  const int q0 = ntile * RB;
 
   // K steps of input spins that exist at this degree (whole channel blocks)
   if (tid == 0) {
-    const int per_spin = 2 * Cin / kBK;
+    const int per_spin = 2 * Cin / BK;
     int n = 0;
     for (int si = 0; si < Sin; ++si)
       if (iabs_(sin_.s[si]) <= l)
@@ -97,28 +132,32 @@ __global__ void __launch_bounds__(kNT) mix_dma_kernel(const __bf16* __restrict__
 
   const __bf16* A0 = coef + (size_t)l * l * B * Kp;  // rows (m, b) of degree l
   const __bf16* K0 = K + (size_t)l * Nc * Kp;        // filter rows q of degree l
-  const unsigned ring_base = (unsigned)(uintptr_t)ring;
+  const unsigned ring_base = (unsigned)(uintptr_t)smem;
 
-  // each wave copies 16 rows (one 1 KiB instruction) of A and 32 rows of B
-  const int ra = wave * 16 + (lane >> 2);
-  const int slot = lane & 3;
-  const int rowA = row0 + ra < Mrows ? row0 + ra : Mrows - 1;  // clamp: rows past the end are discarded
-  const __bf16* gA = A0 + (size_t)rowA * Kp + swz(ra, slot) * 8;
-  const __bf16* gB[2];
+  // copy g = wave * PER_WAVE + u moves tile rows [g RPI, (g + 1) RPI) of the
+  // stage [A rows; B rows]; rows past the end of the matrix are clamped to
+  // its last row (their products are discarded)
+  const __bf16* gsrc[G::PER_WAVE];
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int rb = wave * 32 + h * 16 + (lane >> 2);
-    const int q = q0 + rb < Nc ? q0 + rb : Nc - 1;
-    gB[h] = K0 + (size_t)q * Kp + swz(rb, slot) * 8;
+  for (int u = 0; u < G::PER_WAVE; ++u) {
+    const int g = wave * G::PER_WAVE + u;
+    const int tr = g * G::RPI + lane / G::LPR;  // row of the stage
+    const int slot = lane % G::LPR;
+    if (tr < RA) {
+      const int row = row0 + tr < Mrows ? row0 + tr : Mrows - 1;
+      gsrc[u] = A0 + (size_t)row * Kp + swz<G::CPR>(tr, slot) * 8;
+    } else {
+      const int rb = tr - RA;
+      const int q = q0 + rb < Nc ? q0 + rb : Nc - 1;
+      gsrc[u] = K0 + (size_t)q * Kp + swz<G::CPR>(rb, slot) * 8;
+    }
   }
   auto issue = [&](int i, int stage) {
-    const int koff = live[i] * kBK;
-    const unsigned base = ring_base + stage * kStageBytes;
-    dma16(gA + koff, base + wave * 16 * 64);
-    dma16(gB[0] + koff, base + kRowsA * 64 + (wave * 32) * 64);
-    dma16(gB[1] + koff, base + kRowsA * 64 + (wave * 32 + 16) * 64);
+    const int koff = live[i] * BK;
+    const unsigned base = ring_base + stage * G::STAGE + wave * G::PER_WAVE * 1024;
+#pragma unroll
+    for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + koff, base + u * 1024);
   };
-  constexpr int kPerTile = 3;  // DMA instructions per wave per K step
 
   typedef unsigned v4u __attribute__((ext_vector_type(4)));
   v16f acc[2][2];
@@ -129,37 +168,32 @@ __global__ void __launch_bounds__(kNT) mix_dma_kernel(const __bf16* __restrict__
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // prologue: K steps 0 .. kStages-2 in flight
+  // prologue: K steps 0 .. ST-2 in flight
 #pragma unroll
-  for (int s = 0; s < kStages - 1; ++s)
+  for (int s = 0; s < ST - 1; ++s)
     if (s < nk) issue(s, s);
 
   const int r32 = lane & 31, kh = lane >> 5;
+  // odd expanded rows (im, re): rotate by 16 bits; even rows (re, -im): flip
+  // the high half's sign (the row parity is the lane parity)
   const unsigned rot = (lane & 1) ? 16u : 0u;
   const unsigned sgn = (lane & 1) ? 0u : 0x80000000u;
   for (int i = 0; i < nk; ++i) {
     // K step i has landed once at most (issued - i - 1) steps are outstanding
-    const int issued = nk < i + kStages - 1 ? nk : i + kStages - 1;
-    const int ahead = issued - i - 1;
-    if (ahead >= 2) wait_vmcnt<2 * kPerTile>();
-    else if (ahead == 1) wait_vmcnt<kPerTile>();
-    else wait_vmcnt<0>();
+    const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
+    wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
     __builtin_amdgcn_s_barrier();  // every wave's copies of step i landed; step i-1 is consumed
-    if (i + kStages - 1 < nk) issue(i + kStages - 1, (i + kStages - 1) % kStages);
-    const unsigned char* st = ring + (i % kStages) * kStageBytes;
-    const unsigned char* As = st;
-    const unsigned char* Bs = st + kRowsA * 64;
+    if (i + ST - 1 < nk) issue(i + ST - 1, (i + ST - 1) % ST);
+    const unsigned char* As = smem + (i % ST) * G::STAGE;
+    const unsigned char* Bs = As + RA * G::PITCH;
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {  // two 16-wide MFMA K steps per 32-wide tile
+    for (int kk = 0; kk < BK / 16; ++kk) {  // 16-wide MFMA K steps
       const int c = 2 * kk + kh;
       v8bf a[2], b[2];
 #pragma unroll
       for (int ii = 0; ii < 2; ++ii) {
-        const int er = wm * 64 + ii * 32 + r32;  // expanded GEMM row
-        const int cr = er >> 1;                  // coefficient row in the tile
-        v4u x = *reinterpret_cast<const v4u*>(As + cr * 64 + swz(cr, c) * 16);
-        // odd rows (im, re): rotate by 16 bits; even rows (re, -im): flip the
-        // high half's sign (er & 1 == lane & 1, selected without branches)
+        const int cr = (wm * 64 + ii * 32 + r32) >> 1;  // coefficient row of the expanded row
+        const v4u x = *reinterpret_cast<const v4u*>(As + cr * G::PITCH + swz<G::CPR>(cr, c) * 16);
         v4u y;
 #pragma unroll
         for (int d = 0; d < 4; ++d) y[d] = __builtin_amdgcn_alignbit(x[d], x[d], rot) ^ sgn;
@@ -168,7 +202,7 @@ __global__ void __launch_bounds__(kNT) mix_dma_kernel(const __bf16* __restrict__
 #pragma unroll
       for (int jj = 0; jj < 2; ++jj) {
         const int rb = wn * 64 + jj * 32 + r32;
-        b[jj] = *reinterpret_cast<const v8bf*>(Bs + rb * 64 + swz(rb, c) * 16);
+        b[jj] = *reinterpret_cast<const v8bf*>(Bs + rb * G::PITCH + swz<G::CPR>(rb, c) * 16);
       }
 #pragma unroll
       for (int ii = 0; ii < 2; ++ii)
@@ -181,8 +215,7 @@ __global__ void __launch_bounds__(kNT) mix_dma_kernel(const __bf16* __restrict__
   __syncthreads();
 
   // epilogue: C[er][q] -> out row (row0 + er/2), real column 2q + er%2, via LDS
-  constexpr int LDC = 2 * kRowsB + 8;  // bf16 per LDS row
-  __bf16* cs = reinterpret_cast<__bf16*>(ring);
+  __bf16* cs = reinterpret_cast<__bf16*>(smem);
   const int col_l = lane & 31, row_l = 4 * (lane >> 5);
 #pragma unroll
   for (int ii = 0; ii < 2; ++ii)
@@ -192,19 +225,19 @@ __global__ void __launch_bounds__(kNT) mix_dma_kernel(const __bf16* __restrict__
       for (int r = 0; r < 16; ++r) {
         const int er = wm * 64 + ii * 32 + 8 * (r >> 2) + row_l + (r & 3);
         const int q = wn * 64 + jj * 32 + col_l;
-        cs[(er >> 1) * LDC + 2 * q + (er & 1)] = (__bf16)acc[ii][jj][r];
+        cs[(er >> 1) * G::LDC + 2 * q + (er & 1)] = (__bf16)acc[ii][jj][r];
       }
   __syncthreads();
   const int Np = 2 * Nc;
   __bf16* O0 = out + ((size_t)l * l * B + row0) * Np + 2 * q0;
-  const int rows = Mrows - row0 < kRowsA ? Mrows - row0 : kRowsA;
-  const int cols = 2 * (Nc - q0 < kRowsB ? Nc - q0 : kRowsB);
-  constexpr int VPR = 2 * kRowsB / 8;
-  for (int idx = tid; idx < kRowsA * VPR; idx += kNT) {
+  const int rows = Mrows - row0 < RA ? Mrows - row0 : RA;
+  const int cols = 2 * (Nc - q0 < RB ? Nc - q0 : RB);
+  constexpr int VPR = 2 * RB / 8;
+  for (int idx = tid; idx < RA * VPR; idx += G::NT) {
     const int row = idx / VPR;
     const int col = (idx % VPR) * 8;
     if (row >= rows || col >= cols) continue;
-    uint4 v = *reinterpret_cast<const uint4*>(&cs[row * LDC + col]);
+    uint4 v = *reinterpret_cast<const uint4*>(&cs[row * G::LDC + col]);
     // output spins that do not exist at this degree are zero
     const int tq = (q0 + col / 2) / Cout;  // 8 reals = 4 complex outputs, one spin (Cout % 4 == 0)
     if (iabs_(sout_.s[tq]) > l) v = make_uint4(0, 0, 0, 0);
@@ -212,27 +245,53 @@ __global__ void __launch_bounds__(kNT) mix_dma_kernel(const __bf16* __restrict__
   }
 }
 
+template <int BK, int RA, int RB, int ST>
+hipError_t launch_geom(const Plan& p, int B, int Cin, int Cout, const void* coef, const void* K,
+                       void* out, hipStream_t st) {
+  using G = MixGeom<BK, RA, RB, ST>;
+  Spins si{}, so{};
+  for (int i = 0; i < p.n_in; ++i) si.s[i] = p.spins_in[i];
+  for (int i = 0; i < p.n_out; ++i) so.s[i] = p.spins_out[i];
+  int tiles = 0;
+  for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + RA - 1) / RA;
+  const int Nc = p.n_out * Cout;
+  const long long blocks = (long long)tiles * ((Nc + RB - 1) / RB);
+  hipLaunchKernelGGL((mix_dma_kernel<BK, RA, RB, ST>), dim3(xcd_grid(blocks)), dim3(G::NT), 0,
+                     st, (const __bf16*)coef, (const __bf16*)K, (__bf16*)out, p.L, B, Cin, Cout,
+                     p.n_in, p.n_out, si, so);
+  return hipGetLastError();
+}
+
+// Tile shape: 128 coefficient rows x 128 outputs, two 64-wide K steps
+// resident (two workgroups of 8 waves per CU); channel counts that are a
+// multiple of 16 but not of 32 take 32-wide K steps.
+#ifndef SWSFT_MIX_DMA_BK
+#define SWSFT_MIX_DMA_BK 64
+#endif
+#ifndef SWSFT_MIX_DMA_RA
+#define SWSFT_MIX_DMA_RA 128
+#endif
+#ifndef SWSFT_MIX_DMA_RB
+#define SWSFT_MIX_DMA_RB 128
+#endif
+#ifndef SWSFT_MIX_DMA_STAGES
+#define SWSFT_MIX_DMA_STAGES 2
+#endif
+
 }  // namespace
 
 bool mix_dma_supported(const Plan& p, int Cin, int Cout) {
-  const int Kp = 2 * p.n_in * Cin;
-  return p.dtype == SWSFT_BF16 && (2 * Cin) % kBK == 0 && Kp / kBK <= kMaxKTiles &&
+  return p.dtype == SWSFT_BF16 && (2 * Cin) % 32 == 0 && 2 * p.n_in * Cin <= kMaxKp &&
          Cout % 4 == 0;
 }
 
 hipError_t launch_mix_dma(const Plan& p, int B, int Cin, int Cout, const void* coef,
                           const void* K, void* out, hipStream_t st) {
-  Spins si{}, so{};
-  for (int i = 0; i < p.n_in; ++i) si.s[i] = p.spins_in[i];
-  for (int i = 0; i < p.n_out; ++i) so.s[i] = p.spins_out[i];
-  int tiles = 0;
-  for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + kRowsA - 1) / kRowsA;
-  const int Nc = p.n_out * Cout;
-  const long long blocks = (long long)tiles * ((Nc + kRowsB - 1) / kRowsB);
-  hipLaunchKernelGGL(mix_dma_kernel, dim3(xcd_grid(blocks)), dim3(kNT), 0, st,
-                     (const __bf16*)coef, (const __bf16*)K, (__bf16*)out, p.L, B, Cin, Cout,
-                     p.n_in, p.n_out, si, so);
-  return hipGetLastError();
+  if ((2 * Cin) % SWSFT_MIX_DMA_BK == 0)
+    return launch_geom<SWSFT_MIX_DMA_BK, SWSFT_MIX_DMA_RA, SWSFT_MIX_DMA_RB, SWSFT_MIX_DMA_STAGES>(
+        p, B, Cin, Cout, coef, K, out, st);
+  return launch_geom<32, SWSFT_MIX_DMA_RA, SWSFT_MIX_DMA_RB, 2 * SWSFT_MIX_DMA_STAGES>(
+      p, B, Cin, Cout, coef, K, out, st);
 }
 
 }  // namespace swsft

@@ -162,9 +162,11 @@ EDGE = [
     (4, 2, (0, 1), (1,), 1, 4, 2, "f32"),
     (8, 4, (0,), (0, 1), 5, 7, 9, "bf16"),
     (32, 16, (0, 1), (0, 1), 2, 40, 24, "bf16"),
-    # bf16 mixing through the direct-to-LDS kernel (2 C_in a multiple of 32):
-    (32, 16, (0, 1), (0, 1, -1), 3, 16, 44, "bf16"),  # ragged row tiles, 2 column tiles (last 4 wide)
-    (16, 8, (0, 1, -2), (2, 0), 5, 48, 12, "bf16"),   # input spin |s| = 2 skipped below l = 2
+    # bf16 mixing through the direct-to-LDS kernels (64-wide K steps when
+    # 2 C_in % 64 == 0, else 32-wide):
+    (32, 16, (0, 1), (0, 1, -1), 3, 32, 44, "bf16"),  # ragged row tiles, 2 column tiles (last 4 wide)
+    (16, 8, (-2, 0), (0, 1), 3, 64, 8, "bf16"),       # input spin |s| = 2 skipped below l = 2
+    (16, 8, (0, 1, -2), (2, 0), 5, 48, 12, "bf16"),   # 32-wide K steps, 3 per input spin
     (64, 32, (1,), (0, -1), 1, 33, 17, "f32"),     # ragged tiles everywhere
     (64, 20, (0,), (0,), 3, 8, 8, "f32"),          # spectral truncation L << H/2
 ]
