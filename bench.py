@@ -5,6 +5,7 @@ spins {0,1} -> {0,1}, 256 -> 256 channels, bfloat16 storage with float32
 accumulation (the large weather-shaped workload).
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+    python bench.py --summarize-counters FETCH_CSV WRITE_CSV
 
 Prints one JSON line.  A step is one layer call (forward transform, per-degree
 mixing, inverse transform) on inputs resident in HBM.  `value` is layer calls
@@ -22,6 +23,7 @@ import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -40,7 +42,7 @@ def stage_work(w):
     degree ranges (l >= max(|m|, |s|)) and spins that exist at a degree.
     Bytes count one read of every operand and one write of every result in
     the storage type; X and Y are the longitude spectra between the DFT and
-    latitude stages, [S][2L-1][B C][H] complex.
+    latitude stages, S (2L-1) B C H complex values.
     """
     e = 2 if w.dtype == "bf16" else 4
     H, W, L, B = w.H, w.W, w.L, w.B
@@ -93,6 +95,59 @@ def measured_traffic(kernel: str):
         return None
     k = rec.get("kernels", {}).get(kernel)
     return None if k is None else k.get("hbm_bytes_per_launch")
+
+
+STAGE_KERNELS = re.compile(r"(dft_fwd|dft_inv|lat_fwd|lat_inv|mix)(?:_dma)?_kernel")
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+COPY_BYTES = 1 << 30
+
+
+def summarize_counters(fetch_csv: str, write_csv: str, out_path: str) -> dict:
+    """HBM bytes per launch of each stage kernel from two rocprofv3 counter
+    runs of this script (FETCH_SIZE, then WRITE_SIZE, both with
+    --copy-calibration).  Each counter (KiB per dispatch) is scaled by what it
+    reads for the plain 1 GiB device copy in the same run; the median over a
+    kernel's dispatches is kept."""
+    import csv
+    import statistics
+
+    def per_kernel(path, counter):
+        vals, copies = {}, []
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] != counter:
+                    continue
+                v = float(r["Counter_Value"]) * 1024.0
+                if r["Kernel_Name"].startswith(COPY_KERNEL):
+                    copies.append(v)
+                    continue
+                m = STAGE_KERNELS.search(r["Kernel_Name"])
+                if m:
+                    vals.setdefault(m.group(1), []).append(v)
+        if not copies:
+            raise SystemExit(f"{path}: no {COPY_KERNEL} dispatch (run with --copy-calibration)")
+        scale = COPY_BYTES / max(copies)  # the 1 GiB copy is the largest one
+        return {k: statistics.median(v) for k, v in vals.items()}, scale, len(copies)
+
+    fetch, f_scale, _ = per_kernel(fetch_csv, "FETCH_SIZE")
+    write, w_scale, _ = per_kernel(write_csv, "WRITE_SIZE")
+    rec = {
+        "source_digest": source_digest(),
+        "workload": "wx256",
+        "calibration": {"kernel": COPY_KERNEL, "bytes": COPY_BYTES,
+                        "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)},
+        "kernels": {},
+    }
+    for k in sorted(set(fetch) & set(write)):
+        rd, wr = fetch[k] * f_scale, write[k] * w_scale
+        rec["kernels"][k] = {"fetch_kib": round(fetch[k] / 1024, 1),
+                             "write_kib": round(write[k] / 1024, 1),
+                             "hbm_read_bytes": int(rd), "hbm_write_bytes": int(wr),
+                             "hbm_bytes_per_launch": int(rd + wr)}
+    with open(out_path, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    return rec
 
 
 def cpu_baseline(w, runs: int = 3):
@@ -151,10 +206,16 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (for counter calibration)")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/traffic_<workload>.json from two counter runs and exit")
     args = ap.parse_args(argv)
+    if args.summarize_counters:
+        out = os.path.join(ROOT, "profiles", f"traffic_{args.workload}.json")
+        print(json.dumps(summarize_counters(*args.summarize_counters, out)))
+        return 0
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on one GPU only (the layer has no multi-GPU "
-              "path); run with --gpus 1", file=sys.stderr)
+        print("bench.py: the layer runs on one GPU only (it has no multi-GPU path); "
+              "run with --gpus 1", file=sys.stderr)
         return 2
 
     import torch
