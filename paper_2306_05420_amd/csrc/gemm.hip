@@ -677,19 +677,20 @@ hipError_t lat_inv_t(const Plan& p, int B, int C, const void* coef, void* Y, hip
 
 }  // namespace
 
+#ifndef SWSFT_DMA
+#define SWSFT_DMA 1
+#endif
+
 hipError_t launch_lat_fwd(const Plan& p, int B, int C, const void* X, void* coef,
                           hipStream_t st) {
+  if (SWSFT_DMA && lat_fwd_dma_supported(p, B, C)) return launch_lat_fwd_dma(p, B, C, X, coef, st);
   if (p.dtype == SWSFT_BF16) return lat_fwd_t<__bf16>(p, B, C, X, coef, st);
   return lat_fwd_t<float>(p, B, C, X, coef, st);
 }
 
-#ifndef SWSFT_MIX_DMA
-#define SWSFT_MIX_DMA 1
-#endif
-
 hipError_t launch_mix(const Plan& p, int B, int Cin, int Cout, const void* coef, const void* K,
                       void* out, hipStream_t st) {
-  if (SWSFT_MIX_DMA && mix_dma_supported(p, Cin, Cout))
+  if (SWSFT_DMA && mix_dma_supported(p, Cin, Cout))
     return launch_mix_dma(p, B, Cin, Cout, coef, K, out, st);
   if (p.dtype == SWSFT_BF16) return mix_t<__bf16>(p, B, Cin, Cout, coef, K, out, st);
   return mix_t<float>(p, B, Cin, Cout, coef, K, out, st);
@@ -697,6 +698,7 @@ hipError_t launch_mix(const Plan& p, int B, int Cin, int Cout, const void* coef,
 
 hipError_t launch_lat_inv(const Plan& p, int B, int C, const void* coef, void* Y,
                           hipStream_t st) {
+  if (SWSFT_DMA && lat_inv_dma_supported(p, B, C)) return launch_lat_inv_dma(p, B, C, coef, Y, st);
   if (p.dtype == SWSFT_BF16) return lat_inv_t<__bf16>(p, B, C, coef, Y, st);
   return lat_inv_t<float>(p, B, C, coef, Y, st);
 }

@@ -18,6 +18,7 @@
 //
 // Preconditions (checked by the launcher): bf16, K' = 2 S_in C_in with each
 // input spin's channel block a whole number of BK-wide K steps, C_out % 4 == 0.
+#include "lds_dma.h"
 #include "mfma_tile.h"
 #include "swsft_internal.h"
 #include "xcd.h"
@@ -32,42 +33,6 @@ struct Spins {
 };
 
 __device__ __forceinline__ int iabs_(int v) { return v < 0 ? -v : v; }
-
-// LDS slot of 16-byte chunk c of tile row r (CPR chunks per row): chunks are
-// XOR-swizzled so that the rows one MFMA operand read touches fall in
-// distinct banks, for 8- and for 16-lane groups of a 16-byte read.
-template <int CPR>
-__device__ __forceinline__ int swz(int r, int c) {
-  if constexpr (CPR == 4) return c ^ (((r >> 1) ^ (r >> 3)) & 3);
-  else return c ^ ((r & 7) ^ ((r >> 3) & 1));
-}
-
-// One direct global -> LDS copy of 16 bytes per lane: lane l writes
-// LDS[lds_base + 16 l].  M0 holds the wave-uniform LDS base (with the NOP
-// its write requires before the copy).
-__device__ __forceinline__ void dma16(const void* g, unsigned lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-               :
-               : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(g)
-               : "memory");
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt immediate");
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// Wait until at most `ahead` groups of P copies are outstanding (ahead <= A).
-template <int A, int P>
-__device__ __forceinline__ void wait_groups(int ahead) {
-  if constexpr (A == 0) {
-    wait_vmcnt<0>();
-  } else {
-    if (ahead >= A) wait_vmcnt<A * P>();
-    else wait_groups<A - 1, P>(ahead);
-  }
-}
 
 template <int BK, int RA, int RB, int ST>
 struct MixGeom {
@@ -132,7 +97,7 @@ __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
 
   const __bf16* A0 = coef + (size_t)l * l * B * Kp;  // rows (m, b) of degree l
   const __bf16* K0 = K + (size_t)l * Nc * Kp;        // filter rows q of degree l
-  const unsigned ring_base = (unsigned)(uintptr_t)smem;
+  const unsigned ring_base = lds_addr(smem);
 
   // copy g = wave * PER_WAVE + u moves tile rows [g RPI, (g + 1) RPI) of the
   // stage [A rows; B rows]; rows past the end of the matrix are clamped to

@@ -180,7 +180,7 @@ swsft_status swsft_plan_create(int H, int W, int L, const int* spins_in, int n_s
   SWSFT_TRY(check_spins(spins_in, n_spins_in, L, "spins_in"));
   SWSFT_TRY(check_spins(spins_out, n_spins_out, L, "spins_out"));
   if (!is_pow2(W) || W > 512)
-    return fail(SWSFT_E_UNSUPPORTED, "W = %d: this build implements powers of two up to 512", W);
+    return fail(SWSFT_E_UNSUPPORTED, "W = %d: only powers of two up to 512 are implemented", W);
 
   Plan* p = new (std::nothrow) swsft_plan_s();
   if (p == nullptr) return fail(SWSFT_E_ALLOC, "host allocation of the plan failed");

@@ -81,6 +81,13 @@ hipError_t launch_lat_inv(const Plan& p, int B, int C, const void* coef, void* Y
 // coef [L^2][B][S_in][C_in] x K -> coef' [L^2][B][S_out][C_out]
 hipError_t launch_mix(const Plan& p, int B, int C_in, int C_out, const void* coef,
                       const void* K, void* coef_out, hipStream_t st);
+// bf16 latitude GEMMs fed by direct global -> LDS copies (see lat_dma.hip).
+bool lat_fwd_dma_supported(const Plan& p, int B, int C);
+bool lat_inv_dma_supported(const Plan& p, int B, int C);
+hipError_t launch_lat_fwd_dma(const Plan& p, int B, int C, const void* X, void* coef,
+                              hipStream_t st);
+hipError_t launch_lat_inv_dma(const Plan& p, int B, int C, const void* coef, void* Y,
+                              hipStream_t st);
 // bf16 mixing fed by direct global -> LDS copies (see mix_dma.hip).
 bool mix_dma_supported(const Plan& p, int C_in, int C_out);
 hipError_t launch_mix_dma(const Plan& p, int B, int C_in, int C_out, const void* coef,

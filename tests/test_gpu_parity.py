@@ -167,6 +167,9 @@ EDGE = [
     (32, 16, (0, 1), (0, 1, -1), 3, 32, 44, "bf16"),  # ragged row tiles, 2 column tiles (last 4 wide)
     (16, 8, (-2, 0), (0, 1), 3, 64, 8, "bf16"),       # input spin |s| = 2 skipped below l = 2
     (16, 8, (0, 1, -2), (2, 0), 5, 48, 12, "bf16"),   # 32-wide K steps, 3 per input spin
+    # bf16 latitude GEMMs through the direct-to-LDS kernels (H a multiple of 64):
+    (64, 32, (0,), (0, 1), 2, 20, 64, "bf16"),        # ragged forward columns, H < one latitude tile
+    (64, 32, (1, -2), (2, 0), 2, 64, 64, "bf16"),     # |s| = 2: degree ranges start at max(|m|, |s|)
     (64, 32, (1,), (0, -1), 1, 33, 17, "f32"),     # ragged tiles everywhere
     (64, 20, (0,), (0,), 3, 8, 8, "f32"),          # spectral truncation L << H/2
 ]
