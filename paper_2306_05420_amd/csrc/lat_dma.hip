@@ -359,11 +359,19 @@ __global__ void __launch_bounds__((InvGeom<RA, RB, ST>::NT))
   }
 }
 
+// forward: BK, rows l, columns n', stages; the wide tile when 2BC allows it
+#ifndef SWSFT_LAT_FWD_DMA_WIDE
+#define SWSFT_LAT_FWD_DMA_WIDE 32, 128, 256, 3
+#endif
 #ifndef SWSFT_LAT_FWD_DMA
-#define SWSFT_LAT_FWD_DMA 64, 128, 128, 2  // BK, rows l, columns n', stages
+#define SWSFT_LAT_FWD_DMA 32, 128, 128, 3
+#endif
+// inverse: rows n', columns j, stages; the wide tile when 2C allows it
+#ifndef SWSFT_LAT_INV_DMA_WIDE
+#define SWSFT_LAT_INV_DMA_WIDE 256, 128, 3
 #endif
 #ifndef SWSFT_LAT_INV_DMA
-#define SWSFT_LAT_INV_DMA 128, 128, 3  // rows n', columns j, stages
+#define SWSFT_LAT_INV_DMA 128, 128, 3
 #endif
 
 template <int BK, int RA, int RB, int ST>
@@ -393,6 +401,8 @@ hipError_t inv_geom(const Plan& p, int B, int C, const void* coef, void* Y, hipS
 
 template <int BK, int RA, int RB, int ST>
 constexpr int fwd_bk(int) { return BK; }
+template <int BK, int RA, int RB, int ST>
+constexpr int fwd_rb(int) { return RB; }
 template <int RA, int RB, int ST>
 constexpr int inv_ra(int) { return RA; }
 
@@ -400,23 +410,29 @@ constexpr int inv_ra(int) { return RA; }
 
 bool lat_fwd_dma_supported(const Plan& p, int B, int C) {
   constexpr int BK = fwd_bk<SWSFT_LAT_FWD_DMA>(0);
+  static_assert(fwd_bk<SWSFT_LAT_FWD_DMA_WIDE>(0) == BK, "wide tile");
   return p.dtype == SWSFT_BF16 && p.H >= BK && p.H % BK == 0 && p.Hp == p.H && p.JT == kJT &&
          (2 * C) % 8 == 0;
 }
 
 bool lat_inv_dma_supported(const Plan& p, int B, int C) {
   constexpr int RA = inv_ra<SWSFT_LAT_INV_DMA>(0);
+  static_assert(inv_ra<SWSFT_LAT_INV_DMA_WIDE>(0) % RA == 0, "wide tile");
   return p.dtype == SWSFT_BF16 && p.H % kJT == 0 && p.JT == kJT && (2 * C) % RA == 0 &&
          p.Lp % InvGeom<SWSFT_LAT_INV_DMA>::BK == 0 && p.Hp == p.H;
 }
 
 hipError_t launch_lat_fwd_dma(const Plan& p, int B, int C, const void* X, void* coef,
                               hipStream_t st) {
+  if ((2 * B * C) % fwd_rb<SWSFT_LAT_FWD_DMA_WIDE>(0) == 0)
+    return fwd_geom<SWSFT_LAT_FWD_DMA_WIDE>(p, B, C, X, coef, st);
   return fwd_geom<SWSFT_LAT_FWD_DMA>(p, B, C, X, coef, st);
 }
 
 hipError_t launch_lat_inv_dma(const Plan& p, int B, int C, const void* coef, void* Y,
                               hipStream_t st) {
+  if ((2 * C) % inv_ra<SWSFT_LAT_INV_DMA_WIDE>(0) == 0)
+    return inv_geom<SWSFT_LAT_INV_DMA_WIDE>(p, B, C, coef, Y, st);
   return inv_geom<SWSFT_LAT_INV_DMA>(p, B, C, coef, Y, st);
 }
 
