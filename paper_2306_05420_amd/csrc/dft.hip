@@ -5,7 +5,8 @@
 // for orders |m| < L, n = b*C + c.  This is the e^{i m phi} factor of the
 // harmonics in eqs. (2)-(3); the paper evaluates it as a dense DFT matrix
 // product on TPU (Method, "Efficient TPU implementation"), here it is an
-// in-register FFT because the stage is bound by HBM traffic, not flops.
+// in-register FFT because the stage is bound by HBM traffic and VALU issue,
+// not by flops.
 //
 // One workgroup handles JB consecutive rows j of one map.  Each row of W
 // samples is split W = W1 * W2: W1 threads per row, each holding W2 samples
@@ -16,6 +17,11 @@
 // of the latitude GEMM, is contiguous within a tile, and one tile of all
 // maps is one contiguous block, so the GEMM reads whole 8 KiB blocks per K
 // step and a block of rows of one map writes 128-byte runs.
+//
+// The grid is square (H == W), so the whole workgroup geometry is a
+// compile-time function of W (index arithmetic folds to shifts), and a
+// thread transforms NP adjacent rows: their values at one order are adjacent
+// in the stage, so bfloat16 pairs move as one 32-bit LDS access.
 #include "fft_reg.h"
 #include "swsft_internal.h"
 #include "xcd.h"
@@ -23,37 +29,36 @@
 namespace swsft {
 namespace {
 
-template <typename T>
-struct CplxIO;
-template <>
-struct CplxIO<float> {
-  static __device__ __forceinline__ float2 load(const float* p, size_t i) {
-    return reinterpret_cast<const float2*>(p)[i];
-  }
-  static __device__ __forceinline__ void store(float* p, size_t i, float2 v) {
-    reinterpret_cast<float2*>(p)[i] = v;
-  }
-};
-template <>
-struct CplxIO<__bf16> {
-  static __device__ __forceinline__ float2 load(const __bf16* p, size_t i) {
-    const uint32_t u = reinterpret_cast<const uint32_t*>(p)[i];
-    return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
-  }
-  static __device__ __forceinline__ void store(__bf16* p, size_t i, float2 v) {
-    __bf16 r = (__bf16)v.x, q = (__bf16)v.y;
-    const uint32_t u = (uint32_t)__builtin_bit_cast(uint16_t, r) |
-                       ((uint32_t)__builtin_bit_cast(uint16_t, q) << 16);
-    reinterpret_cast<uint32_t*>(p)[i] = u;
-  }
+#ifndef SWSFT_DFT_THREADS
+#define SWSFT_DFT_THREADS 256
+#endif
+
+// Workgroup geometry for a length-W transform (W = W1 * W2, H = W rows).
+template <int W1_, int W2_>
+struct DftGeom {
+  static constexpr int W1 = W1_, W2 = W2_, W = W1 * W2;
+  static constexpr int RPP = SWSFT_DFT_THREADS / W1 < W ? SWSFT_DFT_THREADS / W1 : W;  // rows per pass
+  static constexpr int NP = (RPP < 32 && 2 * RPP <= W) ? 2 : 1;  // passes (rows per thread)
+  static constexpr int JB = RPP * NP;                            // rows per workgroup (== JT)
+  static constexpr int NT = RPP * W1;
+  static constexpr size_t ex_bytes = (size_t)RPP * W2 * (W1 + 1) * sizeof(float2);
+  static_assert(W2 % W1 == 0 && W % JB == 0, "geometry");
 };
 
 // Row pitch (elements) of the [m][re/im][j] staging buffer: a multiple of
 // 16 bytes so whole 16-byte vectors move between LDS and HBM, and an odd
 // multiple of 16 bytes so consecutive orders start in different banks.
-template <typename T>
-constexpr int stage_pitch(int JB) {
+template <typename T, int JB>
+constexpr int stage_pitch() {
   return sizeof(T) == 4 ? 2 * JB + 4 : 2 * JB + 8;
+}
+
+// Bytes of the shared allocation: the exchange buffer (during the FFTs) and
+// the stage of M orders plus one spare row (after them) share it.
+template <typename T, class G>
+size_t dft_lds_bytes(int M) {
+  const size_t stage = (size_t)(M + 1) * stage_pitch<T, G::JB>() * sizeof(T);
+  return G::ex_bytes > stage ? G::ex_bytes : stage;
 }
 
 // Raw register image of one complex input sample (loaded before any compute).
@@ -78,122 +83,171 @@ struct Raw<__bf16> {
   }
 };
 
-constexpr int kMaxPasses = 2;
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const __bf16 a = (__bf16)lo, b = (__bf16)hi;
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+template <typename T>
+__device__ __forceinline__ void store_cplx(T* p, size_t i, float2 v);
+template <>
+__device__ __forceinline__ void store_cplx<float>(float* p, size_t i, float2 v) {
+  reinterpret_cast<float2*>(p)[i] = v;
+}
+template <>
+__device__ __forceinline__ void store_cplx<__bf16>(__bf16* p, size_t i, float2 v) {
+  reinterpret_cast<uint32_t*>(p)[i] = pack_bf16x2(v.x, v.y);
+}
+
+// The NP values of rows NP*rr .. NP*rr+NP-1 at one stage position.
+template <typename T, int NP>
+struct StageVec;
+template <>
+struct StageVec<__bf16, 2> {
+  static __device__ __forceinline__ void put(__bf16* p, const float (&v)[2]) {
+    *reinterpret_cast<uint32_t*>(p) = pack_bf16x2(v[0], v[1]);
+  }
+  static __device__ __forceinline__ void get(const __bf16* p, float (&v)[2]) {
+    const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
+    v[0] = __uint_as_float(u << 16);
+    v[1] = __uint_as_float(u & 0xffff0000u);
+  }
+};
+template <>
+struct StageVec<__bf16, 1> {
+  static __device__ __forceinline__ void put(__bf16* p, const float (&v)[1]) { *p = (__bf16)v[0]; }
+  static __device__ __forceinline__ void get(const __bf16* p, float (&v)[1]) { v[0] = (float)*p; }
+};
+template <>
+struct StageVec<float, 2> {
+  static __device__ __forceinline__ void put(float* p, const float (&v)[2]) {
+    *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
+  }
+  static __device__ __forceinline__ void get(const float* p, float (&v)[2]) {
+    const float2 u = *reinterpret_cast<const float2*>(p);
+    v[0] = u.x;
+    v[1] = u.y;
+  }
+};
+template <>
+struct StageVec<float, 1> {
+  static __device__ __forceinline__ void put(float* p, const float (&v)[1]) { *p = v[0]; }
+  static __device__ __forceinline__ void get(const float* p, float (&v)[1]) { v[0] = *p; }
+};
 
 // Move the [M][2][JB] spectrum block between the LDS stage (pitch SP) and
-// global memory at gbase[mi * mstride + (n * 2 + ri) * pitch + r] (gbase
-// already offset to the spin, latitude tile and row), in 16-byte vectors
-// when JB allows.
-template <typename T, bool kToGlobal>
-__device__ __forceinline__ void stage_copy(T* stage, T* gbase, int M, int JB, int SP,
-                                           size_t mstride, size_t nbase, int pitch, int tid,
-                                           int nthreads) {
+// global memory at gbase[mi * mstride + (n * 2 + ri) * JB + r] (gbase
+// already offset to the spin and latitude tile), in 16-byte vectors when JB
+// allows.
+template <typename T, bool kToGlobal, int JB, int SP, int NT>
+__device__ __forceinline__ void stage_copy(T* stage, T* gbase, int M, size_t mstride, size_t n,
+                                           int tid) {
   constexpr int VEC = 16 / sizeof(T);
   constexpr int BATCH = 8;  // global loads in flight per thread before their LDS stores
-  if (JB % VEC == 0) {
-    const int vpr = JB / VEC;
-    const int total = M * 2 * vpr;
-    for (int base = tid; base < total; base += BATCH * nthreads) {
+  if constexpr (JB % VEC == 0) {
+    constexpr int VPR = JB / VEC;  // vectors per (order, re/im) run
+    const int total = M * 2 * VPR;
+    T* g0 = gbase + n * 2 * JB;
+    for (int base = tid; base < total; base += BATCH * NT) {
       uint4 buf[BATCH];
 #pragma unroll
       for (int u = 0; u < BATCH; ++u) {
-        const int idx = base + u * nthreads;
+        const int idx = base + u * NT;
         // no per-lane branch around a load: out-of-range lanes read vector 0
         const int id = idx < total ? idx : 0;
-        const int vi = id % vpr;
-        const int ri = (id / vpr) & 1;
-        const int mi = id / (2 * vpr);
-        uint4* s = reinterpret_cast<uint4*>(stage + (size_t)mi * SP + ri * JB + vi * VEC);
-        uint4* g = reinterpret_cast<uint4*>(gbase + mi * mstride + (nbase * 2 + ri) * pitch + vi * VEC);
-        if (kToGlobal) {
+        const int vi = id % VPR, ri = (id / VPR) & 1, mi = id / (2 * VPR);
+        uint4* s = reinterpret_cast<uint4*>(stage + mi * SP + ri * JB + vi * VEC);
+        uint4* g = reinterpret_cast<uint4*>(g0 + mi * mstride + ri * JB + vi * VEC);
+        if constexpr (kToGlobal) {
           if (idx < total) *g = *s;
         } else {
           buf[u] = *g;
         }
       }
-      if (!kToGlobal) {
+      if constexpr (!kToGlobal) {
         // unconditional stores too (a lane past the end rewrites vector 0 with
         // the same data): a conditional store lets the compiler sink each
         // load next to it, which serializes the loads again
 #pragma unroll
         for (int u = 0; u < BATCH; ++u) {
-          const int idx = base + u * nthreads;
+          const int idx = base + u * NT;
           const int id = idx < total ? idx : 0;
-          const int vi = id % vpr;
-          const int ri = (id / vpr) & 1;
-          const int mi = id / (2 * vpr);
-          *reinterpret_cast<uint4*>(stage + (size_t)mi * SP + ri * JB + vi * VEC) = buf[u];
+          const int vi = id % VPR, ri = (id / VPR) & 1, mi = id / (2 * VPR);
+          *reinterpret_cast<uint4*>(stage + mi * SP + ri * JB + vi * VEC) = buf[u];
         }
       }
     }
   } else {
     const int total = M * 2 * JB;
-    for (int idx = tid; idx < total; idx += nthreads) {
-      const int r = idx % JB;
-      const int ri = (idx / JB) & 1;
-      const int mi = idx / (2 * JB);
-      T* s = stage + (size_t)mi * SP + ri * JB + r;
-      T* g = gbase + mi * mstride + (nbase * 2 + ri) * pitch + r;
-      if (kToGlobal) *g = *s;
+    for (int idx = tid; idx < total; idx += NT) {
+      const int r = idx % JB, ri = (idx / JB) & 1, mi = idx / (2 * JB);
+      T* s = stage + mi * SP + ri * JB + r;
+      T* g = gbase + mi * mstride + (n * 2 + ri) * JB + r;
+      if constexpr (kToGlobal) *g = *s;
       else *s = *g;
     }
   }
 }
 
-template <typename Tin, typename Tout, int W1, int W2>
-__global__ void __launch_bounds__(256) dft_fwd_kernel(const Tin* __restrict__ x,
-                                                      Tout* __restrict__ X,
-                                                      const float2* __restrict__ tw, int S,
-                                                      int C, int NB, int NBC, int H, int JT,
-                                                      int L, int JB) {
-  constexpr int W = W1 * W2;
-  extern __shared__ __align__(16) unsigned char smem[];
-  const int RPP = blockDim.x / W1;
-  const int NP = JB / RPP;  // passes, <= kMaxPasses
-  const int tid = threadIdx.x;
-  const int t = tid % W1;
-  const int rr = tid / W1;
-  const int nJB = H / JB;
-  // consecutive row blocks of a map (which share the 128-byte lines of the
-  // transposed spectrum) are numbered together, so they run on one XCD
+// Map and row block of a logical block: consecutive row blocks of a map
+// (which share the 128-byte lines of the transposed spectrum) are numbered
+// together, so they run on one XCD.
+struct MapBlock {
+  int map, j0, si, n;
+};
+template <int JB, int H>
+__device__ __forceinline__ bool map_block(int S, int C, int NB, MapBlock& mb) {
+  constexpr int nJB = H / JB;
   const int lb = xcd_logical_block();
-  if (lb >= S * C * NB * nJB) return;
-  const int map = lb / nJB;
-  const int j0 = (lb % nJB) * JB;
-  const int c = map % C;
-  const int si = (map / C) % S;
-  const int b = map / (C * S);
-  const int n = b * C + c;
+  if (lb >= S * C * NB * nJB) return false;
+  mb.map = lb / nJB;
+  mb.j0 = (lb % nJB) * JB;
+  const int c = mb.map % C;
+  mb.si = (mb.map / C) % S;
+  mb.n = (mb.map / (C * S)) * C + c;
+  return true;
+}
+
+template <typename Tin, typename Tout, int W1, int W2>
+__global__ void __launch_bounds__((DftGeom<W1, W2>::NT))
+    dft_fwd_kernel(const Tin* __restrict__ x, Tout* __restrict__ X,
+                   const float2* __restrict__ tw, int S, int C, int NB, int NBC, int L) {
+  using G = DftGeom<W1, W2>;
+  constexpr int W = G::W, H = W, NP = G::NP, JB = G::JB, NT = G::NT;
+  constexpr int SP = stage_pitch<Tout, JB>();
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x, t = tid % W1, rr = tid / W1;
+  MapBlock mb;
+  if (!map_block<JB, H>(S, C, NB, mb)) return;
   const int M = 2 * L - 1;
-  const int SP = stage_pitch<Tout>(JB);
   // the exchange buffer [RPP][W2][W1+1] (during the FFTs) and the spectrum
-  // stage [M][SP] (after them) share one allocation
+  // stage [M + 1][SP] (after them) share one allocation
   float2* ex = reinterpret_cast<float2*>(smem);
   Tout* stage = reinterpret_cast<Tout*>(smem);
 
-  // every load of the block's JB rows is issued before any arithmetic
-  const size_t row_base = ((size_t)map * H + j0) * W;  // complex index of row j0
-  typename Raw<Tin>::type raw[kMaxPasses][W2];
+  // every load of the block's rows is issued before any arithmetic; this
+  // thread's rows are NP * rr + p
+  const size_t row_base = ((size_t)mb.map * H + mb.j0 + NP * rr) * W + t;
+  typename Raw<Tin>::type raw[NP][W2];
 #pragma unroll
-  for (int p = 0; p < kMaxPasses; ++p)
-    if (p < NP) {
+  for (int p = 0; p < NP; ++p)
 #pragma unroll
-      for (int q = 0; q < W2; ++q)
-        raw[p][q] = Raw<Tin>::load(x, row_base + (size_t)(p * RPP + rr) * W + t + W1 * q);
-    }
+    for (int q = 0; q < W2; ++q) raw[p][q] = Raw<Tin>::load(x, row_base + (size_t)p * W + W1 * q);
+  float2 twr[W2];
+#pragma unroll
+  for (int k2 = 1; k2 < W2; ++k2) twr[k2] = tw[t * k2];
+
   float2* exr = ex + (size_t)rr * W2 * (W1 + 1);
-  // spectra of all passes stay in registers until the exchange buffer is free:
-  // spec[p][i * W1 + k1] is frequency t + W1 * i + W2 * k1 of row p * RPP + rr
-  float2 spec[kMaxPasses][W2];
+  // spec[p][i * W1 + k1] is frequency t + W1 * i + W2 * k1 of row NP * rr + p
+  float2 spec[NP][W2];
 #pragma unroll
-  for (int p = 0; p < kMaxPasses; ++p) {
-    if (p >= NP) break;
+  for (int p = 0; p < NP; ++p) {
     float2 v[W2];
 #pragma unroll
     for (int q = 0; q < W2; ++q) v[q] = Raw<Tin>::unpack(raw[p][q]);
     fft_reg<W2, -1>(v);
 #pragma unroll
-    for (int k2 = 1; k2 < W2; ++k2) v[k2] = cmul(v[k2], tw[t * k2]);
+    for (int k2 = 1; k2 < W2; ++k2) v[k2] = cmul(v[k2], twr[k2]);
     if (p > 0) __syncthreads();  // the previous pass has finished reading ex
 #pragma unroll
     for (int k2 = 0; k2 < W2; ++k2) exr[k2 * (W1 + 1) + t] = v[k2];
@@ -211,96 +265,83 @@ __global__ void __launch_bounds__(256) dft_fwd_kernel(const Tin* __restrict__ x,
   }
   __syncthreads();  // every read of ex is done before the stage overwrites it
 #pragma unroll
-  for (int p = 0; p < kMaxPasses; ++p) {
-    if (p >= NP) break;
-    const int r = p * RPP + rr;
+  for (int i = 0; i < W2 / W1; ++i)
 #pragma unroll
-    for (int i = 0; i < W2 / W1; ++i)
+    for (int k1 = 0; k1 < W1; ++k1) {
+      const int f = t + W1 * i + W2 * k1;
+      const int m = f < L ? f : f - W;
+      // orders outside |m| < L go to the spare row M (never copied out)
+      const int row = (m > -L && m < L) ? m + L - 1 : M;
+      Tout* sp = stage + row * SP + NP * rr;
+      float re[NP], im[NP];
 #pragma unroll
-      for (int k1 = 0; k1 < W1; ++k1) {
-        const int f = t + W1 * i + W2 * k1;
-        const int m = f < L ? f : f - W;
-        if (m > -L && m < L) {
-          Tout* sp = stage + (size_t)(m + L - 1) * SP;
-          sp[r] = (Tout)spec[p][i * W1 + k1].x;
-          sp[JB + r] = (Tout)spec[p][i * W1 + k1].y;
-        }
+      for (int p = 0; p < NP; ++p) {
+        re[p] = spec[p][i * W1 + k1].x;
+        im[p] = spec[p][i * W1 + k1].y;
       }
-  }
+      StageVec<Tout, NP>::put(sp, re);
+      StageVec<Tout, NP>::put(sp + JB, im);
+    }
   __syncthreads();
-  // X[si][mi][n][ri][j0 + r]
-  // X[si][mi][j0 / JT][n][ri][j0 % JT + r]
-  const size_t tile = (size_t)NBC * 2 * JT;  // one latitude tile of one order
-  stage_copy<Tout, true>(stage, X + ((size_t)si * M * (H / JT) + j0 / JT) * tile + j0 % JT, M, JB,
-                         SP, (size_t)(H / JT) * tile, n, JT, tid, blockDim.x);
+  // X[si][mi][j0 / JT][n][ri][j0 % JT + r] with JT == JB
+  const size_t tile = (size_t)NBC * 2 * JB;  // one latitude tile of one order
+  stage_copy<Tout, true, JB, SP, NT>(stage, X + ((size_t)mb.si * M * (H / JB) + mb.j0 / JB) * tile,
+                                     M, (size_t)(H / JB) * tile, mb.n, tid);
 }
 
 template <typename Tin, typename Tout, int W1, int W2>
-__global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
-                                                      Tout* __restrict__ y,
-                                                      const float2* __restrict__ tw, int S,
-                                                      int C, int NB, int NBC, int H, int JT,
-                                                      int L, int JB) {
-  constexpr int W = W1 * W2;
+__global__ void __launch_bounds__((DftGeom<W1, W2>::NT))
+    dft_inv_kernel(const Tin* __restrict__ Y, Tout* __restrict__ y,
+                   const float2* __restrict__ tw, int S, int C, int NB, int NBC, int L) {
+  using G = DftGeom<W1, W2>;
+  constexpr int W = G::W, H = W, NP = G::NP, JB = G::JB, NT = G::NT;
+  constexpr int SP = stage_pitch<Tin, JB>();
   extern __shared__ __align__(16) unsigned char smem[];
-  const int RPP = blockDim.x / W1;
-  const int NP = JB / RPP;
-  const int tid = threadIdx.x;
-  const int t = tid % W1;
-  const int rr = tid / W1;
-  const int nJB = H / JB;
-  // consecutive row blocks of a map (which share the 128-byte lines of the
-  // transposed spectrum) are numbered together, so they run on one XCD
-  const int lb = xcd_logical_block();
-  if (lb >= S * C * NB * nJB) return;
-  const int map = lb / nJB;
-  const int j0 = (lb % nJB) * JB;
-  const int c = map % C;
-  const int si = (map / C) % S;
-  const int b = map / (C * S);
-  const int n = b * C + c;
+  const int tid = threadIdx.x, t = tid % W1, rr = tid / W1;
+  MapBlock mb;
+  if (!map_block<JB, H>(S, C, NB, mb)) return;
   const int M = 2 * L - 1;
-  const int SP = stage_pitch<Tin>(JB);
   // the spectrum stage [M][SP] (first) and the exchange buffer
   // [RPP][W2][W1+1] (during the FFTs) share one allocation
   Tin* stage = reinterpret_cast<Tin*>(smem);
   float2* ex = reinterpret_cast<float2*>(smem);
+  // twiddles [k2][t] = tw[t k2], filled before any store of this workgroup:
+  // a global load issued after the output stores would wait for them (vmcnt
+  // counts stores too)
+  __shared__ float2 twl[W];
+  for (int i = tid; i < W; i += NT) twl[i] = tw[(i % W1) * (i / W1)];
 
-  const size_t tile = (size_t)NBC * 2 * JT;  // one latitude tile of one order
-  stage_copy<Tin, false>(stage,
-                         const_cast<Tin*>(Y) + ((size_t)si * M * (H / JT) + j0 / JT) * tile + j0 % JT,
-                         M, JB, SP, (size_t)(H / JT) * tile, n, JT, tid, blockDim.x);
+  const size_t tile = (size_t)NBC * 2 * JB;  // one latitude tile of one order
+  stage_copy<Tin, false, JB, SP, NT>(
+      stage, const_cast<Tin*>(Y) + ((size_t)mb.si * M * (H / JB) + mb.j0 / JB) * tile, M,
+      (size_t)(H / JB) * tile, mb.n, tid);
   __syncthreads();
 
   // the spectra of all passes are read into registers before the exchange
-  // buffer overwrites the stage
-  float2 v[kMaxPasses][W2];
+  // buffer overwrites the stage; orders outside |m| < L read row 0 and are
+  // zeroed (branch-free)
+  float2 v[NP][W2];
 #pragma unroll
-  for (int p = 0; p < kMaxPasses; ++p) {
-    if (p >= NP) break;
-    const int r = p * RPP + rr;
+  for (int q = 0; q < W2; ++q) {
+    const int f = t + W1 * q;
+    const int m = f < L ? f : f - W;
+    const bool ok = m > -L && m < L;
+    const Tin* sp = stage + (ok ? m + L - 1 : 0) * SP + NP * rr;
+    float re[NP], im[NP];
+    StageVec<Tin, NP>::get(sp, re);
+    StageVec<Tin, NP>::get(sp + JB, im);
 #pragma unroll
-    for (int q = 0; q < W2; ++q) {
-      // branch-free: orders outside |m| < L read row 0 and are zeroed after
-      const int f = t + W1 * q;
-      const int m = f < L ? f : f - W;
-      const bool ok = m > -L && m < L;
-      const Tin* sp = stage + (size_t)(ok ? m + L - 1 : 0) * SP;
-      const float re = (float)sp[r], im = (float)sp[JB + r];
-      v[p][q] = make_float2(ok ? re : 0.f, ok ? im : 0.f);
-    }
+    for (int p = 0; p < NP; ++p) v[p][q] = make_float2(ok ? re[p] : 0.f, ok ? im[p] : 0.f);
   }
   __syncthreads();
 
-  const size_t row_base = ((size_t)map * H + j0) * W;
+  const size_t row_base = ((size_t)mb.map * H + mb.j0 + NP * rr) * W;
   float2* exr = ex + (size_t)rr * W2 * (W1 + 1);
 #pragma unroll
-  for (int p = 0; p < kMaxPasses; ++p) {
-    if (p >= NP) break;
-    const int r = p * RPP + rr;
+  for (int p = 0; p < NP; ++p) {
     fft_reg<W2, +1>(v[p]);
 #pragma unroll
-    for (int k2 = 1; k2 < W2; ++k2) v[p][k2] = cmulc(v[p][k2], tw[t * k2]);
+    for (int k2 = 1; k2 < W2; ++k2) v[p][k2] = cmulc(v[p][k2], twl[k2 * W1 + t]);
     if (p > 0) __syncthreads();  // the previous pass has finished reading ex
 #pragma unroll
     for (int k2 = 0; k2 < W2; ++k2) exr[k2 * (W1 + 1) + t] = v[p][k2];
@@ -314,72 +355,44 @@ __global__ void __launch_bounds__(256) dft_inv_kernel(const Tin* __restrict__ Y,
       fft_reg<W1, +1>(u);
 #pragma unroll
       for (int k1 = 0; k1 < W1; ++k1)
-        CplxIO<Tout>::store(y, row_base + (size_t)r * W + k2 + W2 * k1, u[k1]);
+        store_cplx<Tout>(y, row_base + (size_t)p * W + k2 + W2 * k1, u[k1]);
     }
   }
 }
 
-// Rows per workgroup JB = NP * RPP: RPP rows are transformed at a time by
-// 256 / W1 threads (fewer for small grids), NP <= 2 passes.  JB = 32 gives
-// 64-byte (bf16) / 128-byte (f32) runs per order in the transposed layout.
-#ifndef SWSFT_DFT_THREADS
-#define SWSFT_DFT_THREADS 256
-#endif
-#ifndef SWSFT_DFT_JB
-#define SWSFT_DFT_JB 32
-#endif
-
-template <typename Ts, int W1, int W2>
-void dft_geometry(const Plan& p, int* JB, int* nthreads, size_t* lds) {
-  int rpp = SWSFT_DFT_THREADS / W1;
-  if (rpp < 1) rpp = 1;
-  if (rpp > p.H) rpp = p.H;
-  int jb = rpp;
-  if (jb < SWSFT_DFT_JB && 2 * jb <= p.H) jb *= 2;  // a second pass when rows allow
-  auto bytes = [&](int j) {  // exchange buffer and stage alias
-    const size_t ex = (size_t)rpp * W2 * (W1 + 1) * sizeof(float2);
-    const size_t stage = (size_t)p.M * stage_pitch<Ts>(j) * sizeof(Ts);
-    return ex > stage ? ex : stage;
-  };
-  if (bytes(jb) > 160 * 1024) jb = rpp;  // one pass if two do not fit the CU's LDS
-  *JB = jb;
-  *nthreads = rpp * W1;
-  *lds = bytes(jb);
+template <class Kern>
+hipError_t allow_lds(Kern kern, size_t lds) {
+  if (lds <= 64 * 1024) return hipSuccess;
+  return hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
 }
 
 template <typename Tin, typename Tout, int W1, int W2>
 hipError_t launch_fwd_shape(const Plan& p, int S, int B, int C, const void* x, void* X,
                             hipStream_t st) {
-  int JB, nthreads;
-  size_t lds;
-  dft_geometry<Tout, W1, W2>(p, &JB, &nthreads, &lds);
+  using G = DftGeom<W1, W2>;
+  if (p.H != G::W || p.JT != G::JB) return hipErrorInvalidValue;
+  const size_t lds = dft_lds_bytes<Tout, G>(p.M);
   auto kern = dft_fwd_kernel<Tin, Tout, W1, W2>;
-  if (lds > 64 * 1024) {
-    const hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-  }
-  const long long blocks = (long long)B * S * C * (p.H / JB);
-  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(nthreads), lds, st, (const Tin*)x,
-                     (Tout*)X, p.twiddle, S, C, B, B * C, p.H, p.JT, p.L, JB);
+  const hipError_t e = allow_lds(kern, lds);
+  if (e != hipSuccess) return e;
+  const long long blocks = (long long)B * S * C * (p.H / G::JB);
+  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(G::NT), lds, st, (const Tin*)x, (Tout*)X,
+                     p.twiddle, S, C, B, B * C, p.L);
   return hipGetLastError();
 }
 
 template <typename Tin, typename Tout, int W1, int W2>
 hipError_t launch_inv_shape(const Plan& p, int S, int B, int C, const void* Y, void* y,
                             hipStream_t st) {
-  int JB, nthreads;
-  size_t lds;
-  dft_geometry<Tin, W1, W2>(p, &JB, &nthreads, &lds);
+  using G = DftGeom<W1, W2>;
+  if (p.H != G::W || p.JT != G::JB) return hipErrorInvalidValue;
+  const size_t lds = dft_lds_bytes<Tin, G>(p.M);
   auto kern = dft_inv_kernel<Tin, Tout, W1, W2>;
-  if (lds > 64 * 1024) {
-    const hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-  }
-  const long long blocks = (long long)B * S * C * (p.H / JB);
-  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(nthreads), lds, st, (const Tin*)Y,
-                     (Tout*)y, p.twiddle, S, C, B, B * C, p.H, p.JT, p.L, JB);
+  const hipError_t e = allow_lds(kern, lds);
+  if (e != hipSuccess) return e;
+  const long long blocks = (long long)B * S * C * (p.H / G::JB);
+  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(G::NT), lds, st, (const Tin*)Y, (Tout*)y,
+                     p.twiddle, S, C, B, B * C, p.L);
   return hipGetLastError();
 }
 
