@@ -62,7 +62,8 @@ constexpr int bitrev(int i, int bits) {
 }
 
 // In-place length-N DFT of v: v[k] <- sum_q v[q] exp(SIGN 2 pi i q k / N).
-// Radix-2 decimation in time, fully unrolled, twiddles folded to constants.
+// Radix-2 decimation in time, fully unrolled, twiddles folded to constants;
+// the butterflies with twiddle 1 or -+i take no multiplies.
 template <int N, int SIGN>
 __device__ __forceinline__ void fft_reg(float2 (&v)[N]) {
   if constexpr (N > 1) {
@@ -90,6 +91,8 @@ __device__ __forceinline__ void fft_reg(float2 (&v)[N]) {
           float2 bw;
           if (idx == 0) {
             bw = b;
+          } else if (4 * idx == N) {  // w = -i (forward) or +i (inverse): exact, no multiplies
+            bw = SIGN < 0 ? make_float2(b.y, -b.x) : make_float2(-b.y, b.x);
           } else {
             bw = make_float2(b.x * wr - b.y * wi, b.x * wi + b.y * wr);
           }
