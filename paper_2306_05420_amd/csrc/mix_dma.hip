@@ -255,8 +255,7 @@ hipError_t launch_mix_dma(const Plan& p, int B, int Cin, int Cout, const void* c
   if ((2 * Cin) % SWSFT_MIX_DMA_BK == 0)
     return launch_geom<SWSFT_MIX_DMA_BK, SWSFT_MIX_DMA_RA, SWSFT_MIX_DMA_RB, SWSFT_MIX_DMA_STAGES>(
         p, B, Cin, Cout, coef, K, out, st);
-  return launch_geom<32, SWSFT_MIX_DMA_RA, SWSFT_MIX_DMA_RB, 2 * SWSFT_MIX_DMA_STAGES>(
-      p, B, Cin, Cout, coef, K, out, st);
+  return launch_geom<32, 128, 128, 4>(p, B, Cin, Cout, coef, K, out, st);
 }
 
 }  // namespace swsft
