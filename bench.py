@@ -5,6 +5,7 @@ spins {0,1} -> {0,1}, 256 -> 256 channels, bfloat16 storage with float32
 accumulation (the large weather-shaped workload).
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+    python bench.py --table            (every workload: layer, transforms, stack)
     python bench.py --summarize-counters FETCH_CSV WRITE_CSV
 
 Prints one JSON line.  A step is one layer call (forward transform, per-degree
@@ -206,6 +207,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (for counter calibration)")
+    ap.add_argument("--table", action="store_true",
+                    help="measure every workload and print markdown table rows")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic_<workload>.json from two counter runs and exit")
     args = ap.parse_args(argv)
@@ -220,111 +223,30 @@ def main(argv=None):
 
     import torch
 
-    from paper_2306_05420_amd import swsft as S
-    from paper_2306_05420_amd import synthetic as syn
-
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         return 1
-    w = syn.workload(args.workload)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    plan = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_out, w.dtype)
+    if args.table:
+        from paper_2306_05420_amd import synthetic as syn
+        print(TABLE_HEAD)
+        for i, wl in enumerate(syn.WORKLOADS):
+            r = measure(wl.name, min(args.steps, 100), min(args.warmup, 10), dev)
+            for row in table_rows(i + 1, r):
+                print(row, flush=True)
+        return 0
 
-    # inputs: band-limited fields synthesised on the GPU from seeded
-    # CN(0,1)/(l+1) coefficients by the library's own inverse transform
-    gen = torch.Generator(device=dev)
-    gen.manual_seed(w.seed)
-    decay = {"white": 0.0, "decay1": 1.0}.get(w.field, 1.0)
-    coef = syn.torch_random_coefficients(gen, w.L, w.B, w.spins_in, w.C_in, decay)
-    K = syn.torch_random_filters(gen, w.L, w.spins_in, w.C_in, w.spins_out, w.C_out,
-                                 w.filter_var)
-    if w.dtype == "bf16":
-        coef = torch.view_as_real(coef).to(torch.bfloat16).contiguous()
-        K = torch.view_as_real(K).to(torch.bfloat16).contiguous()
-    plan_syn = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_in, w.dtype)
-    x = plan_syn.inverse(coef)
-    y = plan.empty(w.B, len(w.spins_out), w.C_out, w.H, w.W)
-    torch.cuda.synchronize()
-    plan_syn.close()
-    del coef
-
-    if args.copy_calibration:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-
-    for _ in range(args.warmup):
-        plan.conv(x, K, y)
-    torch.cuda.synchronize()
-
-    # timed region: K layer calls
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    start.record()
-    for _ in range(args.steps):
-        plan.conv(x, K, y)
-    stop.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    gpu_ms = start.elapsed_time(stop)
-    elapsed = max(wall, gpu_ms / 1e3)
-    ms_per_step = 1e3 * elapsed / args.steps
-    value = args.steps / elapsed
-
-    # per-stage HIP events over a second pass of K layer calls
-    plan.stage_timing(True)
-    for _ in range(args.steps):
-        plan.conv(x, K, y)
-    torch.cuda.synchronize()
-    times = plan.stage_times()
-    plan.stage_timing(False)
-
-    work = stage_work(w)
-    useful = sum(v["flops"] for v in work.values())
-    stages = {}
-    for name, (ms, n) in times.items():
-        avg_s = ms / 1e3 / n
-        rec = {"avg_us": round(avg_s * 1e6, 2), "launches": n}
-        wk = work.get(name)
-        if wk:
-            rec["GB/s"] = round(wk["bytes"] / avg_s / 1e9, 1)
-            rec["hbm_frac"] = round(wk["bytes"] / avg_s / 1e9 / HBM_PEAK_GBS, 4)
-            if wk["flops"]:
-                rec["TFLOP/s"] = round(wk["flops"] / avg_s / 1e12, 2)
-                rec["mfma_frac"] = round(wk["flops"] / avg_s / 1e12 / PEAK_TFLOPS[w.dtype], 4)
-        stages[name] = rec
-    dom = max((k for k in stages if k in work), key=lambda k: stages[k]["avg_us"])
-    avg_s = stages[dom]["avg_us"] / 1e6
-    wk = work[dom]
-    flops_per_byte = wk["flops"] / wk["bytes"]
-    ridge = PEAK_TFLOPS[w.dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
-    if wk["flops"] and flops_per_byte > ridge:
-        roof = {"bound": "mfma", "achieved": round(wk["flops"] / avg_s / 1e12, 2),
-                "peak": PEAK_TFLOPS[w.dtype], "unit": "TFLOP/s"}
-    else:
-        roof = {"bound": "hbm", "achieved": round(wk["bytes"] / avg_s / 1e9, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s"}
-    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = measured_traffic(dom)
-    roof["kernel"] = dom
-    roof["algorithmic_bytes_per_launch"] = wk["bytes"]
-    roof["algorithmic_flops_per_launch"] = wk["flops"]
-
-    tflops = useful / (elapsed / args.steps) / 1e12
+    r = measure(args.workload, args.steps, args.warmup, dev, args.copy_calibration)
+    w = r["w"]
     out = {
         "metric": METRIC,
-        "value": round(value, 2),
+        "value": round(r["value"], 2),
         "unit": "fwd/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": round(r["ms_per_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -339,17 +261,186 @@ def main(argv=None):
             "bandlimit": w.L,
             "parallelism": "single GPU",
         },
-        "tflops": round(tflops, 2),
-        "mfma_peak_frac": round(tflops / PEAK_TFLOPS[w.dtype], 4),
-        "useful_gflop_per_fwd": round(useful / 1e9, 3),
-        "stages": stages,
-        "roofline": roof,
+        "tflops": round(r["tflops"], 2),
+        "mfma_peak_frac": round(r["tflops"] / PEAK_TFLOPS[w.dtype], 4),
+        "useful_gflop_per_fwd": round(r["useful"] / 1e9, 3),
+        "stages": r["stages"],
+        "roofline": r["roofline"],
+        "transforms": r["transforms"],
     }
+    if "stack2" in r:
+        out["stack2"] = r["stack2"]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
-    plan.close()
     print(json.dumps(out), flush=True)
     return 0
+
+
+def _time_calls(fn, steps: int, warmup: int):
+    """Seconds per call of fn over `steps` calls after `warmup`, bracketed by
+    device synchronizations: the larger of wall clock and stream events."""
+    import torch
+
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(steps):
+        fn()
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return max(wall, start.elapsed_time(stop) / 1e3) / steps
+
+
+def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = False) -> dict:
+    """Time one workload: the layer (with per-stage HIP events and the
+    roofline of its dominant stage), the forward and inverse transforms alone,
+    and for the molecule workload the two-layer stack with phase collapse."""
+    import torch
+
+    from paper_2306_05420_amd import swsft as S
+    from paper_2306_05420_amd import synthetic as syn
+
+    w = syn.workload(name)
+    plan = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_out, w.dtype)
+
+    # inputs: band-limited fields synthesised on the GPU from seeded
+    # CN(0,1)/(l+1) coefficients by the library's own inverse transform
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(w.seed)
+    decay = {"white": 0.0, "decay1": 1.0}.get(w.field, 1.0)
+
+    def storage(t):
+        return torch.view_as_real(t).to(torch.bfloat16).contiguous() if w.dtype == "bf16" else t
+
+    coef = storage(syn.torch_random_coefficients(gen, w.L, w.B, w.spins_in, w.C_in, decay))
+    K = storage(syn.torch_random_filters(gen, w.L, w.spins_in, w.C_in, w.spins_out, w.C_out,
+                                         w.filter_var))
+    coef_out = storage(syn.torch_random_coefficients(gen, w.L, w.B, w.spins_out, w.C_out, decay))
+    plan_syn = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_in, w.dtype)
+    x = plan_syn.inverse(coef)
+    y = plan.empty(w.B, len(w.spins_out), w.C_out, w.H, w.W)
+    torch.cuda.synchronize()
+    plan_syn.close()
+
+    if copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    # timed region: K layer calls
+    t_layer = _time_calls(lambda: plan.conv(x, K, y), steps, warmup)
+
+    # per-stage HIP events over a second pass of K layer calls
+    plan.stage_timing(True)
+    for _ in range(steps):
+        plan.conv(x, K, y)
+    torch.cuda.synchronize()
+    times = plan.stage_times()
+    plan.stage_timing(False)
+
+    work = stage_work(w)
+    useful = sum(v["flops"] for v in work.values())
+    stages = {}
+    for sname, (ms, n) in times.items():
+        avg_s = ms / 1e3 / n
+        rec = {"avg_us": round(avg_s * 1e6, 2), "launches": n}
+        wk = work.get(sname)
+        if wk:
+            rec["GB/s"] = round(wk["bytes"] / avg_s / 1e9, 1)
+            rec["hbm_frac"] = round(wk["bytes"] / avg_s / 1e9 / HBM_PEAK_GBS, 4)
+            if wk["flops"]:
+                rec["TFLOP/s"] = round(wk["flops"] / avg_s / 1e12, 2)
+                rec["mfma_frac"] = round(wk["flops"] / avg_s / 1e12 / PEAK_TFLOPS[w.dtype], 4)
+        stages[sname] = rec
+    dom = max((k for k in stages if k in work), key=lambda k: stages[k]["avg_us"])
+    avg_s = stages[dom]["avg_us"] / 1e6
+    wk = work[dom]
+    flops_per_byte = wk["flops"] / wk["bytes"]
+    ridge = PEAK_TFLOPS[w.dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if wk["flops"] and flops_per_byte > ridge:
+        roof = {"bound": "mfma", "achieved": round(wk["flops"] / avg_s / 1e12, 2),
+                "peak": PEAK_TFLOPS[w.dtype], "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(wk["bytes"] / avg_s / 1e9, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = measured_traffic(dom) if name == "wx256" else None
+    roof["kernel"] = dom
+    roof["algorithmic_bytes_per_launch"] = wk["bytes"]
+    roof["algorithmic_flops_per_launch"] = wk["flops"]
+
+    # the transforms alone: forward on x (input spins), inverse on a
+    # coefficient set of the output spins
+    coef_f = plan.forward(x)
+    y_i = plan.empty(w.B, len(w.spins_out), w.C_out, w.H, w.W)
+    t_fwd = _time_calls(lambda: plan.forward(x, coef_f), steps, warmup)
+    t_inv = _time_calls(lambda: plan.inverse(coef_out, y_i), steps, warmup)
+    transforms = {}
+    for tname, t, keys in (("forward", t_fwd, ("dft_fwd", "lat_fwd")),
+                           ("inverse", t_inv, ("lat_inv", "dft_inv"))):
+        byt = sum(work[k]["bytes"] for k in keys)
+        fl = sum(work[k]["flops"] for k in keys)
+        transforms[tname] = {"us": round(t * 1e6, 2), "per_s": round(1.0 / t, 1),
+                             "GB/s": round(byt / t / 1e9, 1),
+                             "TFLOP/s": round(fl / t / 1e12, 2)}
+    r = {"w": w, "value": 1.0 / t_layer, "ms_per_step": t_layer * 1e3,
+         "tflops": useful / t_layer / 1e12, "useful": useful, "stages": stages,
+         "roofline": roof, "transforms": transforms}
+
+    if name == "mol":
+        # two stacked layers with the phase collapse between them
+        plan2 = S.Plan(w.H, w.W, w.L, w.spins_out, w.spins_out, w.dtype)
+        K2 = storage(syn.torch_random_filters(gen, w.L, w.spins_out, w.C_out, w.spins_out,
+                                              w.C_out, w.filter_var))
+        So = len(w.spins_out)
+        W1 = syn.torch_complex_normal(gen, (w.C_out, w.C_out), 1.0 / w.C_out)
+        W2 = syn.torch_complex_normal(gen, (w.C_out, So * w.C_out), 1.0 / (So * w.C_out))
+        bias = syn.torch_complex_normal(gen, (w.C_out,), 0.01)
+        z = plan.empty(w.B, So, w.C_out, w.H, w.W)
+        y2 = plan.empty(w.B, So, w.C_out, w.H, w.W)
+
+        def stack():
+            plan.conv(x, K, y)
+            plan.phase_collapse(y, W1, W2, bias, y=z)
+            plan2.conv(z, K2, y2)
+
+        t2 = _time_calls(stack, steps, warmup)
+        r["stack2"] = {"us": round(t2 * 1e6, 2), "per_s": round(1.0 / t2, 1),
+                       "TFLOP/s": round(2 * useful / t2 / 1e12, 2)}
+        plan2.close()
+    plan.close()
+    return r
+
+
+TABLE_HEAD = ("| Cfg | Op | median µs | calls/s | useful TFLOP/s | % MFMA peak | "
+              "GB/s (DFT stages fwd / inv) | % HBM roofline (dominant stage) |\n"
+              "|---|---|---|---|---|---|---|---|")
+
+
+def table_rows(cfg: int, r: dict):
+    w, st = r["w"], r["stages"]
+    peak = PEAK_TFLOPS[w.dtype]
+    dft = f"{st['dft_fwd']['GB/s']:.0f} / {st['dft_inv']['GB/s']:.0f}"
+    roof = f"{100 * r['roofline']['frac']:.1f} ({r['roofline']['kernel']})"
+    rows = [f"| {cfg} {w.name} | layer | {r['ms_per_step'] * 1e3:.1f} | {r['value']:.0f} | "
+            f"{r['tflops']:.1f} | {100 * r['tflops'] / peak:.1f} | {dft} | {roof} |"]
+    for op in ("forward", "inverse"):
+        t = r["transforms"][op]
+        rows.append(f"| {cfg} {w.name} | swsft_{op} | {t['us']:.1f} | {t['per_s']:.0f} | "
+                    f"{t['TFLOP/s']:.1f} | {100 * t['TFLOP/s'] / peak:.1f} | {t['GB/s']:.0f} (whole transform) | — |")
+    if "stack2" in r:
+        t = r["stack2"]
+        rows.append(f"| {cfg} {w.name} | 2 layers + phase collapse | {t['us']:.1f} | {t['per_s']:.0f} | "
+                    f"{t['TFLOP/s']:.1f} | {100 * t['TFLOP/s'] / peak:.1f} | — | — |")
+    return rows
 
 
 if __name__ == "__main__":

@@ -137,18 +137,33 @@ def test_two_layer_stack_with_phase_collapse():
     plan2.close()
 
 
-def test_phase_collapse_in_place_and_passthrough():
-    w = syn.workload("mol")
-    rng = np.random.default_rng(5)
-    x = round_to(syn.complex_normal(rng, (3, 2, 5, w.H, w.W)), "f32")
-    W1, W2, b = (np.asarray(t, np.complex64) for t in syn.phase_collapse_parameters(rng, 2, 5))
-    plan = S.Plan(w.H, w.W, w.L, (0,), (1, 0), "f32")   # spin 0 second in the list
-    xd = to_device(x, "f32")
+PC_CASES = [
+    # H, L, spins_out, C, dtype
+    (32, 16, (1, 0), 5, "f32"),        # C % 16 != 0: per-output loop kernel; spin 0 second
+    (4, 2, (1, 0, -1), 32, "f32"),     # MFMA kernel; 16 points (< one 64-point workgroup)
+    (32, 16, (0, 1), 64, "f32"),       # MFMA kernel at the molecule workload's width
+    (32, 16, (0, 1), 32, "bf16"),      # bf16 storage
+]
+
+
+@pytest.mark.parametrize("case", PC_CASES, ids=[f"H{c[0]}S{len(c[2])}C{c[3]}{c[4]}" for c in PC_CASES])
+def test_phase_collapse_in_place_and_passthrough(case):
+    H, L, so, C, dt = case
+    rng = np.random.default_rng(5 + C)
+    x = round_to(syn.complex_normal(rng, (3, len(so), C, H, H)), dt)
+    W1, W2, b = (np.asarray(t, np.complex64) for t in syn.phase_collapse_parameters(rng, len(so), C))
+    plan = S.Plan(H, H, L, (0,), so, dt)
+    xd = to_device(x, dt)
     tW = [torch.from_numpy(t).cuda() for t in (W1, W2, b)]
     y = from_device(plan.phase_collapse(xd, *tW))
-    ref = O.phase_collapse(x, (1, 0), W1.astype(complex), W2.astype(complex), b.astype(complex))
-    assert np.array_equal(y[:, 0], x[:, 0])              # spin 1 bit-identical
-    assert rel_l2(y, ref) <= 1e-6
+    ref = O.phase_collapse(x, so, W1.astype(complex), W2.astype(complex), b.astype(complex))
+    s0 = so.index(0)
+    for i in range(len(so)):
+        if i != s0:
+            assert np.array_equal(y[:, i], x[:, i])      # other spins bit-identical
+    err = rel_l2(y, ref)
+    print(f"phase collapse {case}: rel-L2 {err:.2e}")
+    assert err <= (1e-6 if dt == "f32" else TOL[dt])
     plan.phase_collapse(xd, *tW, y=xd)                     # in place
     assert np.array_equal(from_device(xd), y)
     plan.close()
