@@ -45,9 +45,7 @@ struct MixGeom {
   static constexpr int NI = (RA + RB) / RPI;         // copies per stage
   static constexpr int PER_WAVE = NI / NW;
   static constexpr int STAGE = (RA + RB) * PITCH;
-  static constexpr int LDC = 2 * RB + 8;  // bf16 per row of the epilogue tile
-  static constexpr int RING = ST * STAGE, CTILE = RA * LDC * 2;
-  static constexpr int SMEM = RING > CTILE ? RING : CTILE;
+  static constexpr int SMEM = ST * STAGE;  // the ring (the epilogue needs no LDS)
   static constexpr int MAX_KT = kMaxKp / BK;
   static_assert(RA % RPI == 0 && NI % NW == 0 && RA % 32 == 0 && RB % 64 == 0, "tile shape");
   static_assert(ST >= 2 && (ST - 2) * PER_WAVE < 64, "stages");
@@ -177,36 +175,32 @@ __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
     }
   }
   wait_vmcnt<0>();
-  __syncthreads();
 
-  // epilogue: C[er][q] -> out row (row0 + er/2), real column 2q + er%2, via LDS
-  __bf16* cs = reinterpret_cast<__bf16*>(smem);
+  // epilogue straight from the accumulators: registers r and r + 1 (r even)
+  // of a lane hold expanded rows 2i and 2i + 1 of its column q, i.e. the real
+  // and imaginary part of output (row0 + i, q0 + q); packed as one bf16 pair,
+  // the 32 lanes of a row write 128 contiguous bytes.  Output spins that do
+  // not exist at this degree are written as zero.
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  const int Np = 2 * Nc;
   const int col_l = lane & 31, row_l = 4 * (lane >> 5);
 #pragma unroll
-  for (int ii = 0; ii < 2; ++ii)
+  for (int jj = 0; jj < 2; ++jj) {
+    const int q = q0 + wn * 64 + jj * 32 + col_l;
+    const bool qok = q < Nc;
+    const bool tok = qok && iabs_(sout_.s[(qok ? q : 0) / Cout]) <= l;
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj)
+    for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int er = wm * 64 + ii * 32 + 8 * (r >> 2) + row_l + (r & 3);
-        const int q = wn * 64 + jj * 32 + col_l;
-        cs[(er >> 1) * G::LDC + 2 * q + (er & 1)] = (__bf16)acc[ii][jj][r];
+      for (int r = 0; r < 16; r += 2) {
+        const int er = wm * 64 + ii * 32 + 8 * (r >> 2) + row_l + (r & 3);  // even
+        const int row = row0 + (er >> 1);
+        if (!qok || row >= Mrows) continue;
+        const f32x2_t v = tok ? (f32x2_t){acc[ii][jj][r], acc[ii][jj][r + 1]} : (f32x2_t){0.f, 0.f};
+        *reinterpret_cast<bf16x2_t*>(out + ((size_t)l * l * B + row) * Np + 2 * q) =
+            __builtin_convertvector(v, bf16x2_t);
       }
-  __syncthreads();
-  const int Np = 2 * Nc;
-  __bf16* O0 = out + ((size_t)l * l * B + row0) * Np + 2 * q0;
-  const int rows = Mrows - row0 < RA ? Mrows - row0 : RA;
-  const int cols = 2 * (Nc - q0 < RB ? Nc - q0 : RB);
-  constexpr int VPR = 2 * RB / 8;
-  for (int idx = tid; idx < RA * VPR; idx += G::NT) {
-    const int row = idx / VPR;
-    const int col = (idx % VPR) * 8;
-    if (row >= rows || col >= cols) continue;
-    uint4 v = *reinterpret_cast<const uint4*>(&cs[row * G::LDC + col]);
-    // output spins that do not exist at this degree are zero
-    const int tq = (q0 + col / 2) / Cout;  // 8 reals = 4 complex outputs, one spin (Cout % 4 == 0)
-    if (iabs_(sout_.s[tq]) > l) v = make_uint4(0, 0, 0, 0);
-    *reinterpret_cast<uint4*>(O0 + (size_t)row * Np + col) = v;
   }
 }
 
