@@ -18,8 +18,7 @@ ICML 2023):
 * the Funk--Hecke projection of isotropic bumps used to synthesise the
   molecule-shaped inputs.
 
-Conventions (the paper fixes them only through eqs. (4) and (6); the readings
-are listed in the design doc):
+Conventions (the paper fixes them only through eqs. (4) and (6)):
 
 * grid: theta_j = pi (2j+1) / (2H), phi_k = 2 pi k / W;
 * Wigner d: d^1_{10}(beta) = -sin(beta)/sqrt(2);
@@ -53,6 +52,11 @@ __all__ = [
     "evaluate",
     "mix",
     "conv",
+    "forward_adjoint",
+    "inverse_adjoint",
+    "mix_adjoint",
+    "filter_grad",
+    "conv_backward",
     "phase_collapse",
     "bump_coefficients",
 ]
@@ -387,6 +391,100 @@ def conv(x: np.ndarray, K: np.ndarray, L: int, spins_in, spins_out) -> np.ndarra
     H, W = x.shape[-2:]
     a = forward(x, L, spins_in)
     return inverse(mix(a, K, spins_in, spins_out), H, W, spins_out)
+
+
+# --------------------------------------------------------------------------
+# Backward pass of the layer (adjoints of the linear maps above)
+#
+# For a real loss of the complex output y with gradient g = dL/dy in the
+# convention dL = Re <g, dy> (complex inner product <u, v> = sum conj(u) v),
+# a linear map y = A x has input gradient A^H g.  The layer is
+# y = G(K . F(x)): F the weighted analysis (eq. (2) by quadrature), K the
+# per-degree mixing, G the synthesis (eq. (3)).
+# --------------------------------------------------------------------------
+
+def _quadrature_weights(H: int, W: int) -> np.ndarray:
+    """q_j = (2 pi / W) w_j: the weight of every sample of latitude j in eq. (2)."""
+    return (2.0 * np.pi / W) * dh_weights(H)
+
+
+def forward_adjoint(coef: np.ndarray, H: int, W: int, spins) -> np.ndarray:
+    """F^H: the forward transform's matrix has entries q_j conj(sY_lm(theta_j, phi_k)),
+    so its adjoint is x[j, k] = q_j sum_lm a_lm sY_lm(theta_j, phi_k), i.e. the
+    synthesis of eq. (3) weighted by q_j.  coef [L^2, B, S, C] -> [B, S, C, H, W].
+    Pinned by: <F x, a> = <x, F^H a> (tests/test_oracle_backward.py).
+    """
+    q = _quadrature_weights(H, W)
+    return inverse(coef, H, W, spins) * q[:, None]
+
+
+def inverse_adjoint(y: np.ndarray, L: int, spins) -> np.ndarray:
+    """G^H: a_lm = sum_{j,k} conj(sY_lm(theta_j, phi_k)) y[j, k], the analysis
+    sum of eq. (2) without quadrature weights: forward(y / q_j) (the weights
+    q_j are positive on this grid).  y [B, S, C, H, W] -> [L^2, B, S, C].
+    Pinned by: <G a, y> = <a, G^H y> (tests/test_oracle_backward.py).
+    """
+    y = np.asarray(y, dtype=np.complex128)
+    H, W = y.shape[-2:]
+    q = _quadrature_weights(H, W)
+    return forward(y / q[:, None], L, spins)
+
+
+def mix_adjoint(coef_out: np.ndarray, K: np.ndarray, spins_in, spins_out) -> np.ndarray:
+    """The adjoint of `mix`: a[l^2+l+m, b, s, c] = sum_{t, c'} conj(K[l, t, c', s, c])
+    a'[l^2+l+m, b, t, c'] over |t| <= l, for |s| <= l (else 0).
+    coef_out [L^2, B, S_out, C_out] -> [L^2, B, S_in, C_in].
+    Pinned by: <mix(a), a'> = <a, mix^H(a')> (tests/test_oracle_backward.py).
+    """
+    coef_out = np.asarray(coef_out, dtype=np.complex128)
+    K = np.asarray(K, dtype=np.complex128)
+    L2, B, T, Co = coef_out.shape
+    L, S, C = K.shape[0], K.shape[3], K.shape[4]
+    out = np.zeros((L2, B, S, C), dtype=np.complex128)
+    sin_ = np.abs(np.asarray(list(spins_in)))
+    sout = np.abs(np.asarray(list(spins_out)))
+    for l in range(L):
+        Kl = K[l] * (sout[:, None, None, None] <= l) * (sin_[None, None, :, None] <= l)
+        rows = slice(l * l, (l + 1) * (l + 1))
+        g = coef_out[rows].reshape(-1, T * Co)               # [(2l+1) B, T Co]
+        out[rows] = (g @ np.conj(Kl.reshape(T * Co, S * C))).reshape(2 * l + 1, B, S, C)
+    return out
+
+
+def filter_grad(coef_out_grad: np.ndarray, coef: np.ndarray, spins_in, spins_out) -> np.ndarray:
+    """Gradient of the filters of `mix`: since a' = K a per degree,
+    dL/dK[l, t, c', s, c] = sum_{|m| <= l, b} g'[l^2+l+m, b, t, c'] conj(a[l^2+l+m, b, s, c]),
+    zero where |s| > l or |t| > l.  Returns [L, S_out, C_out, S_in, C_in].
+    Pinned by: Re <dL/dK, dK> = d/dh Re <g', mix(a; K + h dK)> and an explicit
+    loop over (l, m, b) (tests/test_oracle_backward.py).
+    """
+    g = np.asarray(coef_out_grad, dtype=np.complex128)
+    a = np.asarray(coef, dtype=np.complex128)
+    L2, B, T, Co = g.shape
+    S, C = a.shape[2], a.shape[3]
+    L = int(round(math.sqrt(L2)))
+    gK = np.zeros((L, T, Co, S, C), dtype=np.complex128)
+    sin_ = np.abs(np.asarray(list(spins_in)))
+    sout = np.abs(np.asarray(list(spins_out)))
+    for l in range(L):
+        rows = slice(l * l, (l + 1) * (l + 1))
+        gl = g[rows].reshape(-1, T * Co)                     # [(2l+1) B, T Co]
+        al = a[rows].reshape(-1, S * C)
+        gK[l] = (gl.T @ np.conj(al)).reshape(T, Co, S, C)
+        gK[l] *= (sout[:, None, None, None] <= l) * (sin_[None, None, :, None] <= l)
+    return gK
+
+
+def conv_backward(x: np.ndarray, K: np.ndarray, grad_y: np.ndarray, L: int, spins_in,
+                  spins_out):
+    """Input and filter gradients of `conv` for output gradient grad_y:
+    grad_x = F^H (K^H (G^H grad_y)), grad_K = filter_grad(G^H grad_y, F x)."""
+    H, W = x.shape[-2:]
+    g_out = inverse_adjoint(grad_y, L, spins_out)
+    a = forward(x, L, spins_in)
+    grad_K = filter_grad(g_out, a, spins_in, spins_out)
+    grad_x = forward_adjoint(mix_adjoint(g_out, K, spins_in, spins_out), H, W, spins_in)
+    return grad_x, grad_K
 
 
 # --------------------------------------------------------------------------

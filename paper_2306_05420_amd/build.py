@@ -3,7 +3,8 @@
     python -m paper_2306_05420_amd.build        (or build() from Python)
 
 Every HIP source is compiled with packed-FP32 instruction selection turned
-off and -O3; objects go to paper_2306_05420_amd/_build/.
+off (packed FP32 instructions are avoided on this target) and -O3; objects go
+to paper_2306_05420_amd/_build/.
 """
 
 from __future__ import annotations
