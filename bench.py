@@ -5,7 +5,7 @@ spins {0,1} -> {0,1}, 256 -> 256 channels, bfloat16 storage with float32
 accumulation (the large weather-shaped workload).
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
-    python bench.py --table            (every workload: layer, transforms, stack)
+    python bench.py --table            (every workload: layer, transforms, backward, stack)
     python bench.py --summarize-counters FETCH_CSV WRITE_CSV
 
 Prints one JSON line.  A step is one layer call (forward transform, per-degree
@@ -267,6 +267,7 @@ def main(argv=None):
         "stages": r["stages"],
         "roofline": r["roofline"],
         "transforms": r["transforms"],
+        "backward": r["backward"],
     }
     if "stack2" in r:
         out["stack2"] = r["stack2"]
@@ -393,7 +394,8 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
                              "TFLOP/s": round(fl / t / 1e12, 2)}
     r = {"w": w, "value": 1.0 / t_layer, "ms_per_step": t_layer * 1e3,
          "tflops": useful / t_layer / 1e12, "useful": useful, "stages": stages,
-         "roofline": roof, "transforms": transforms}
+         "roofline": roof, "transforms": transforms,
+         "backward": measure_backward(plan, w, x, K, y, steps, warmup)}
 
     if name == "mol":
         # two stacked layers with the phase collapse between them
@@ -420,6 +422,41 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
     return r
 
 
+def backward_flops(w) -> int:
+    """Useful flops of one backward call (both gradients): G^H on the output
+    gradient and F on x (forward-transform contractions), the filter gradient
+    and the adjoint mixing (each as many as the mixing), F^H (an inverse
+    contraction over the input spins)."""
+    work = stage_work(w)
+    H, L, B = w.H, w.L, w.B
+    lat_out = sum(4 * H * B * w.C_out * (L * L - t * t) for t in w.spins_out)
+    return 2 * work["lat_fwd"]["flops"] + lat_out + 2 * work["mix"]["flops"]
+
+
+def measure_backward(plan, w, x, K, grad_y, steps: int, warmup: int) -> dict:
+    """Time spin_sph_conv_backward (grad_x and grad_filters) with per-stage
+    HIP events over a second pass."""
+    import torch
+
+    gx = plan.empty(w.B, len(w.spins_in), w.C_in, w.H, w.W)
+    gk = plan.empty(w.L, len(w.spins_out), w.C_out, len(w.spins_in), w.C_in)
+    fn = lambda: plan.conv_backward(x, K, grad_y, grad_x=gx, grad_filters=gk)
+    t = _time_calls(fn, steps, warmup)
+    plan.stage_timing(True)
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    times = plan.stage_times()
+    plan.stage_timing(False)
+    fl = backward_flops(w)
+    # per call: stage -> (microseconds, launches)
+    stages = {k: {"us_per_call": round(ms * 1e3 / steps, 2), "launches_per_call": n // steps}
+              for k, (ms, n) in times.items()}
+    return {"us": round(t * 1e6, 2), "per_s": round(1.0 / t, 1),
+            "TFLOP/s": round(fl / t / 1e12, 2), "useful_gflop": round(fl / 1e9, 3),
+            "stages": stages}
+
+
 TABLE_HEAD = ("| Cfg | Op | median µs | calls/s | useful TFLOP/s | % MFMA peak | "
               "GB/s (DFT stages fwd / inv) | % HBM roofline (dominant stage) |\n"
               "|---|---|---|---|---|---|---|---|")
@@ -436,6 +473,9 @@ def table_rows(cfg: int, r: dict):
         t = r["transforms"][op]
         rows.append(f"| {cfg} {w.name} | swsft_{op} | {t['us']:.1f} | {t['per_s']:.0f} | "
                     f"{t['TFLOP/s']:.1f} | {100 * t['TFLOP/s'] / peak:.1f} | {t['GB/s']:.0f} (whole transform) | — |")
+    t = r["backward"]
+    rows.append(f"| {cfg} {w.name} | layer backward (grad_x, grad_filters) | {t['us']:.1f} | "
+                f"{t['per_s']:.0f} | {t['TFLOP/s']:.1f} | {100 * t['TFLOP/s'] / peak:.1f} | — | — |")
     if "stack2" in r:
         t = r["stack2"]
         rows.append(f"| {cfg} {w.name} | 2 layers + phase collapse | {t['us']:.1f} | {t['per_s']:.0f} | "

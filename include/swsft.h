@@ -76,15 +76,16 @@ typedef enum {
 typedef enum {
   SWSFT_OP_FORWARD = 0, /* swsft_forward          */
   SWSFT_OP_INVERSE = 1, /* swsft_inverse          */
-  SWSFT_OP_CONV = 2     /* spin_sph_conv_forward  */
+  SWSFT_OP_CONV = 2,    /* spin_sph_conv_forward  */
+  SWSFT_OP_CONV_BACKWARD = 3 /* spin_sph_conv_backward */
 } swsft_op;
 
 /*
  * Create a plan for H x W grids with bandlimit L (Background, eqs. (2)-(3)).
  *  H, W        grid size; H == W (the transform needs equal sample counts on
- *              both axes, appendix "WeatherBench"), H even.  This build
- *              implements W a power of two in [2, 512]; other even sizes
- *              return SWSFT_E_UNSUPPORTED.
+ *              both axes, appendix "WeatherBench"), H even.  Implemented:
+ *              W a power of two in [2, 512]; other even sizes return
+ *              SWSFT_E_UNSUPPORTED.
  *  L           bandlimit, 1 <= L <= H/2 (L < H/2 is spectral pooling:
  *              Method, "Spectral pooling").
  *  spins_in    host array of n_spins_in distinct spins, |s| < L, 1..8 of them.
@@ -146,6 +147,33 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
                                    void* stream);
 
 /*
+ * Backward pass of spin_sph_conv_forward: the gradients that training needs.
+ * For a real loss L with output gradient grad_y = dL/dy in the convention
+ * dL = Re sum conj(grad_y) dy (the convention of torch's complex autograd),
+ * the layer y = G(K F x) -- F the quadrature analysis of eq. (2), K the
+ * per-degree mixing, G the synthesis of eq. (3), all linear -- has
+ *   grad_x       = F^H (K^H (G^H grad_y)),
+ *   grad_filters[l][t][c'][s][c] = sum_{|m|<=l, b} g[l*l+l+m][b][t][c'] conj(a[l*l+l+m][b][s][c]),
+ * with g = G^H grad_y (the analysis sum of eq. (2) without quadrature
+ * weights), a = F x, and zeros where |s| > l or |t| > l.  F^H is the
+ * synthesis of eq. (3) weighted by (2 pi / W) w_j; K^H applies conj(K).
+ *  x             [B][S_in][C_in][H][W] complex; read when grad_filters != NULL.
+ *  filters       [L][S_out][C_out][S_in][C_in] complex; read when grad_x != NULL.
+ *  grad_y        [B][S_out][C_out][H][W] complex, read only.
+ *  grad_x        [B][S_in][C_in][H][W] complex, written; NULL: not computed.
+ *  grad_filters  [L][S_out][C_out][S_in][C_in] complex, written; NULL: not computed.
+ *  At least one output must be requested.  Outputs must not overlap each
+ *  other or an input that is read; an input that no requested output needs
+ *  (x for grad_x alone, filters for grad_filters alone) may be NULL.
+ *  Returns SWSFT_E_INVALID / SWSFT_E_WORKSPACE on bad arguments before any
+ *  launch, SWSFT_E_HIP if a launch fails.
+ *  ws  workspace of ws_bytes >= swsft_workspace_bytes(p, SWSFT_OP_CONV_BACKWARD, B, C_in, C_out).
+ */
+swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, const void* x,
+                                    const void* filters, const void* grad_y, void* grad_x,
+                                    void* grad_filters, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Phase-collapse nonlinearity (Method, "Phase collapse nonlinearity") on a
  * spatial feature map with the plan's spins_out, which must contain spin 0:
  * at every grid point, x0 <- W1 x0 + W2 |x| + b, where x0 are the C spin-0
@@ -192,6 +220,10 @@ const char* swsft_stage_name(int stage);
  *  which 1: inverse table, [2L-1][H][Lp] per spins_out entry:
  *           (-1)^s sqrt((2l+1)/(4 pi)) d^l_{m,-s}(theta_j), Lp = L rounded
  *           up to a multiple of 8.
+ *  which 2: backward synthesis table, [2L-1][H][Lp] per spins_in entry: the
+ *           values of table 0 in the layout of table 1.
+ *  which 3: backward analysis table, [2L-1][L][Hp] per spins_out entry: the
+ *           values of table 1 in the layout of table 0.
  *  Elements are of the plan's storage type.  `bytes` must equal the table
  *  size; returns SWSFT_E_INVALID otherwise.
  */

@@ -21,7 +21,8 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libswsft.so")
 INCLUDE = os.path.join(os.path.dirname(PKG), "include")
 
-SOURCES = ["tables.hip", "dft.hip", "gemm.hip", "mix_dma.hip", "lat_dma.hip", "phase_collapse.hip", "swsft_api.cpp"]
+SOURCES = ["tables.hip", "dft.hip", "gemm.hip", "mix_dma.hip", "lat_dma.hip", "phase_collapse.hip",
+           "backward.hip", "swsft_api.cpp"]
 ARCH = "gfx950"
 
 

@@ -1,0 +1,398 @@
+// Backward pass of the spectral convolution layer (Method, eqs. (2)-(3) and
+// the per-degree mixing): the two kernels that have no forward counterpart.
+//
+//  filter_adjoint  KH[l][(s,c)][(t,c')] = conj(K[l][(t,c')][(s,c)]): the
+//                  filters of the adjoint mixing K^H, in the row-major
+//                  [out][in] layout that the mixing GEMM reads.
+//  filter_grad     gK[l][(t,c')][(s,c)] = sum_{(m,b)} g[l][(m,b)][(t,c')] conj(a[l][(m,b)][(s,c)]),
+//                  the derivative of a real loss with respect to the filters
+//                  (one complex GEMM per degree l, contraction length (2l+1) B).
+//
+// filter_grad as a real MFMA GEMM: the complex product g conj(a) splits into
+//   Re = sum gr ar + gi ai,  Im = sum gi ar - gr ai,
+// so per 16-wide slice of output rows t' the tile takes 16 "real" rows and 16
+// "imaginary" rows, and the contraction index is (k, rho), rho in {re, im}:
+//   real rows: A = [gr | gi],   imaginary rows: A = [gi | -gr],   B = [ar ; ai].
+// g and a are staged in LDS as separate real and imaginary planes [k][channel]
+// (de-interleaved on the way in), so every MFMA operand is one plane read
+// along k: ds_read_b64_tr_b16 for bf16 (lanes of a 16-lane group take 16
+// consecutive channels, 4 consecutive k each), one dword per lane for fp32.
+#include <type_traits>
+
+#include "mfma_tile.h"
+#include "swsft_internal.h"
+#include "xcd.h"
+
+namespace swsft {
+namespace {
+
+struct Spins {
+  int s[kMaxSpins];
+};
+
+__device__ __forceinline__ int iabs_(int v) { return v < 0 ? -v : v; }
+
+// ---------------------------------------------------------------- adjoint
+constexpr int TA = 64;  // transpose tile (complex elements per side)
+
+template <typename T>
+struct Cplx;
+template <>
+struct Cplx<float> {
+  typedef float2 type;
+  __device__ static float2 conj(float2 v) { return make_float2(v.x, -v.y); }
+};
+template <>
+struct Cplx<__bf16> {
+  typedef unsigned type;  // (re, im) bf16 pair, im in the high half
+  __device__ static unsigned conj(unsigned v) { return v ^ 0x80000000u; }
+};
+
+template <typename T>
+__global__ void __launch_bounds__(256) filter_adjoint_kernel(const typename Cplx<T>::type* __restrict__ K,
+                                                             typename Cplx<T>::type* __restrict__ KH,
+                                                             int Nc, int Kc, int tiles_r, int tiles_c) {
+  using V = typename Cplx<T>::type;
+  __shared__ V tile[TA][TA + 1];
+  const int per_l = tiles_r * tiles_c;
+  const int l = blockIdx.x / per_l;
+  const int t = blockIdx.x % per_l;
+  const int r0 = (t / tiles_c) * TA, c0 = (t % tiles_c) * TA;
+  const size_t base = (size_t)l * Nc * Kc;
+  for (int idx = threadIdx.x; idx < TA * TA; idx += 256) {
+    const int r = idx / TA, c = idx % TA;
+    if (r0 + r < Nc && c0 + c < Kc) tile[r][c] = K[base + (size_t)(r0 + r) * Kc + c0 + c];
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < TA * TA; idx += 256) {
+    const int c = idx / TA, r = idx % TA;  // output row (s,c), output column (t,c')
+    if (r0 + r < Nc && c0 + c < Kc) KH[base + (size_t)(c0 + c) * Nc + r0 + r] = Cplx<T>::conj(tile[r][c]);
+  }
+}
+
+// ---------------------------------------------------------------- filter gradient
+constexpr int GBM = 64;   // output rows (t,c') per workgroup: 4 slices of 16
+constexpr int GBN = 128;  // output columns (s,c) per workgroup: 4 MFMA columns of 32
+constexpr int GBK = 32;   // contraction rows (m,b) per LDS stage
+constexpr int GNT = 256;  // 4 waves, 2 x 2: each owns 2 row slices x 2 column tiles
+
+template <typename T>
+struct GradGeom {
+  // Plane pitches and gaps in elements.  bf16: a row stride of 8 dwords past
+  // a multiple of 32 puts the 4 rows of one transposed read on distinct
+  // banks, and the real and imaginary g planes (read by neighbouring 16-lane
+  // groups of one instruction) start 32 dwords apart modulo 64.  fp32: rows
+  // k and k + 1 (the two half-waves) 32 dwords apart, the g planes 16 apart.
+  static constexpr bool BF = std::is_same<T, __bf16>::value;
+  static constexpr int PG = BF ? GBM + 16 : GBM + 32;
+  static constexpr int PA = BF ? GBN + 16 : GBN + 32;
+  static constexpr int PLANE_G = GBK * PG + (BF ? 64 : 16), PLANE_A = GBK * PA;
+  static constexpr int G_CHUNKS = GBK * GBM / 4 / GNT;  // 4-complex chunks per thread
+  static constexpr int A_CHUNKS = GBK * GBN / 4 / GNT;
+  static constexpr int SMEM = (2 * PLANE_G + 2 * PLANE_A) * (int)sizeof(T);
+};
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+
+template <typename T>
+struct Chunk {  // 4 consecutive complex values, de-interleaved
+  float re[4], im[4];
+};
+
+template <typename T, bool VEC>
+__device__ __forceinline__ void load_chunk(const T* __restrict__ src, size_t row_off, int col,
+                                           int ncols, bool row_ok, Chunk<T>& ch) {
+  // src row starts at row_off (reals); col is the first of 4 complex columns
+#pragma unroll
+  for (int e = 0; e < 4; ++e) ch.re[e] = ch.im[e] = 0.f;
+  if (!row_ok) return;
+  const T* p = src + row_off + 2 * (size_t)col;
+  if constexpr (VEC) {
+    if (col >= ncols) return;  // ncols % 4 == 0: a chunk is all in or all out
+    if constexpr (std::is_same<T, float>::value) {
+      const float4 u = *reinterpret_cast<const float4*>(p);
+      const float4 v = *reinterpret_cast<const float4*>(p + 4);
+      ch.re[0] = u.x; ch.im[0] = u.y; ch.re[1] = u.z; ch.im[1] = u.w;
+      ch.re[2] = v.x; ch.im[2] = v.y; ch.re[3] = v.z; ch.im[3] = v.w;
+    } else {
+      typedef __bf16 v8b __attribute__((ext_vector_type(8)));
+      const v8b u = *reinterpret_cast<const v8b*>(p);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ch.re[e] = (float)u[2 * e];
+        ch.im[e] = (float)u[2 * e + 1];
+      }
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (col + e < ncols) {
+        ch.re[e] = (float)p[2 * e];
+        ch.im[e] = (float)p[2 * e + 1];
+      }
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store_chunk(T* re_plane, T* im_plane, int off, const Chunk<T>& ch) {
+  if constexpr (std::is_same<T, float>::value) {
+    *reinterpret_cast<float4*>(re_plane + off) = make_float4(ch.re[0], ch.re[1], ch.re[2], ch.re[3]);
+    *reinterpret_cast<float4*>(im_plane + off) = make_float4(ch.im[0], ch.im[1], ch.im[2], ch.im[3]);
+  } else {
+    typedef __bf16 v4b __attribute__((ext_vector_type(4)));
+    v4b r, i;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      r[e] = (__bf16)ch.re[e];
+      i[e] = (__bf16)ch.im[e];
+    }
+    *reinterpret_cast<v4b*>(re_plane + off) = r;
+    *reinterpret_cast<v4b*>(im_plane + off) = i;
+  }
+}
+
+// lane i of a 16-lane group addresses row k + i/4, columns col + 4 (i%4) .. +3;
+// lane L of the group receives plane[k + e][col + L] for e = 0..3
+__device__ __forceinline__ v4s tr4(const __bf16* plane, int pitch, int k, int col, int gl) {
+  const __bf16* p = plane + (k + (gl >> 2)) * pitch + col + 4 * (gl & 3);
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4s*)((__attribute__((address_space(3))) __bf16*)p));
+}
+
+__device__ __forceinline__ v8bf cat8(v4s lo, v4s hi, unsigned flip) {
+  typedef unsigned v4u __attribute__((ext_vector_type(4)));
+  v4u u;
+  u[0] = ((unsigned)(unsigned short)lo[0] | ((unsigned)(unsigned short)lo[1] << 16)) ^ flip;
+  u[1] = ((unsigned)(unsigned short)lo[2] | ((unsigned)(unsigned short)lo[3] << 16)) ^ flip;
+  u[2] = ((unsigned)(unsigned short)hi[0] | ((unsigned)(unsigned short)hi[1] << 16)) ^ flip;
+  u[3] = ((unsigned)(unsigned short)hi[2] | ((unsigned)(unsigned short)hi[3] << 16)) ^ flip;
+  return __builtin_bit_cast(v8bf, u);
+}
+
+// Degree numbering: q -> l alternates between the top and the bottom of the
+// range (L-1, 0, L-2, 1, ...), so any run of consecutive q (one XCD's share
+// of the grid) pairs long contractions with short ones.
+__device__ __forceinline__ int paired_degree(int q, int L) { return (q & 1) ? (q >> 1) : L - 1 - (q >> 1); }
+
+template <typename T, bool VEC>
+__global__ void __launch_bounds__(GNT) filter_grad_kernel(const T* __restrict__ a,
+                                                          const T* __restrict__ g, T* __restrict__ gK,
+                                                          int L, int B, int Cin, int Cout, int n_in,
+                                                          int n_out, Spins sin_, Spins sout_,
+                                                          int tiles_r, int tiles_c) {
+  using G = GradGeom<T>;
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  T* Gr = reinterpret_cast<T*>(smem_raw);
+  T* Gi = Gr + G::PLANE_G;
+  T* Ar = Gi + G::PLANE_G;
+  T* Ai = Ar + G::PLANE_A;
+
+  const int per_l = tiles_r * tiles_c;
+  const int lb = xcd_logical_block();
+  if (lb >= L * per_l) return;
+  const int l = paired_degree(lb / per_l, L);
+  const int tile = lb % per_l;
+  const int r0 = (tile / tiles_c) * GBM, c0 = (tile % tiles_c) * GBN;
+  const int Nc = n_out * Cout, Kc = n_in * Cin;
+  const int Kl = (2 * l + 1) * B;               // contraction length
+  const size_t row0 = (size_t)l * l * B;        // first (m,b) row of degree l
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+
+  // whole-tile spin test: every row or every column belongs to a spin that
+  // does not exist at degree l
+  bool rows_dead = true, cols_dead = true;
+  for (int t = r0 / Cout; t <= (min(r0 + GBM, Nc) - 1) / Cout; ++t)
+    if (iabs_(sout_.s[t]) <= l) rows_dead = false;
+  for (int s = c0 / Cin; s <= (min(c0 + GBN, Kc) - 1) / Cin; ++s)
+    if (iabs_(sin_.s[s]) <= l) cols_dead = false;
+
+  v16f acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  if (!rows_dead && !cols_dead) {
+    Chunk<T> cg[G::G_CHUNKS], ca[G::A_CHUNKS];
+    auto load = [&](int k0) {
+#pragma unroll
+      for (int u = 0; u < G::G_CHUNKS; ++u) {
+        const int idx = u * GNT + tid;
+        const int kr = idx / (GBM / 4), cc = 4 * (idx % (GBM / 4));
+        const bool ok = k0 + kr < Kl;
+        load_chunk<T, VEC>(g, (row0 + k0 + kr) * Nc * 2, r0 + cc, Nc, ok, cg[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < G::A_CHUNKS; ++u) {
+        const int idx = u * GNT + tid;
+        const int kr = idx / (GBN / 4), cc = 4 * (idx % (GBN / 4));
+        const bool ok = k0 + kr < Kl;
+        load_chunk<T, VEC>(a, (row0 + k0 + kr) * Kc * 2, c0 + cc, Kc, ok, ca[u]);
+      }
+    };
+    auto store = [&]() {
+#pragma unroll
+      for (int u = 0; u < G::G_CHUNKS; ++u) {
+        const int idx = u * GNT + tid;
+        const int kr = idx / (GBM / 4), cc = 4 * (idx % (GBM / 4));
+        store_chunk<T>(Gr, Gi, kr * G::PG + cc, cg[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < G::A_CHUNKS; ++u) {
+        const int idx = u * GNT + tid;
+        const int kr = idx / (GBN / 4), cc = 4 * (idx % (GBN / 4));
+        store_chunk<T>(Ar, Ai, kr * G::PA + cc, ca[u]);
+      }
+    };
+
+    const int nkb = (Kl + GBK - 1) / GBK;
+    load(0);
+    store();
+    __syncthreads();
+    for (int kb = 0; kb < nkb; ++kb) {
+      if (kb + 1 < nkb) load((kb + 1) * GBK);
+      if constexpr (G::BF) {
+        const int grp = lane >> 4, gl = lane & 15;
+        const int half = grp & 1, kq = grp >> 1;
+        const unsigned flip1 = half ? 0x80008000u : 0u;  // imaginary rows take -gr
+#pragma unroll
+        for (int ks = 0; ks < GBK; ks += 16) {
+          const int kb8 = ks + 8 * kq;
+#pragma unroll
+          for (int rho = 0; rho < 2; ++rho) {
+            const __bf16* pa = (rho == 0) == (half == 0) ? Gr : Gi;
+            const __bf16* pb = rho == 0 ? Ar : Ai;
+            v8bf av[2], bv[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+              const int col = wr * 32 + i * 16;
+              av[i] = cat8(tr4(pa, G::PG, kb8, col, gl), tr4(pa, G::PG, kb8 + 4, col, gl),
+                           rho ? flip1 : 0u);
+            }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+              const int col = wc * 64 + j * 32 + 16 * half;
+              bv[j] = cat8(tr4(pb, G::PA, kb8, col, gl), tr4(pb, G::PA, kb8 + 4, col, gl), 0u);
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+              for (int j = 0; j < 2; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+          }
+        }
+      } else {
+        const int r32 = lane & 31, kh = lane >> 5, half = r32 >> 4;
+        const float sgn1 = half ? -1.f : 1.f;
+#pragma unroll 4
+        for (int kk = 0; kk < GBK; kk += 2) {
+          const int k = kk + kh;
+#pragma unroll
+          for (int rho = 0; rho < 2; ++rho) {
+            const float* pa = (rho == 0) == (half == 0) ? Gr : Gi;
+            const float* pb = rho == 0 ? Ar : Ai;
+            float av[2], bv[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+              av[i] = (rho ? sgn1 : 1.f) * pa[k * G::PG + wr * 32 + i * 16 + (r32 & 15)];
+#pragma unroll
+            for (int j = 0; j < 2; ++j) bv[j] = pb[k * G::PA + wc * 64 + j * 32 + r32];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+              for (int j = 0; j < 2; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+          }
+        }
+      }
+      __syncthreads();
+      if (kb + 1 < nkb) {
+        store();
+        __syncthreads();
+      }
+    }
+  }
+
+  // epilogue: registers (r, r + 8) of a lane are the real and imaginary parts
+  // of one output; zeros where a spin does not exist at degree l
+  T* out = gK + (size_t)l * Nc * Kc * 2;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int sc = c0 + wc * 64 + j * 32 + (lane & 31);
+      if (sc >= Kc) continue;
+      const bool col_live = iabs_(sin_.s[sc / Cin]) <= l;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const int tc = r0 + wr * 32 + i * 16 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (tc >= Nc) continue;
+        const bool live = col_live && iabs_(sout_.s[tc / Cout]) <= l;
+        const float re = live ? acc[i][j][r] : 0.f, im = live ? acc[i][j][r + 8] : 0.f;
+        T* o = out + ((size_t)tc * Kc + sc) * 2;
+        if constexpr (G::BF) {
+          typedef float f32x2 __attribute__((ext_vector_type(2)));
+          typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+          *reinterpret_cast<bf16x2*>(o) = __builtin_convertvector((f32x2){re, im}, bf16x2);
+        } else {
+          *reinterpret_cast<float2*>(o) = make_float2(re, im);
+        }
+      }
+    }
+}
+
+Spins to_spins(const int* s, int n) {
+  Spins r{};
+  for (int i = 0; i < n && i < kMaxSpins; ++i) r.s[i] = s[i];
+  return r;
+}
+
+template <typename T>
+hipError_t filter_grad_t(const Plan& p, int B, int Cin, int Cout, const void* a, const void* g,
+                         void* gK, hipStream_t st) {
+  using G = GradGeom<T>;
+  const int Nc = p.n_out * Cout, Kc = p.n_in * Cin;
+  const int tiles_r = (Nc + GBM - 1) / GBM, tiles_c = (Kc + GBN - 1) / GBN;
+  const long long blocks = (long long)p.L * tiles_r * tiles_c;
+  const bool vec = Nc % 4 == 0 && Kc % 4 == 0;
+  auto kern = vec ? filter_grad_kernel<T, true> : filter_grad_kernel<T, false>;
+  if (G::SMEM > 64 * 1024) {
+    const hipError_t e =
+        hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, G::SMEM);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(GNT), G::SMEM, st, (const T*)a,
+                     (const T*)g, (T*)gK, p.L, B, Cin, Cout, p.n_in, p.n_out,
+                     to_spins(p.spins_in, p.n_in), to_spins(p.spins_out, p.n_out), tiles_r, tiles_c);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t filter_adjoint_t(const Plan& p, int Cin, int Cout, const void* K, void* KH,
+                            hipStream_t st) {
+  using V = typename Cplx<T>::type;
+  const int Nc = p.n_out * Cout, Kc = p.n_in * Cin;
+  const int tr = (Nc + TA - 1) / TA, tc = (Kc + TA - 1) / TA;
+  hipLaunchKernelGGL(filter_adjoint_kernel<T>, dim3((unsigned)((long long)p.L * tr * tc)), dim3(256),
+                     0, st, (const V*)K, (V*)KH, Nc, Kc, tr, tc);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_filter_adjoint(const Plan& p, int C_in, int C_out, const void* K, void* KH,
+                                 hipStream_t st) {
+  if (p.dtype == SWSFT_BF16) return filter_adjoint_t<__bf16>(p, C_in, C_out, K, KH, st);
+  return filter_adjoint_t<float>(p, C_in, C_out, K, KH, st);
+}
+
+hipError_t launch_filter_grad(const Plan& p, int B, int C_in, int C_out, const void* a,
+                              const void* g, void* gK, hipStream_t st) {
+  if (p.dtype == SWSFT_BF16) return filter_grad_t<__bf16>(p, B, C_in, C_out, a, g, gK, st);
+  return filter_grad_t<float>(p, B, C_in, C_out, a, g, gK, st);
+}
+
+}  // namespace swsft

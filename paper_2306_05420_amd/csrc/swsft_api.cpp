@@ -58,6 +58,10 @@ swsft_status check_bc(int B, int C, const char* cname) {
   return SWSFT_OK;
 }
 
+size_t filter_elems(const Plan& p, int Cin, int Cout) {
+  return (size_t)p.L * p.n_out * Cout * p.n_in * Cin * 2;
+}
+
 size_t ws_need(const Plan& p, int op, int B, int Cin, int Cout) {
   const size_t e = p.elem;
   switch (op) {
@@ -70,6 +74,13 @@ size_t ws_need(const Plan& p, int op, int B, int Cin, int Cout) {
       return align_up((xin > xout ? xin : xout) * e) +
              align_up(swsft::coef_elems(p, p.n_in, B, Cin) * e) +
              align_up(swsft::coef_elems(p, p.n_out, B, Cout) * e);
+    }
+    case SWSFT_OP_CONV_BACKWARD: {
+      size_t xin = swsft::xy_elems(p, p.n_in, B, Cin), xout = swsft::xy_elems(p, p.n_out, B, Cout);
+      return align_up((xin > xout ? xin : xout) * e) +
+             2 * align_up(swsft::coef_elems(p, p.n_in, B, Cin) * e) +
+             align_up(swsft::coef_elems(p, p.n_out, B, Cout) * e) +
+             align_up(filter_elems(p, Cin, Cout) * e);
     }
     default:
       return 0;
@@ -133,6 +144,8 @@ void free_plan(Plan* p) {
   if (p == nullptr) return;
   if (p->tab_fwd) (void)hipFree(p->tab_fwd);
   if (p->tab_inv) (void)hipFree(p->tab_inv);
+  if (p->tab_bwd_syn) (void)hipFree(p->tab_bwd_syn);
+  if (p->tab_bwd_ana) (void)hipFree(p->tab_bwd_ana);
   if (p->twiddle) (void)hipFree(p->twiddle);
   if (p->ev) {
     for (int i = 0; i < 2 * swsft::kMaxTimedLaunches; ++i)
@@ -162,7 +175,8 @@ const char* swsft_last_error(void) { return g_last_error; }
 
 const char* swsft_stage_name(int stage) {
   static const char* names[swsft::kNumStages] = {"dft_fwd", "lat_fwd", "mix", "lat_inv",
-                                                 "dft_inv", "phase_collapse", "tables"};
+                                                 "dft_inv", "phase_collapse", "tables",
+                                                 "filter_grad", "filter_adjoint"};
   if (stage < 0 || stage >= swsft::kNumStages) return "";
   return names[stage];
 }
@@ -206,16 +220,21 @@ swsft_status swsft_plan_create(int H, int W, int L, const int* spins_in, int n_s
   }
   const size_t fb = (size_t)p->n_in * p->fwd_table_elems() * p->elem;
   const size_t ib = (size_t)p->n_out * p->inv_table_elems() * p->elem;
+  const size_t sb = (size_t)p->n_in * p->inv_table_elems() * p->elem;   // backward synthesis
+  const size_t ab = (size_t)p->n_out * p->fwd_table_elems() * p->elem;  // backward analysis
   if (hipMalloc(&p->tab_fwd, fb) != hipSuccess || hipMalloc(&p->tab_inv, ib) != hipSuccess ||
+      hipMalloc(&p->tab_bwd_syn, sb) != hipSuccess || hipMalloc(&p->tab_bwd_ana, ab) != hipSuccess ||
       hipMalloc((void**)&p->twiddle, (size_t)W * sizeof(float2)) != hipSuccess) {
     (void)hipGetLastError();
     free_plan(p);
     delete static_cast<swsft_plan_s*>(p);
-    return fail(SWSFT_E_ALLOC, "hipMalloc of %zu + %zu table bytes failed", fb, ib);
+    return fail(SWSFT_E_ALLOC, "hipMalloc of %zu table bytes failed", fb + ib + sb + ab);
   }
   // zero padding and the rows below max(|m|, |s|); the table kernel fills the rest
   if ((e = hipMemset(p->tab_fwd, 0, fb)) != hipSuccess ||
       (e = hipMemset(p->tab_inv, 0, ib)) != hipSuccess ||
+      (e = hipMemset(p->tab_bwd_syn, 0, sb)) != hipSuccess ||
+      (e = hipMemset(p->tab_bwd_ana, 0, ab)) != hipSuccess ||
       (e = swsft::launch_tables(*p, nullptr)) != hipSuccess ||
       (e = hipDeviceSynchronize()) != hipSuccess) {
     free_plan(p);
@@ -319,6 +338,111 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
   return SWSFT_OK;
 }
 
+swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, const void* x,
+                                    const void* filters, const void* grad_y, void* grad_x,
+                                    void* grad_filters, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error[0] = 0;
+  if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
+  SWSFT_TRY(check_bc(B, C_in, "C_in"));
+  SWSFT_TRY(check_bc(B, C_out, "C_out"));
+  if (grad_x == nullptr && grad_filters == nullptr)
+    return fail(SWSFT_E_INVALID, "neither grad_x nor grad_filters requested");
+  SWSFT_TRY(check_ptr(grad_y, "grad_y"));
+  if (grad_filters != nullptr) {
+    SWSFT_TRY(check_ptr(x, "x"));
+    SWSFT_TRY(check_ptr(grad_filters, "grad_filters"));
+  }
+  if (grad_x != nullptr) {
+    SWSFT_TRY(check_ptr(filters, "filters"));
+    SWSFT_TRY(check_ptr(grad_x, "grad_x"));
+  }
+  SWSFT_TRY(check_ws(*p, SWSFT_OP_CONV_BACKWARD, B, C_in, C_out, ws, ws_bytes));
+  {
+    // outputs must not overlap inputs
+    const size_t xs = (size_t)B * p->n_in * C_in * p->H * p->W * 2 * p->elem;
+    const size_t ys = (size_t)B * p->n_out * C_out * p->H * p->W * 2 * p->elem;
+    const size_t ks = filter_elems(*p, C_in, C_out) * p->elem;
+    struct R { const void* a; size_t n; };
+    const R ins[3] = {{grad_filters ? x : nullptr, xs}, {grad_x ? filters : nullptr, ks}, {grad_y, ys}};
+    const R outs[2] = {{grad_x, xs}, {grad_filters, ks}};
+    for (const R& o : outs) {
+      if (o.a == nullptr) continue;
+      for (const R& i : ins) {
+        if (i.a == nullptr) continue;
+        const char *ob = static_cast<const char*>(o.a), *ib = static_cast<const char*>(i.a);
+        if (ob < ib + i.n && ib < ob + o.n) return fail(SWSFT_E_INVALID, "an output overlaps an input");
+      }
+    }
+    if (grad_x && grad_filters) {
+      const char *a = static_cast<const char*>(grad_x), *b = static_cast<const char*>(grad_filters);
+      if (a < b + ks && b < a + xs) return fail(SWSFT_E_INVALID, "grad_x and grad_filters overlap");
+    }
+  }
+  SWSFT_TRY(check_device(*p));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const size_t xin = swsft::xy_elems(*p, p->n_in, B, C_in);
+  const size_t xout = swsft::xy_elems(*p, p->n_out, B, C_out);
+  char* w = static_cast<char*>(ws);
+  void* XY = w;
+  w += align_up((xin > xout ? xin : xout) * p->elem);
+  void* a_in = w;  // F x
+  w += align_up(swsft::coef_elems(*p, p->n_in, B, C_in) * p->elem);
+  void* g_in = w;  // K^H g
+  w += align_up(swsft::coef_elems(*p, p->n_in, B, C_in) * p->elem);
+  void* g_out = w;  // G^H grad_y
+  w += align_up(swsft::coef_elems(*p, p->n_out, B, C_out) * p->elem);
+  void* KH = w;
+
+  // Views of the plan for the adjoint stages (shallow copies, nothing owned):
+  // G^H grad_y is the forward latitude GEMM with the unweighted l-major table
+  // on the output spins; K^H swaps the roles of the spin lists; F^H is the
+  // inverse latitude GEMM with the weighted j-major table on the input spins.
+  Plan ana = *p;
+  ana.tab_fwd = p->tab_bwd_ana;
+  ana.n_in = p->n_out;
+  for (int i = 0; i < swsft::kMaxSpins; ++i) ana.spins_in[i] = p->spins_out[i];
+  Plan adj = *p;
+  adj.n_in = p->n_out;
+  adj.n_out = p->n_in;
+  for (int i = 0; i < swsft::kMaxSpins; ++i) {
+    adj.spins_in[i] = p->spins_out[i];
+    adj.spins_out[i] = p->spins_in[i];
+  }
+  Plan syn = *p;
+  syn.tab_inv = p->tab_bwd_syn;
+  syn.n_out = p->n_in;
+  for (int i = 0; i < swsft::kMaxSpins; ++i) syn.spins_out[i] = p->spins_in[i];
+
+  SWSFT_TRY(run_stage(*p, swsft::kStageDftFwd, st, "dft_fwd", [&] {
+    return swsft::launch_dft_fwd(*p, p->n_out, B, C_out, grad_y, XY, st);
+  }));
+  SWSFT_TRY(run_stage(*p, swsft::kStageLatFwd, st, "lat_fwd",
+                      [&] { return swsft::launch_lat_fwd(ana, B, C_out, XY, g_out, st); }));
+  if (grad_filters != nullptr) {
+    SWSFT_TRY(run_stage(*p, swsft::kStageDftFwd, st, "dft_fwd",
+                        [&] { return swsft::launch_dft_fwd(*p, p->n_in, B, C_in, x, XY, st); }));
+    SWSFT_TRY(run_stage(*p, swsft::kStageLatFwd, st, "lat_fwd",
+                        [&] { return swsft::launch_lat_fwd(*p, B, C_in, XY, a_in, st); }));
+    SWSFT_TRY(run_stage(*p, swsft::kStageFilterGrad, st, "filter_grad", [&] {
+      return swsft::launch_filter_grad(*p, B, C_in, C_out, a_in, g_out, grad_filters, st);
+    }));
+  }
+  if (grad_x != nullptr) {
+    SWSFT_TRY(run_stage(*p, swsft::kStageFilterAdjoint, st, "filter_adjoint", [&] {
+      return swsft::launch_filter_adjoint(*p, C_in, C_out, filters, KH, st);
+    }));
+    SWSFT_TRY(run_stage(*p, swsft::kStageMix, st, "mix", [&] {
+      return swsft::launch_mix(adj, B, C_out, C_in, g_out, KH, g_in, st);
+    }));
+    SWSFT_TRY(run_stage(*p, swsft::kStageLatInv, st, "lat_inv",
+                        [&] { return swsft::launch_lat_inv(syn, B, C_in, g_in, XY, st); }));
+    SWSFT_TRY(run_stage(*p, swsft::kStageDftInv, st, "dft_inv", [&] {
+      return swsft::launch_dft_inv(*p, p->n_in, B, C_in, XY, grad_x, st);
+    }));
+  }
+  return SWSFT_OK;
+}
+
 swsft_status spin_sph_phase_collapse(swsft_plan p, int B, int C, const void* x, const void* W1,
                                      const void* W2, const void* bias, void* y, void* stream) {
   g_last_error[0] = 0;
@@ -401,6 +525,14 @@ swsft_status swsft_plan_table(swsft_plan p, int which, int spin_index, void* hos
     if (spin_index < 0 || spin_index >= p->n_out) return fail(SWSFT_E_INVALID, "spin index");
     elems = p->inv_table_elems();
     base = static_cast<const char*>(p->tab_inv) + spin_index * elems * p->elem;
+  } else if (which == 2) {
+    if (spin_index < 0 || spin_index >= p->n_in) return fail(SWSFT_E_INVALID, "spin index");
+    elems = p->inv_table_elems();
+    base = static_cast<const char*>(p->tab_bwd_syn) + spin_index * elems * p->elem;
+  } else if (which == 3) {
+    if (spin_index < 0 || spin_index >= p->n_out) return fail(SWSFT_E_INVALID, "spin index");
+    elems = p->fwd_table_elems();
+    base = static_cast<const char*>(p->tab_bwd_ana) + spin_index * elems * p->elem;
   } else {
     return fail(SWSFT_E_INVALID, "which = %d", which);
   }

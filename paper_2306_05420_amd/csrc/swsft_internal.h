@@ -22,7 +22,9 @@ enum Stage : int {
   kStageDftInv = 4,
   kStagePhaseCollapse = 5,
   kStageTables = 6,
-  kNumStages = 7
+  kStageFilterGrad = 7,
+  kStageFilterAdjoint = 8,
+  kNumStages = 9
 };
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
@@ -42,6 +44,10 @@ struct Plan {
   // device tables
   void* tab_fwd = nullptr;  // [n_in][M][L][Hp]
   void* tab_inv = nullptr;  // [n_out][M][Hp][Lp]   (rows j < H used)
+  // backward pass: weighted factors j-major for spins_in (adjoint of the
+  // analysis), unweighted factors l-major for spins_out (adjoint of the synthesis)
+  void* tab_bwd_syn = nullptr;  // [n_in][M][Hp][Lp]
+  void* tab_bwd_ana = nullptr;  // [n_out][M][L][Hp]
   float2* twiddle = nullptr;  // [W]: exp(-2 pi i r / W)
   // stage timing
   bool timing = false;
@@ -81,6 +87,14 @@ hipError_t launch_lat_inv(const Plan& p, int B, int C, const void* coef, void* Y
 // coef [L^2][B][S_in][C_in] x K -> coef' [L^2][B][S_out][C_out]
 hipError_t launch_mix(const Plan& p, int B, int C_in, int C_out, const void* coef,
                       const void* K, void* coef_out, hipStream_t st);
+// Backward pass (backward.hip, gemm.hip).
+// KH[l][(s,c)][(t,c')] = conj(K[l][(t,c')][(s,c)]): the filters of the adjoint mixing
+hipError_t launch_filter_adjoint(const Plan& p, int C_in, int C_out, const void* K, void* KH,
+                                 hipStream_t st);
+// gK[l][(t,c')][(s,c)] = sum_{(m,b)} g[l][(m,b)][(t,c')] conj(a[l][(m,b)][(s,c)]), zero
+// where |s| > l or |t| > l; a [L^2][B][S_in][C_in], g [L^2][B][S_out][C_out]
+hipError_t launch_filter_grad(const Plan& p, int B, int C_in, int C_out, const void* a,
+                              const void* g, void* gK, hipStream_t st);
 // bf16 latitude GEMMs fed by direct global -> LDS copies (see lat_dma.hip).
 bool lat_fwd_dma_supported(const Plan& p, int B, int C);
 bool lat_inv_dma_supported(const Plan& p, int B, int C);

@@ -7,7 +7,10 @@
 // Driscoll--Healy weights.  These are the latitude factors of the spin
 // harmonics of eqs. (2)-(3); the paper factors the same d^l(theta) through
 // Wigner Delta = d(pi/2) and a torus FFT (eqs. (4)-(6)), which we evaluate
-// directly instead.
+// directly instead.  The backward pass uses the same values in the other
+// layout: the unweighted factors l-major for the output spins (the adjoint of
+// the synthesis is an unweighted analysis) and the weighted factors j-major
+// for the input spins (the adjoint of the analysis is a weighted synthesis).
 //
 // One thread per (spin, m, j) runs the three-term recurrence in l from the
 // single-term seed at l0 = max(|m|, |s|).
@@ -48,9 +51,9 @@ __device__ double wigner_seed(int m, int n, double c, double s) {
   return neg ? -v : v;
 }
 
+// weighted: include (2 pi / W) w_j; l_rows: layout [l][Hp] per (s, m), else [Hp][Lp]
 template <typename T>
-__global__ void tables_kernel(T* __restrict__ tab_fwd, T* __restrict__ tab_inv,
-                              const int* __restrict__ spins_dummy, int s, int si, bool fwd,
+__global__ void tables_kernel(T* __restrict__ tab, int s, int si, bool weighted, bool l_rows,
                               int H, int W, int L, int Hp, int Lp) {
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   const int mi = blockIdx.y;
@@ -65,7 +68,7 @@ __global__ void tables_kernel(T* __restrict__ tab_fwd, T* __restrict__ tab_inv,
   const double theta = pi * (2.0 * j + 1.0) / (2.0 * H);
   const double c = cos(0.5 * theta), sn = sin(0.5 * theta), cb = cos(theta);
   double scale = (s & 1) ? -1.0 : 1.0;
-  if (fwd) {
+  if (weighted) {
     // Driscoll--Healy weight on the offset grid, times the longitude step
     double acc = 0.0;
     for (int p = 0; p < H / 2; ++p) acc += sin((2.0 * p + 1.0) * theta) / (2.0 * p + 1.0);
@@ -76,8 +79,8 @@ __global__ void tables_kernel(T* __restrict__ tab_fwd, T* __restrict__ tab_inv,
   for (int l = l0; l < L; ++l) {
     const double Nl = sqrt((2.0 * l + 1.0) / (4.0 * pi));
     const double v = scale * Nl * dcur;
-    if (fwd) tab_fwd[(((size_t)si * M + mi) * L + l) * Hp + j] = to_storage<T>(v);
-    else     tab_inv[(((size_t)si * M + mi) * Hp + j) * Lp + l] = to_storage<T>(v);
+    if (l_rows) tab[(((size_t)si * M + mi) * L + l) * Hp + j] = to_storage<T>(v);
+    else        tab[(((size_t)si * M + mi) * Hp + j) * Lp + l] = to_storage<T>(v);
     if (l + 1 < L) {
       const double lp = l + 1.0;
       const double a = lp * (2.0 * l + 1.0) / sqrt((lp * lp - (double)m * m) * (lp * lp - (double)n * n));
@@ -105,13 +108,18 @@ hipError_t launch_tables_t(const Plan& p, hipStream_t st) {
   const int M = p.M;
   dim3 block(64);
   dim3 grid((p.H + 63) / 64, M);
-  for (int si = 0; si < p.n_in; ++si)
-    hipLaunchKernelGGL(tables_kernel<T>, grid, block, 0, st, (T*)p.tab_fwd, (T*)nullptr,
-                       (const int*)nullptr, p.spins_in[si], si, true, p.H, p.W, p.L, p.Hp, p.Lp);
-  for (int si = 0; si < p.n_out; ++si)
-    hipLaunchKernelGGL(tables_kernel<T>, grid, block, 0, st, (T*)nullptr, (T*)p.tab_inv,
-                       (const int*)nullptr, p.spins_out[si], si, false, p.H, p.W, p.L, p.Hp,
-                       p.Lp);
+  for (int si = 0; si < p.n_in; ++si) {
+    hipLaunchKernelGGL(tables_kernel<T>, grid, block, 0, st, (T*)p.tab_fwd, p.spins_in[si], si,
+                       true, true, p.H, p.W, p.L, p.Hp, p.Lp);
+    hipLaunchKernelGGL(tables_kernel<T>, grid, block, 0, st, (T*)p.tab_bwd_syn, p.spins_in[si],
+                       si, true, false, p.H, p.W, p.L, p.Hp, p.Lp);
+  }
+  for (int si = 0; si < p.n_out; ++si) {
+    hipLaunchKernelGGL(tables_kernel<T>, grid, block, 0, st, (T*)p.tab_inv, p.spins_out[si], si,
+                       false, false, p.H, p.W, p.L, p.Hp, p.Lp);
+    hipLaunchKernelGGL(tables_kernel<T>, grid, block, 0, st, (T*)p.tab_bwd_ana, p.spins_out[si],
+                       si, false, true, p.H, p.W, p.L, p.Hp, p.Lp);
+  }
   hipLaunchKernelGGL(twiddle_kernel, dim3((p.W + 63) / 64), dim3(64), 0, st, p.twiddle, p.W);
   return hipGetLastError();
 }

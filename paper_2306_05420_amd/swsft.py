@@ -28,8 +28,9 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "swsft.h")
 
 OK, E_INVALID, E_UNSUPPORTED, E_ALLOC, E_HIP, E_WORKSPACE = range(6)
 F32, BF16 = 0, 1
-OP_FORWARD, OP_INVERSE, OP_CONV = 0, 1, 2
-STAGES = ("dft_fwd", "lat_fwd", "mix", "lat_inv", "dft_inv", "phase_collapse", "tables")
+OP_FORWARD, OP_INVERSE, OP_CONV, OP_CONV_BACKWARD = 0, 1, 2, 3
+STAGES = ("dft_fwd", "lat_fwd", "mix", "lat_inv", "dft_inv", "phase_collapse", "tables",
+          "filter_grad", "filter_adjoint")
 
 _lib = None
 
@@ -58,6 +59,7 @@ def lib() -> ctypes.CDLL:
         "swsft_forward": (i, [vp, i, i, vp, vp, vp, sz, vp]),
         "swsft_inverse": (i, [vp, i, i, vp, vp, vp, sz, vp]),
         "spin_sph_conv_forward": (i, [vp, i, i, i, vp, vp, vp, vp, sz, vp]),
+        "spin_sph_conv_backward": (i, [vp, i, i, i, vp, vp, vp, vp, vp, vp, sz, vp]),
         "spin_sph_phase_collapse": (i, [vp, i, i, vp, vp, vp, vp, vp, vp]),
         "swsft_status_string": (ctypes.c_char_p, [i]),
         "swsft_last_error": (ctypes.c_char_p, []),
@@ -225,6 +227,46 @@ class Plan:
                                            _stream_handle(stream)), "spin_sph_conv_forward")
         return y
 
+    def conv_backward(self, x: torch.Tensor, filters: torch.Tensor, grad_y: torch.Tensor,
+                      need_x: bool = True, need_filters: bool = True, grad_x: torch.Tensor = None,
+                      grad_filters: torch.Tensor = None, stream=None):
+        """Gradients of the layer for a real loss with dL = Re sum conj(grad_y) dy:
+        returns (grad_x [B, S_in, C_in, H, W] or None,
+                 grad_filters [L, S_out, C_out, S_in, C_in] or None)."""
+        if not (need_x or need_filters):
+            raise ValueError("request grad_x, grad_filters or both")
+        xr = self.real_view(x)
+        B, S, Cin = xr.shape[:3]
+        self._shape(xr, (B, len(self.spins_in), Cin, self.H, self.W), "x")
+        kr = self.real_view(filters)
+        Cout = kr.shape[2]
+        self._shape(kr, (self.L, len(self.spins_out), Cout, len(self.spins_in), Cin), "filters")
+        gr = self.real_view(grad_y)
+        self._shape(gr, (B, len(self.spins_out), Cout, self.H, self.W), "grad_y")
+        gx_ptr = gk_ptr = None
+        if need_x:
+            if grad_x is None:
+                grad_x = self.empty(B, len(self.spins_in), Cin, self.H, self.W)
+            gxr = self.real_view(grad_x)
+            self._shape(gxr, tuple(xr.shape[:-1]), "grad_x")
+            gx_ptr = gxr.data_ptr()
+        else:
+            grad_x = None
+        if need_filters:
+            if grad_filters is None:
+                grad_filters = self.empty(*kr.shape[:-1])
+            gkr = self.real_view(grad_filters)
+            self._shape(gkr, tuple(kr.shape[:-1]), "grad_filters")
+            gk_ptr = gkr.data_ptr()
+        else:
+            grad_filters = None
+        ws = self.workspace(OP_CONV_BACKWARD, B, Cin, Cout)
+        _check(lib().spin_sph_conv_backward(self._h, B, Cin, Cout, xr.data_ptr(), kr.data_ptr(),
+                                            gr.data_ptr(), gx_ptr, gk_ptr, ws.data_ptr(),
+                                            ws.numel(), _stream_handle(stream)),
+               "spin_sph_conv_backward")
+        return grad_x, grad_filters
+
     def phase_collapse(self, x: torch.Tensor, W1: torch.Tensor, W2: torch.Tensor,
                        bias: torch.Tensor, y: torch.Tensor = None, stream=None) -> torch.Tensor:
         """x0 <- W1 x0 + W2 |x| + b on spins_out (in place if y is x)."""
@@ -248,11 +290,13 @@ class Plan:
     # -- tables and timing -------------------------------------------------
     def table(self, which: int, spin_index: int) -> torch.Tensor:
         """Copy of a plan table on the host (float32 or bfloat16 tensor):
-        which 0: [2L-1, L, Hp] forward; which 1: [2L-1, Hp, Lp] inverse."""
+        which 0: [2L-1, L, Hp] forward; which 1: [2L-1, Hp, Lp] inverse;
+        which 2: [2L-1, Hp, Lp] backward synthesis (input spins);
+        which 3: [2L-1, L, Hp] backward analysis (output spins)."""
         Hp = (self.H + 7) // 8 * 8
         Lp = (self.L + 7) // 8 * 8
         M = 2 * self.L - 1
-        shape = (M, self.L, Hp) if which == 0 else (M, Hp, Lp)
+        shape = (M, self.L, Hp) if which in (0, 3) else (M, Hp, Lp)
         dt = torch.float32 if self.dtype == "f32" else torch.bfloat16
         out = torch.empty(shape, dtype=dt)
         _check(lib().swsft_plan_table(self._h, which, spin_index, out.data_ptr(),

@@ -16,7 +16,7 @@ def L():
 
 def test_exports_every_declared_function(L):
     names = S.header_functions()
-    assert len(names) == 13
+    assert len(names) == 14
     for n in names:
         assert hasattr(L, n), n
 
@@ -58,6 +58,7 @@ def test_calls_reject_null_plan(L):
     assert L.swsft_forward(None, 1, 1, x, x, x, 1 << 30, None) == S.E_INVALID
     assert L.swsft_inverse(None, 1, 1, x, x, x, 1 << 30, None) == S.E_INVALID
     assert L.spin_sph_conv_forward(None, 1, 1, 1, x, x, x, x, 1 << 30, None) == S.E_INVALID
+    assert L.spin_sph_conv_backward(None, 1, 1, 1, x, x, x, x, x, x, 1 << 30, None) == S.E_INVALID
     assert L.spin_sph_phase_collapse(None, 1, 1, x, x, x, x, x, None) == S.E_INVALID
     assert L.swsft_stage_timing(None, 1) == S.E_INVALID
     assert L.swsft_workspace_bytes(None, 0, 1, 1, 1) == 0
@@ -69,5 +70,5 @@ def test_status_strings_and_stage_names(L):
     for st in range(6):
         assert L.swsft_status_string(st).decode().startswith("SWSFT_")
     assert L.swsft_status_string(99).decode() == "unknown swsft status"
-    assert [L.swsft_stage_name(i).decode() for i in range(7)] == list(S.STAGES)
-    assert L.swsft_stage_name(7).decode() == ""
+    assert [L.swsft_stage_name(i).decode() for i in range(len(S.STAGES))] == list(S.STAGES)
+    assert L.swsft_stage_name(len(S.STAGES)).decode() == ""

@@ -1,0 +1,192 @@
+"""GPU parity of the layer's backward pass against the float64 oracle.
+
+spin_sph_conv_backward returns grad_x = F^H K^H G^H grad_y and
+grad_filters = filter_grad(G^H grad_y, F x) for a real loss with
+dL = Re sum conj(grad_y) dy.  The oracle's adjoints are pinned by adjoint
+identities and finite differences (tests/test_oracle_backward.py); here the
+HIP path is compared with them element by element on the same seeded inputs
+(rounded to the storage type first), to the forward tolerances: relative
+L2 <= 1e-5 for float32 storage, <= 2e-2 for bfloat16 storage.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2306_05420_amd import swsft as S
+from paper_2306_05420_amd import synthetic as syn
+from helpers import TOL, from_device, rel_l2, round_to, to_device, workload_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    S.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _grad_y(rng, B, spins_out, C_out, H, W, dtype):
+    """Output gradient: i.i.d. complex normal on the grid (not band-limited)."""
+    return round_to(syn.complex_normal(rng, (B, len(spins_out), C_out, H, W)), dtype)
+
+
+def _dead_spin_zeros(gK, L, spins_in, spins_out):
+    for l in range(L):
+        for ti, t in enumerate(spins_out):
+            for si, s in enumerate(spins_in):
+                if abs(t) > l or abs(s) > l:
+                    assert np.all(gK[l, ti, :, si, :] == 0), (l, t, s)
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "mol", "wx128"])
+def test_conv_backward_parity(name):
+    w = syn.workload(name)
+    x, K, _ = workload_inputs(w)
+    rng = np.random.default_rng(w.seed + 501)
+    gy = _grad_y(rng, w.B, w.spins_out, w.C_out, w.H, w.W, w.dtype)
+    plan = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_out, w.dtype)
+    gx_d, gk_d = plan.conv_backward(to_device(x, w.dtype), to_device(K, w.dtype),
+                                    to_device(gy, w.dtype))
+    gx, gk = from_device(gx_d), from_device(gk_d)
+    rx, rk = O.conv_backward(x, K, gy, w.L, w.spins_in, w.spins_out)
+    ex, ek = rel_l2(gx, rx), rel_l2(gk, rk)
+    print(f"{name} backward rel-L2: grad_x {ex:.3e}, grad_filters {ek:.3e}")
+    assert ex <= TOL[w.dtype] and ek <= TOL[w.dtype]
+    _dead_spin_zeros(gk, w.L, w.spins_in, w.spins_out)
+    plan.close()
+
+
+def test_backward_outputs_independent_and_deterministic():
+    """grad_x alone and grad_filters alone equal the joint call bit for bit;
+    repeated calls are bit-identical."""
+    w = syn.workload("small")
+    x, K, _ = workload_inputs(w)
+    rng = np.random.default_rng(7)
+    gy = _grad_y(rng, w.B, w.spins_out, w.C_out, w.H, w.W, w.dtype)
+    plan = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_out, w.dtype)
+    xd, Kd, gd = to_device(x, w.dtype), to_device(K, w.dtype), to_device(gy, w.dtype)
+    gx, gk = plan.conv_backward(xd, Kd, gd)
+    gx, gk = gx.clone(), gk.clone()
+    gx_only, none_k = plan.conv_backward(xd, Kd, gd, need_filters=False)
+    none_x, gk_only = plan.conv_backward(xd, Kd, gd, need_x=False)
+    assert none_k is None and none_x is None
+    assert torch.equal(gx, gx_only) and torch.equal(gk, gk_only)
+    gx2, gk2 = plan.conv_backward(xd, Kd, gd)
+    assert torch.equal(gx, gx2) and torch.equal(gk, gk2)
+    plan.close()
+
+
+BACKWARD_EDGE = [
+    # H, L, spins_in, spins_out, B, C_in, C_out, dtype
+    (16, 5, (0,), (0,), 1, 1, 1, "f32"),               # one channel, L < H/2
+    (16, 8, (-1, 2, 0), (1, 0, -2), 3, 3, 5, "f32"),   # odd channel counts: scalar loads
+    (2, 1, (0,), (0,), 2, 2, 3, "f32"),                # smallest grid, l = 0 only
+    (64, 32, (1,), (0, -1), 1, 33, 17, "f32"),         # ragged tiles, spin 1 absent at l = 0
+    (8, 4, (0,), (0, 1), 5, 7, 9, "bf16"),
+    (32, 16, (0, 1), (0, 1), 2, 40, 24, "bf16"),        # several column tiles of the gradient
+    (32, 16, (0, 1), (0, 1, -1), 3, 32, 44, "bf16"),    # adjoint mixing with 2 C_out % 32 == 0
+    (16, 8, (-2, 0), (0, 1), 3, 64, 8, "bf16"),         # |s| = 2: gradient zero below l = 2
+    (64, 32, (1, -2), (2, 0), 2, 64, 64, "bf16"),       # latitude GEMMs on the direct-to-LDS path
+    (64, 32, (0,), (0, 1), 2, 20, 64, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", BACKWARD_EDGE,
+                         ids=[f"H{c[0]}L{c[1]}S{len(c[2])}{len(c[3])}C{c[5]}x{c[6]}{c[7]}"
+                              for c in BACKWARD_EDGE])
+def test_backward_edge_cases(case):
+    H, L, si, so, B, Ci, Co, dt = case
+    rng = np.random.default_rng(H * 7919 + L * 31 + Ci)
+    a = syn.random_coefficients(rng, L, B, si, Ci, 0.5)
+    x = round_to(O.inverse(a, H, H, si), dt)
+    K = round_to(syn.random_filters(rng, L, si, Ci, so, Co, 1.0 / Ci), dt)
+    gy = _grad_y(rng, B, so, Co, H, H, dt)
+    plan = S.Plan(H, H, L, si, so, dt)
+    gx_d, gk_d = plan.conv_backward(to_device(x, dt), to_device(K, dt), to_device(gy, dt))
+    gx, gk = from_device(gx_d), from_device(gk_d)
+    rx, rk = O.conv_backward(x, K, gy, L, si, so)
+    ex, ek = rel_l2(gx, rx), rel_l2(gk, rk)
+    print(f"backward edge {case}: grad_x {ex:.2e} grad_filters {ek:.2e}")
+    assert ex <= TOL[dt] and ek <= TOL[dt]
+    _dead_spin_zeros(gk, L, si, so)
+    plan.close()
+
+
+def test_backward_tables_match_forward_tables():
+    """Tables 2 and 3 hold the values of tables 0 and 1 in each other's layout."""
+    for dt in ("f32", "bf16"):
+        plan = S.Plan(32, 32, 16, (0, 1, -2), (1, 0), dt)
+        H, L = plan.H, plan.L
+        for si in range(3):
+            t0 = plan.table(0, si)[:, :, :H]            # [M, L, H]
+            t2 = plan.table(2, si)[:, :H, :L]           # [M, H, L]
+            assert torch.equal(t0, t2.transpose(1, 2))
+        for so in range(2):
+            t1 = plan.table(1, so)[:, :H, :L]
+            t3 = plan.table(3, so)[:, :, :H]
+            assert torch.equal(t1, t3.transpose(1, 2))
+        plan.close()
+
+
+def test_backward_call_validation():
+    w = syn.workload("tiny")
+    plan = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_out, w.dtype)
+    L = S.lib()
+    x = plan.empty(1, 1, 4, 16, 16)
+    y = plan.empty(1, 2, 4, 16, 16)
+    K = plan.empty(8, 2, 4, 1, 4)
+    gx = plan.empty(1, 1, 4, 16, 16)
+    gk = plan.empty(8, 2, 4, 1, 4)
+    p = lambda t: torch.view_as_real(t).data_ptr()
+    need = plan.workspace_bytes(S.OP_CONV_BACKWARD, 1, 4, 4)
+    assert need > plan.workspace_bytes(S.OP_CONV, 1, 4, 4)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    call = lambda *a: L.spin_sph_conv_backward(plan._h, 1, 4, 4, *a, ws.data_ptr(), need, None)
+    assert call(p(x), p(K), p(y), None, None) == S.E_INVALID            # nothing requested
+    assert call(p(x), p(K), None, p(gx), p(gk)) == S.E_INVALID         # no grad_y
+    assert call(None, p(K), p(y), None, p(gk)) == S.E_INVALID          # grad_filters needs x
+    assert call(p(x), None, p(y), p(gx), None) == S.E_INVALID          # grad_x needs filters
+    assert call(p(x), p(K), p(y), p(y), None) == S.E_INVALID           # grad_x overlaps grad_y
+    assert call(p(x), p(K), p(y), p(gx), p(K)) == S.E_INVALID          # grad_filters overlaps filters
+    assert call(p(x), p(K), p(y), None, p(x)) == S.E_INVALID           # grad_filters overlaps x
+    assert call(p(x), p(K), p(y), p(gx), p(gx)) == S.E_INVALID         # the outputs overlap
+    assert L.spin_sph_conv_backward(plan._h, 1, 4, 4, p(x), p(K), p(y), p(gx), p(gk),
+                                    ws.data_ptr(), need - 1, None) == S.E_WORKSPACE
+    assert call(None, p(K), p(y), p(gx), None) == S.OK                  # x unused for grad_x only
+    assert call(p(x), None, p(y), None, p(gk)) == S.OK                  # filters unused
+    torch.cuda.synchronize()
+    plan.close()
+
+
+# ---------------------------------------------------------------------------
+# The 256 x 256, C = 256, bfloat16 workload at its full size.  The oracle
+# computes sampled channels: grad_x of batch item 0 for a few input channels
+# (needs G^H grad_y of all of item 0's output maps) and the filter gradient
+# for a few output channels (needs F x of every input map).
+# ---------------------------------------------------------------------------
+
+def test_wx256_backward_sampled():
+    w = syn.workload("wx256")
+    x, K, _ = workload_inputs(w)
+    rng = np.random.default_rng(w.seed + 501)
+    gy = _grad_y(rng, w.B, w.spins_out, w.C_out, w.H, w.W, "bf16")
+    plan = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_out, "bf16")
+    gx_d, gk_d = plan.conv_backward(to_device(x, "bf16"), to_device(K, "bf16"),
+                                    to_device(gy, "bf16"))
+    cs = [0, 1, 77, 200, 255]
+    gx = from_device(gx_d[:1, :, cs])
+    gk = from_device(gk_d[:, :, cs])
+    plan.close()
+    g0 = O.inverse_adjoint(gy[:1], w.L, w.spins_out)
+    rx = O.forward_adjoint(O.mix_adjoint(g0, K[..., cs], w.spins_in, w.spins_out),
+                           w.H, w.W, w.spins_in)
+    g_cs = O.inverse_adjoint(np.ascontiguousarray(gy[:, :, cs]), w.L, w.spins_out)
+    a = O.forward(x, w.L, w.spins_in)
+    rk = O.filter_grad(g_cs, a, w.spins_in, w.spins_out)
+    ex, ek = rel_l2(gx, rx), rel_l2(gk, rk)
+    print(f"wx256 backward (sampled channels) rel-L2: grad_x {ex:.3e}, grad_filters {ek:.3e}")
+    assert ex <= TOL["bf16"] and ek <= TOL["bf16"]
