@@ -268,6 +268,7 @@ def main(argv=None):
         "roofline": r["roofline"],
         "transforms": r["transforms"],
         "backward": r["backward"],
+        "graph": r["graph"],
     }
     if "stack2" in r:
         out["stack2"] = r["stack2"]
@@ -295,6 +296,24 @@ def _time_calls(fn, steps: int, warmup: int):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     return max(wall, start.elapsed_time(stop) / 1e3) / steps
+
+
+def _time_graph(fn, steps: int, warmup: int):
+    """Seconds per replay of a HIP graph holding one call of fn."""
+    import torch
+
+    fn()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        fn()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    t = _time_calls(g.replay, steps, warmup)
+    del g
+    return t
 
 
 def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = False) -> dict:
@@ -396,6 +415,17 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
          "tflops": useful / t_layer / 1e12, "useful": useful, "stages": stages,
          "roofline": roof, "transforms": transforms,
          "backward": measure_backward(plan, w, x, K, y, steps, warmup)}
+    # launch overhead removed: one layer call (and one backward call) per
+    # replay of a captured graph
+    gx = plan.empty(w.B, len(w.spins_in), w.C_in, w.H, w.W)
+    gk = plan.empty(w.L, len(w.spins_out), w.C_out, len(w.spins_in), w.C_in)
+    y_g = plan.empty(w.B, len(w.spins_out), w.C_out, w.H, w.W)
+    t_gl = _time_graph(lambda: plan.conv(x, K, y_g), steps, warmup)
+    t_gb = _time_graph(lambda: plan.conv_backward(x, K, y, grad_x=gx, grad_filters=gk),
+                       steps, warmup)
+    r["graph"] = {"layer_us": round(t_gl * 1e6, 2), "layer_per_s": round(1.0 / t_gl, 1),
+                  "backward_us": round(t_gb * 1e6, 2)}
+    del gx, gk, y_g
 
     if name == "mol":
         # two stacked layers with the phase collapse between them
@@ -473,6 +503,10 @@ def table_rows(cfg: int, r: dict):
         t = r["transforms"][op]
         rows.append(f"| {cfg} {w.name} | swsft_{op} | {t['us']:.1f} | {t['per_s']:.0f} | "
                     f"{t['TFLOP/s']:.1f} | {100 * t['TFLOP/s'] / peak:.1f} | {t['GB/s']:.0f} (whole transform) | — |")
+    t = r["graph"]
+    rows.append(f"| {cfg} {w.name} | layer, HIP graph replay | {t['layer_us']:.1f} | "
+                f"{t['layer_per_s']:.0f} | {r['useful'] / t['layer_us'] / 1e6:.1f} | "
+                f"{100 * r['useful'] / t['layer_us'] / 1e6 / peak:.1f} | — | — |")
     t = r["backward"]
     rows.append(f"| {cfg} {w.name} | layer backward (grad_x, grad_filters) | {t['us']:.1f} | "
                 f"{t['per_s']:.0f} | {t['TFLOP/s']:.1f} | {100 * t['TFLOP/s'] / peak:.1f} | — | — |")

@@ -359,11 +359,8 @@ hipError_t filter_grad_t(const Plan& p, int B, int Cin, int Cout, const void* a,
   const long long blocks = (long long)p.L * tiles_r * tiles_c;
   const bool vec = Nc % 4 == 0 && Kc % 4 == 0;
   auto kern = vec ? filter_grad_kernel<T, true> : filter_grad_kernel<T, false>;
-  if (G::SMEM > 64 * 1024) {
-    const hipError_t e =
-        hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, G::SMEM);
-    if (e != hipSuccess) return e;
-  }
+  const hipError_t e = ensure_dynamic_lds((const void*)kern, G::SMEM);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(GNT), G::SMEM, st, (const T*)a,
                      (const T*)g, (T*)gK, p.L, B, Cin, Cout, p.n_in, p.n_out,
                      to_spins(p.spins_in, p.n_in), to_spins(p.spins_out, p.n_out), tiles_r, tiles_c);

@@ -366,8 +366,7 @@ __global__ void __launch_bounds__((DftGeom<W1, W2>::NT))
 
 template <class Kern>
 hipError_t allow_lds(Kern kern, size_t lds) {
-  if (lds <= 64 * 1024) return hipSuccess;
-  return hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  return ensure_dynamic_lds((const void*)kern, lds);
 }
 
 template <typename Tin, typename Tout, int W1, int W2>

@@ -192,11 +192,8 @@ hipError_t launch_t(const Plan& p, int B, int C, const void* x, const float2* W1
   if (C % 16 == 0) {
     const size_t lds = (size_t)(2 * C + p.n_out * C) * PM * sizeof(float);
     auto kern = phase_collapse_mfma_kernel<T>;
-    if (lds > 64 * 1024) {
-      const hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-      if (e != hipSuccess) return e;
-    }
+    const hipError_t e = ensure_dynamic_lds((const void*)kern, lds);
+    if (e != hipSuccess) return e;
     dim3 grid((HW + PM - 1) / PM, B);
     hipLaunchKernelGGL(kern, grid, dim3(NTP), lds, st, (const T*)x, (const float*)W1,
                        (const float*)W2, bias, (T*)y, p.n_out, C, HW, s0, x != y ? 1 : 0);
@@ -204,11 +201,8 @@ hipError_t launch_t(const Plan& p, int B, int C, const void* x, const float2* W1
   }
   const size_t lds = (size_t)C * PB * sizeof(float2) + (size_t)p.n_out * C * PB * sizeof(float);
   auto kern = phase_collapse_kernel<T>;
-  if (lds > 64 * 1024) {
-    const hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-  }
+  const hipError_t e = ensure_dynamic_lds((const void*)kern, lds);
+  if (e != hipSuccess) return e;
   dim3 grid((HW + PB - 1) / PB, B);
   hipLaunchKernelGGL(kern, grid, dim3(NTP), lds, st, (const T*)x, W1, W2, bias, (T*)y, p.n_out, C,
                      HW, s0, x != y ? 1 : 0);

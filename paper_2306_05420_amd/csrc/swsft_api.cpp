@@ -6,7 +6,10 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <map>
+#include <mutex>
 #include <new>
+#include <utility>
 
 #include "swsft_internal.h"
 
@@ -105,6 +108,27 @@ swsft_status check_ptr(const void* ptr, const char* name) {
     return fail(SWSFT_E_INVALID, "%s must be 16-byte aligned", name);
   return SWSFT_OK;
 }
+
+}  // namespace
+
+namespace swsft {
+hipError_t ensure_dynamic_lds(const void* kern, size_t bytes) {
+  if (bytes <= 64 * 1024) return hipSuccess;
+  static std::mutex mu;
+  static std::map<std::pair<int, const void*>, size_t> done;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  size_t& have = done[{dev, kern}];
+  if (have >= bytes) return hipSuccess;
+  e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (e == hipSuccess) have = bytes;
+  return e;
+}
+}  // namespace swsft
+
+namespace {
 
 swsft_status check_device(const Plan& p) {
   int dev = -1;

@@ -69,6 +69,12 @@ inline size_t coef_elems(const Plan& p, int S, int B, int C) {
   return (size_t)p.L * p.L * (size_t)B * S * C * 2;
 }
 
+// Raise a kernel's dynamic LDS limit to `bytes` (no-op up to 64 KiB).  The
+// attribute is set once per (device, kernel) and size: later launches make no
+// runtime call, so a launch sequence can be captured in a graph once it has
+// run eagerly.
+hipError_t ensure_dynamic_lds(const void* kern, size_t bytes);
+
 // ---- kernel launchers (return hipGetLastError() of the launch) ----
 hipError_t launch_tables(const Plan& p, hipStream_t st);
 
