@@ -15,6 +15,10 @@ ICML 2023):
   across the order m ("Spherical CNNs" paragraph: spin-weighted convolutions
   are products of spin-weighted harmonic coefficients; Fig. 2's "*K");
 * the phase-collapse nonlinearity (Method, "Phase collapse nonlinearity");
+* the backward pass of the layer (adjoints of the linear maps above);
+* spectral batch normalization, spectral pooling and the residual block with
+  its skip connection between Fourier coefficients (Method, "Spectral batch
+  normalization", "Spectral pooling and efficient residual block", Fig. 2);
 * the Funk--Hecke projection of isotropic bumps used to synthesise the
   molecule-shaped inputs.
 
@@ -58,6 +62,8 @@ __all__ = [
     "filter_grad",
     "conv_backward",
     "phase_collapse",
+    "spectral_batch_norm",
+    "residual_block",
     "bump_coefficients",
 ]
 
@@ -512,6 +518,68 @@ def phase_collapse(x: np.ndarray, spins, W1: np.ndarray, W2: np.ndarray,
                 + np.einsum("oc,bchw->bohw", W2, mag)
                 + bias[None, :, None, None])
     return y
+
+
+# --------------------------------------------------------------------------
+# Spectral batch normalization and the residual block (Method, "Spectral
+# batch normalization", "Spectral pooling and efficient residual block")
+# --------------------------------------------------------------------------
+
+def spectral_batch_norm(coef: np.ndarray, spins, gamma: np.ndarray, beta=None,
+                        eps: float = 1e-5, var=None, skip=None):
+    """Batch normalization computed on the coefficients.
+
+    The l = 0 coefficient is the function's mean (times sqrt(4 pi)) and, by
+    Parseval, (1/4pi) sum_{l>=1, m} |a_lm|^2 is the variance of the function
+    over the sphere.  Per (spin s, channel c), with batch statistics
+        var[s, c] = (1 / (4 pi B)) sum_b sum_{l >= 1} sum_m |a_lm[b, s, c]|^2
+    (or the given `var`, e.g. running statistics at inference):
+        out_lm = gamma[s, c] a_lm / sqrt(var[s, c] + eps)   for l >= 1,
+        out_00 = beta[c] for spin 0 (0 without beta): the mean is removed by
+                 zeroing the l = 0 coefficient and the bias sets it,
+    then `skip` (same shape as coef) is added if given.
+    coef [L^2, B, S, C] complex; gamma [S, C] real; beta [C] complex.
+    Returns (out, var).
+    Pinned by: the spatial mean and variance of the synthesised output,
+    integrated by Gauss--Legendre quadrature independently of the transform
+    (tests/test_oracle_block.py).
+    """
+    a = np.asarray(coef, dtype=np.complex128)
+    L2, B, S, C = a.shape
+    spins = list(spins)
+    if var is None:
+        var = np.sum(np.abs(a[1:]) ** 2, axis=(0, 1)) / (4.0 * np.pi * B)   # [S, C]
+    var = np.asarray(var, dtype=np.float64)
+    scale = np.asarray(gamma, dtype=np.float64) / np.sqrt(var + eps)
+    out = a * scale[None, None]
+    out[0] = 0.0
+    if beta is not None and 0 in spins:
+        out[0, :, spins.index(0), :] = np.asarray(beta, dtype=np.complex128)[None, :]
+    if skip is not None:
+        out = out + np.asarray(skip, dtype=np.complex128)
+    return out, var
+
+
+def residual_block(x: np.ndarray, L: int, H_out: int, spins, K1, K2, bn1, bn2, pc1, pc2,
+                   eps: float = 1e-5) -> np.ndarray:
+    """The residual block of Fig. 2 with the skip connection in Fourier space:
+        a = FT(x)                          (bandlimit L: spectral pooling when L < H_in/2)
+        z = sigma1(IFT(BN1(K1 * a)))       on the H_out x H_out grid
+        y = sigma2(IFT(BN2(K2 * FT(z)) + a))
+    FT / IFT are `forward` / `inverse`, K * the per-degree mixing `mix`,
+    BN the spectral batch norm with batch statistics, sigma the phase collapse.
+    x [B, S, C, H_in, W_in]; K1, K2 [L, S, C, S, C]; bn = (gamma, beta);
+    pc = (W1, W2, bias).  Returns [B, S, C, H_out, H_out].
+    Pinned by: K2 = 0 reductions to the phase collapse of the input (same grid)
+    and of the input evaluated on the coarse grid (pooling), and exact
+    longitude-shift equivariance (tests/test_oracle_block.py).
+    """
+    a = forward(x, L, spins)
+    h = spectral_batch_norm(mix(a, K1, spins, spins), spins, *bn1, eps=eps)[0]
+    z = phase_collapse(inverse(h, H_out, H_out, spins), spins, *pc1)
+    b = forward(z, L, spins)
+    c = spectral_batch_norm(mix(b, K2, spins, spins), spins, *bn2, eps=eps, skip=a)[0]
+    return phase_collapse(inverse(c, H_out, H_out, spins), spins, *pc2)
 
 
 # --------------------------------------------------------------------------
