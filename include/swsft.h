@@ -77,7 +77,8 @@ typedef enum {
   SWSFT_OP_FORWARD = 0, /* swsft_forward          */
   SWSFT_OP_INVERSE = 1, /* swsft_inverse          */
   SWSFT_OP_CONV = 2,    /* spin_sph_conv_forward  */
-  SWSFT_OP_CONV_BACKWARD = 3 /* spin_sph_conv_backward */
+  SWSFT_OP_CONV_BACKWARD = 3, /* spin_sph_conv_backward */
+  SWSFT_OP_BATCH_NORM = 4     /* spin_sph_spectral_batch_norm (C_out = C, C_in ignored) */
 } swsft_op;
 
 /*
@@ -190,6 +191,96 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
 swsft_status spin_sph_phase_collapse(swsft_plan p, int B, int C, const void* x,
                                      const void* W1, const void* W2, const void* bias,
                                      void* y, void* stream);
+
+/*
+ * The per-degree mixing alone (Background, "Spherical CNNs": convolution as
+ * products of coefficients, filters shared across m; Fig. 2 "*K"):
+ *   coef_out[l*l+l+m][b][t][c'] = sum_{s, |s| <= l} sum_c K[l][t][c'][s][c] coef[l*l+l+m][b][s][c]
+ * for |t| <= l, else 0.
+ *  coef      [L*L][B][S_in][C_in] complex, read only.
+ *  filters   [L][S_out][C_out][S_in][C_in] complex, read only.
+ *  coef_out  [L*L][B][S_out][C_out] complex, written; must not overlap the inputs.
+ * Needs no workspace.
+ */
+swsft_status spin_sph_mix(swsft_plan p, int B, int C_in, int C_out, const void* coef,
+                          const void* filters, void* coef_out, void* stream);
+
+/*
+ * Spectral batch normalization (Method, "Spectral batch normalization") of
+ * coefficients of the plan's output spins.  The l = 0 coefficient is the
+ * function's mean times sqrt(4 pi), and by Parseval the remaining ones carry
+ * its variance over the sphere, so per (spin s, channel c):
+ *   var[s][c] = (1 / (4 pi B)) sum_b sum_{l >= 1} sum_m |coef|^2    (batch statistics)
+ *   out = gamma[s][c] coef / sqrt(var[s][c] + eps)                   for l >= 1
+ *   out[0][b][s0][c] = beta[c] (spin 0), 0 for the other spins       for l = 0
+ *   out += skip                                                      (if skip != NULL)
+ *  coef     [L*L][B][S_out][C] complex (storage type).
+ *  gamma    [S_out][C] float, device.  beta: [C] complex float, device, or NULL (0).
+ *  eps      >= 0, added under the square root.
+ *  var_in   [S_out][C] float (device) to normalise with given statistics (e.g.
+ *           running averages at inference), or NULL for batch statistics.
+ *  var_out  [S_out][C] float (device) receiving the variance used, or NULL.
+ *  skip     [L*L][B][S_out][C] complex added after normalising (the Fourier-
+ *           space residual connection of Fig. 2), or NULL.
+ *  out      [L*L][B][S_out][C] complex; out == coef and out == skip are allowed.
+ *  ws       >= swsft_workspace_bytes(p, SWSFT_OP_BATCH_NORM, B, 1, C) bytes.
+ * The statistics are summed in float32 in a fixed order (deterministic).
+ */
+swsft_status spin_sph_spectral_batch_norm(swsft_plan p, int B, int C, const void* coef,
+                                          const float* gamma, const void* beta, float eps,
+                                          const float* var_in, float* var_out, const void* skip,
+                                          void* out, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Parameters of the residual block; every pointer is device memory.
+ *  K1, K2          [L][S][C][S][C] complex filters in the plans' storage type.
+ *  gamma1, gamma2  [S][C] float; beta1, beta2 [C] complex float or NULL.
+ *  pc*_W1 [C][C], pc*_W2 [C][S*C], pc*_b [C]: complex float phase-collapse parameters.
+ *  eps             batch-norm epsilon (>= 0).
+ *  var1_out, var2_out  [S][C] float receiving the batch variances, or NULL.
+ */
+typedef struct swsft_block_params {
+  const void* K1;
+  const void* K2;
+  const float* gamma1;
+  const void* beta1;
+  const float* gamma2;
+  const void* beta2;
+  const void* pc1_W1;
+  const void* pc1_W2;
+  const void* pc1_b;
+  const void* pc2_W1;
+  const void* pc2_W2;
+  const void* pc2_b;
+  float eps;
+  float* var1_out;
+  float* var2_out;
+} swsft_block_params;
+
+/* Workspace bytes of spin_sph_residual_block_forward (0 for invalid arguments). */
+size_t swsft_block_workspace_bytes(swsft_plan p_in, swsft_plan p_out, int B, int C);
+
+/*
+ * The residual block of Fig. 2 (Method, "Spectral pooling and efficient
+ * residual block"), with the skip connection between Fourier coefficients:
+ *   a = FT(x)                                   with p_in (grid H_in, bandlimit L)
+ *   z = PC1(IFT(BN1(K1 * a)))                   with p_out (grid H_out)
+ *   y = PC2(IFT(BN2(K2 * FT(z)) + a))
+ * FT / IFT are swsft_forward / swsft_inverse, K * the per-degree mixing, BN
+ * the spectral batch norm with batch statistics, PC the phase collapse.
+ * Spectral pooling: L < H_in / 2 skips the coefficients of degree >= L in
+ * the first transform, and H_out = 2 L puts the output on the coarser grid;
+ * H_out = H_in is the block without pooling.
+ *  p_in, p_out  plans with the same device, dtype, bandlimit L, and the same
+ *               spin list S (containing 0) as both spins_in and spins_out.
+ *  x   [B][S][C][H_in][W_in] complex, read only.
+ *  y   [B][S][C][H_out][W_out] complex, written; must not overlap x.
+ *  ws  >= swsft_block_workspace_bytes(p_in, p_out, B, C) bytes.
+ * Stage timing, if enabled, is recorded on p_out.
+ */
+swsft_status spin_sph_residual_block_forward(swsft_plan p_in, swsft_plan p_out, int B, int C,
+                                             const void* x, const swsft_block_params* params,
+                                             void* y, void* ws, size_t ws_bytes, void* stream);
 
 /* Static text for a status code. */
 const char* swsft_status_string(int status);

@@ -1,0 +1,165 @@
+// Spectral batch normalization (Method, "Spectral batch normalization") on
+// coefficients [L^2][B][S][C] (row l^2 + l + m, then batch, spin, channel).
+//
+// The l = 0 coefficient is the function's mean (times sqrt(4 pi)); by
+// Parseval the other coefficients carry its variance.  Per (spin, channel):
+//   var   = (1 / (4 pi B)) sum_{b, l >= 1, m} |a|^2    (batch statistics), or given,
+//   out   = gamma a / sqrt(var + eps)                    for l >= 1,
+//   out_0 = beta (spin 0; 0 for other spins)             for l = 0,
+//   out  += skip                                         (optional).
+//
+// Three launches, all deterministic (no atomics):
+//   bn_partial   each workgroup sums |a|^2 over a fixed range of rows for
+//                every column (threads across columns: coalesced rows);
+//   bn_finalize  per column: the partial sums in workgroup order -> var, scale;
+//   bn_apply     elementwise, 4 complex values per thread.
+#include "swsft_internal.h"
+
+namespace swsft {
+namespace {
+
+constexpr int kNT = 256;
+constexpr float kInv4Pi = 0.0795774715459476679f;  // 1 / (4 pi)
+
+template <typename T>
+__device__ __forceinline__ float2 ld_c(const T* p, size_t i) {
+  return make_float2((float)p[2 * i], (float)p[2 * i + 1]);
+}
+
+template <typename T>
+__global__ void __launch_bounds__(kNT) bn_partial_kernel(const T* __restrict__ a,
+                                                         float* __restrict__ partial, int rows,
+                                                         int row_begin, int rows_per_blk, int ncol) {
+  const int r0 = row_begin + blockIdx.x * rows_per_blk;
+  const int r1 = min(r0 + rows_per_blk, rows);
+  for (int col = threadIdx.x; col < ncol; col += kNT) {
+    float acc = 0.f;
+    for (int r = r0; r < r1; ++r) {
+      const float2 v = ld_c(a, (size_t)r * ncol + col);
+      acc += v.x * v.x + v.y * v.y;
+    }
+    partial[(size_t)blockIdx.x * ncol + col] = acc;
+  }
+}
+
+__global__ void __launch_bounds__(kNT) bn_finalize_kernel(const float* __restrict__ partial,
+                                                          int nblk, int ncol, float inv_norm,
+                                                          const float* __restrict__ var_in,
+                                                          const float* __restrict__ gamma,
+                                                          float eps, float* __restrict__ scale,
+                                                          float* __restrict__ var_out) {
+  const int col = blockIdx.x * kNT + threadIdx.x;
+  if (col >= ncol) return;
+  float var;
+  if (var_in != nullptr) {
+    var = var_in[col];
+  } else {
+    float acc = 0.f;
+    for (int b = 0; b < nblk; ++b) acc += partial[(size_t)b * ncol + col];
+    var = acc * inv_norm;
+  }
+  scale[col] = gamma[col] / sqrtf(var + eps);
+  if (var_out != nullptr) var_out[col] = var;
+}
+
+// rows [0, B) are degree 0; columns are (spin, channel), s0 the spin-0 slot or -1
+template <typename T>
+__global__ void __launch_bounds__(kNT) bn_apply_kernel(const T* a,  // may be out (in place)
+                                                       const float* __restrict__ scale,
+                                                       const float2* __restrict__ beta,
+                                                       const T* skip, T* out,
+                                                       long long n_cplx, int ncol, int C, int B,
+                                                       int s0) {
+  const long long i0 = ((long long)blockIdx.x * kNT + threadIdx.x) * 4;
+  if (i0 >= n_cplx) return;
+  float2 v[4];
+  const int n = n_cplx - i0 < 4 ? (int)(n_cplx - i0) : 4;
+  if (n == 4) {  // 4 whole complex values: a 16-byte (bf16) or 2 x 16-byte (f32) load
+    if constexpr (sizeof(T) == 4) {
+      const float4 u = *reinterpret_cast<const float4*>(a + 2 * i0);
+      const float4 w = *reinterpret_cast<const float4*>(a + 2 * i0 + 4);
+      v[0] = make_float2(u.x, u.y); v[1] = make_float2(u.z, u.w);
+      v[2] = make_float2(w.x, w.y); v[3] = make_float2(w.z, w.w);
+    } else {
+      typedef __bf16 v8b __attribute__((ext_vector_type(8)));
+      const v8b u = *reinterpret_cast<const v8b*>(a + 2 * i0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = make_float2((float)u[2 * e], (float)u[2 * e + 1]);
+    }
+  } else {
+    for (int e = 0; e < n; ++e) v[e] = ld_c(a, i0 + e);
+  }
+  float2 o[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if (e >= n) break;
+    const long long i = i0 + e;
+    const int col = (int)(i % ncol);
+    const long long row = i / ncol;
+    if (row < B) {  // degree 0: the bias for spin 0, else 0
+      o[e] = (col / C == s0 && beta != nullptr) ? beta[col % C] : make_float2(0.f, 0.f);
+    } else {
+      const float sc = scale[col];
+      o[e] = make_float2(v[e].x * sc, v[e].y * sc);
+    }
+    if (skip != nullptr) {
+      const float2 k = ld_c(skip, i);
+      o[e].x += k.x;
+      o[e].y += k.y;
+    }
+  }
+  for (int e = 0; e < n; ++e) {
+    out[2 * (i0 + e)] = (T)o[e].x;
+    out[2 * (i0 + e) + 1] = (T)o[e].y;
+  }
+}
+
+}  // namespace
+
+int bn_partial_blocks(const Plan& p, int B) {
+  const int rows = p.L * p.L * B - B;  // rows of degrees l >= 1
+  int nblk = (rows + 63) / 64;         // at least 64 rows per workgroup
+  return nblk < 1 ? 1 : (nblk > 512 ? 512 : nblk);
+}
+
+size_t bn_workspace_bytes(const Plan& p, int B, int C) {
+  const int ncol = p.n_out * C;
+  return ((size_t)bn_partial_blocks(p, B) * ncol + ncol) * sizeof(float);
+}
+
+template <typename T>
+hipError_t bn_t(const Plan& p, int B, int C, const void* a, const float* gamma,
+                const float2* beta, float eps, const float* var_in, float* var_out,
+                const void* skip, void* out, float* ws, hipStream_t st) {
+  const int ncol = p.n_out * C;
+  const int rows = p.L * p.L * B;
+  const int nblk = bn_partial_blocks(p, B);
+  float* partial = ws;
+  float* scale = ws + (size_t)nblk * ncol;
+  if (var_in == nullptr) {
+    const int body = rows - B;
+    const int per = (body + nblk - 1) / nblk;
+    hipLaunchKernelGGL(bn_partial_kernel<T>, dim3(nblk), dim3(kNT), 0, st, (const T*)a, partial,
+                       rows, B, per, ncol);
+  }
+  hipLaunchKernelGGL(bn_finalize_kernel, dim3((ncol + kNT - 1) / kNT), dim3(kNT), 0, st, partial,
+                     nblk, ncol, kInv4Pi / (float)B, var_in, gamma, eps, scale, var_out);
+  int s0 = -1;
+  for (int i = 0; i < p.n_out; ++i)
+    if (p.spins_out[i] == 0) s0 = i;
+  const long long n = (long long)rows * ncol;
+  const long long grid = (n + 4LL * kNT - 1) / (4LL * kNT);
+  hipLaunchKernelGGL(bn_apply_kernel<T>, dim3((unsigned)grid), dim3(kNT), 0, st, (const T*)a, scale,
+                     beta, (const T*)skip, (T*)out, n, ncol, C, B, s0);
+  return hipGetLastError();
+}
+
+hipError_t launch_batch_norm(const Plan& p, int B, int C, const void* a, const float* gamma,
+                             const float2* beta, float eps, const float* var_in, float* var_out,
+                             const void* skip, void* out, void* ws, hipStream_t st) {
+  if (p.dtype == SWSFT_BF16)
+    return bn_t<__bf16>(p, B, C, a, gamma, beta, eps, var_in, var_out, skip, out, (float*)ws, st);
+  return bn_t<float>(p, B, C, a, gamma, beta, eps, var_in, var_out, skip, out, (float*)ws, st);
+}
+
+}  // namespace swsft

@@ -2,6 +2,7 @@
 // sequence of kernel launches of each call.  Every call checks its
 // arguments on the host before it touches HIP; on an error nothing is
 // enqueued.
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -61,6 +62,11 @@ swsft_status check_bc(int B, int C, const char* cname) {
   return SWSFT_OK;
 }
 
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const char *pa = static_cast<const char*>(a), *pb = static_cast<const char*>(b);
+  return pa != nullptr && pb != nullptr && pa < pb + nb && pb < pa + na;
+}
+
 size_t filter_elems(const Plan& p, int Cin, int Cout) {
   return (size_t)p.L * p.n_out * Cout * p.n_in * Cin * 2;
 }
@@ -85,6 +91,8 @@ size_t ws_need(const Plan& p, int op, int B, int Cin, int Cout) {
              align_up(swsft::coef_elems(p, p.n_out, B, Cout) * e) +
              align_up(filter_elems(p, Cin, Cout) * e);
     }
+    case SWSFT_OP_BATCH_NORM:
+      return align_up(swsft::bn_workspace_bytes(p, B, Cout));
     default:
       return 0;
   }
@@ -200,7 +208,7 @@ const char* swsft_last_error(void) { return g_last_error; }
 const char* swsft_stage_name(int stage) {
   static const char* names[swsft::kNumStages] = {"dft_fwd", "lat_fwd", "mix", "lat_inv",
                                                  "dft_inv", "phase_collapse", "tables",
-                                                 "filter_grad", "filter_adjoint"};
+                                                 "filter_grad", "filter_adjoint", "batch_norm"};
   if (stage < 0 || stage >= swsft::kNumStages) return "";
   return names[stage];
 }
@@ -465,6 +473,181 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
     }));
   }
   return SWSFT_OK;
+}
+
+swsft_status spin_sph_mix(swsft_plan p, int B, int C_in, int C_out, const void* coef,
+                          const void* filters, void* coef_out, void* stream) {
+  g_last_error[0] = 0;
+  if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
+  SWSFT_TRY(check_bc(B, C_in, "C_in"));
+  SWSFT_TRY(check_bc(B, C_out, "C_out"));
+  SWSFT_TRY(check_ptr(coef, "coef"));
+  SWSFT_TRY(check_ptr(filters, "filters"));
+  SWSFT_TRY(check_ptr(coef_out, "coef_out"));
+  {
+    const size_t as = swsft::coef_elems(*p, p->n_in, B, C_in) * p->elem;
+    const size_t ks = filter_elems(*p, C_in, C_out) * p->elem;
+    const size_t os = swsft::coef_elems(*p, p->n_out, B, C_out) * p->elem;
+    if (overlaps(coef_out, os, coef, as) || overlaps(coef_out, os, filters, ks))
+      return fail(SWSFT_E_INVALID, "coef_out overlaps an input");
+  }
+  SWSFT_TRY(check_device(*p));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return run_stage(*p, swsft::kStageMix, st, "mix", [&] {
+    return swsft::launch_mix(*p, B, C_in, C_out, coef, filters, coef_out, st);
+  });
+}
+
+swsft_status spin_sph_spectral_batch_norm(swsft_plan p, int B, int C, const void* coef,
+                                          const float* gamma, const void* beta, float eps,
+                                          const float* var_in, float* var_out, const void* skip,
+                                          void* out, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error[0] = 0;
+  if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
+  SWSFT_TRY(check_bc(B, C, "C"));
+  SWSFT_TRY(check_ptr(coef, "coef"));
+  SWSFT_TRY(check_ptr(out, "out"));
+  if (gamma == nullptr) return fail(SWSFT_E_INVALID, "gamma is NULL");
+  if (!std::isfinite(eps) || eps < 0.f) return fail(SWSFT_E_INVALID, "eps must be finite and >= 0");
+  if ((reinterpret_cast<uintptr_t>(gamma) | reinterpret_cast<uintptr_t>(var_in) |
+       reinterpret_cast<uintptr_t>(var_out)) % 4 != 0 ||
+      reinterpret_cast<uintptr_t>(beta) % 8 != 0)
+    return fail(SWSFT_E_INVALID, "gamma, var_in, var_out must be 4-byte, beta 8-byte aligned");
+  if (skip != nullptr) SWSFT_TRY(check_ptr(skip, "skip"));
+  SWSFT_TRY(check_ws(*p, SWSFT_OP_BATCH_NORM, B, 1, C, ws, ws_bytes));
+  {
+    const size_t cs = swsft::coef_elems(*p, p->n_out, B, C) * p->elem;
+    if (out != coef && overlaps(out, cs, coef, cs))
+      return fail(SWSFT_E_INVALID, "out overlaps coef without being equal");
+    if (skip != nullptr && out != skip && overlaps(out, cs, skip, cs))
+      return fail(SWSFT_E_INVALID, "out overlaps skip without being equal");
+    if (overlaps(ws, ws_bytes, coef, cs) || overlaps(ws, ws_bytes, out, cs))
+      return fail(SWSFT_E_INVALID, "the workspace overlaps the coefficients");
+  }
+  SWSFT_TRY(check_device(*p));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return run_stage(*p, swsft::kStageBatchNorm, st, "batch_norm", [&] {
+    return swsft::launch_batch_norm(*p, B, C, coef, gamma, static_cast<const float2*>(beta), eps,
+                                    var_in, var_out, skip, out, ws, st);
+  });
+}
+
+size_t swsft_block_workspace_bytes(swsft_plan p_in, swsft_plan p_out, int B, int C) {
+  if (p_in == nullptr || p_out == nullptr || check_bc(B, C, "C") != SWSFT_OK) return 0;
+  const int S = p_out->n_out;
+  const size_t xy_in = swsft::xy_elems(*p_in, S, B, C), xy_out = swsft::xy_elems(*p_out, S, B, C);
+  const size_t e = p_out->elem;
+  return align_up((xy_in > xy_out ? xy_in : xy_out) * e) +
+         3 * align_up(swsft::coef_elems(*p_out, S, B, C) * e) +
+         align_up((size_t)B * S * C * p_out->H * p_out->W * 2 * e) +
+         align_up(swsft::bn_workspace_bytes(*p_out, B, C));
+}
+
+swsft_status spin_sph_residual_block_forward(swsft_plan p_in, swsft_plan p_out, int B, int C,
+                                             const void* x, const swsft_block_params* prm,
+                                             void* y, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error[0] = 0;
+  if (p_in == nullptr || p_out == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
+  if (prm == nullptr) return fail(SWSFT_E_INVALID, "params is NULL");
+  SWSFT_TRY(check_bc(B, C, "C"));
+  SWSFT_TRY(check_ptr(x, "x"));
+  SWSFT_TRY(check_ptr(y, "y"));
+  SWSFT_TRY(check_ptr(prm->K1, "K1"));
+  SWSFT_TRY(check_ptr(prm->K2, "K2"));
+  if (prm->gamma1 == nullptr || prm->gamma2 == nullptr)
+    return fail(SWSFT_E_INVALID, "gamma1 and gamma2 must not be NULL");
+  if ((reinterpret_cast<uintptr_t>(prm->gamma1) | reinterpret_cast<uintptr_t>(prm->gamma2) |
+       reinterpret_cast<uintptr_t>(prm->var1_out) | reinterpret_cast<uintptr_t>(prm->var2_out)) %
+              4 != 0 ||
+      (reinterpret_cast<uintptr_t>(prm->beta1) | reinterpret_cast<uintptr_t>(prm->beta2)) % 8 != 0)
+    return fail(SWSFT_E_INVALID, "gamma, var must be 4-byte, beta 8-byte aligned");
+  const void* pcs[6] = {prm->pc1_W1, prm->pc1_W2, prm->pc1_b, prm->pc2_W1, prm->pc2_W2, prm->pc2_b};
+  for (const void* q : pcs)
+    if (q == nullptr || reinterpret_cast<uintptr_t>(q) % 8 != 0)
+      return fail(SWSFT_E_INVALID, "phase-collapse parameters must be non-NULL and 8-byte aligned");
+  if (!std::isfinite(prm->eps) || prm->eps < 0.f)
+    return fail(SWSFT_E_INVALID, "eps must be finite and >= 0");
+  swsft::Plan &pi = *p_in, &po = *p_out;
+  if (pi.device != po.device || pi.dtype != po.dtype || pi.L != po.L)
+    return fail(SWSFT_E_INVALID, "the plans differ in device, dtype or bandlimit");
+  const int S = po.n_out;
+  bool same = pi.n_in == S && pi.n_out == S && po.n_in == S, has0 = false;
+  for (int i = 0; same && i < S; ++i) {
+    same = pi.spins_in[i] == po.spins_out[i] && pi.spins_out[i] == po.spins_out[i] &&
+           po.spins_in[i] == po.spins_out[i];
+    has0 |= po.spins_out[i] == 0;
+  }
+  if (!same) return fail(SWSFT_E_INVALID, "both plans must map the same spin list to itself");
+  if (!has0) return fail(SWSFT_E_INVALID, "the spin list must contain spin 0");
+  if (C > swsft::phase_collapse_max_channels(S))
+    return fail(SWSFT_E_UNSUPPORTED, "C = %d exceeds %d channels for %d spins", C,
+                swsft::phase_collapse_max_channels(S), S);
+  const size_t need = swsft_block_workspace_bytes(p_in, p_out, B, C);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(SWSFT_E_WORKSPACE, "workspace: %zu bytes given, %zu needed",
+                ws == nullptr ? (size_t)0 : ws_bytes, need);
+  if (reinterpret_cast<uintptr_t>(ws) % 16 != 0)
+    return fail(SWSFT_E_INVALID, "workspace must be 16-byte aligned");
+  {
+    const size_t xs = (size_t)B * S * C * pi.H * pi.W * 2 * pi.elem;
+    const size_t ys = (size_t)B * S * C * po.H * po.W * 2 * po.elem;
+    if (overlaps(x, xs, y, ys)) return fail(SWSFT_E_INVALID, "x and y overlap");
+    if (overlaps(ws, ws_bytes, x, xs) || overlaps(ws, ws_bytes, y, ys))
+      return fail(SWSFT_E_INVALID, "the workspace overlaps x or y");
+  }
+  SWSFT_TRY(check_device(po));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const size_t xy_in = swsft::xy_elems(pi, S, B, C), xy_out = swsft::xy_elems(po, S, B, C);
+  const size_t cb = align_up(swsft::coef_elems(po, S, B, C) * po.elem);
+  char* w = static_cast<char*>(ws);
+  void* XY = w;
+  w += align_up((xy_in > xy_out ? xy_in : xy_out) * po.elem);
+  void* a = w;  // FT(x): also the skip connection
+  void* h = w + cb;
+  void* g = w + 2 * cb;
+  w += 3 * cb;
+  void* z = w;  // the block's middle feature map, on the output grid
+  w += align_up((size_t)B * S * C * po.H * po.W * 2 * po.elem);
+  void* bnws = w;
+  auto f2 = [](const void* q) { return static_cast<const float2*>(q); };
+
+  // stage timing is recorded on the output plan
+  SWSFT_TRY(run_stage(po, swsft::kStageDftFwd, st, "dft_fwd",
+                      [&] { return swsft::launch_dft_fwd(pi, S, B, C, x, XY, st); }));
+  SWSFT_TRY(run_stage(po, swsft::kStageLatFwd, st, "lat_fwd",
+                      [&] { return swsft::launch_lat_fwd(pi, B, C, XY, a, st); }));
+  SWSFT_TRY(run_stage(po, swsft::kStageMix, st, "mix",
+                      [&] { return swsft::launch_mix(po, B, C, C, a, prm->K1, h, st); }));
+  SWSFT_TRY(run_stage(po, swsft::kStageBatchNorm, st, "batch_norm", [&] {
+    return swsft::launch_batch_norm(po, B, C, h, prm->gamma1, f2(prm->beta1), prm->eps, nullptr,
+                                    prm->var1_out, nullptr, h, bnws, st);
+  }));
+  SWSFT_TRY(run_stage(po, swsft::kStageLatInv, st, "lat_inv",
+                      [&] { return swsft::launch_lat_inv(po, B, C, h, XY, st); }));
+  SWSFT_TRY(run_stage(po, swsft::kStageDftInv, st, "dft_inv",
+                      [&] { return swsft::launch_dft_inv(po, S, B, C, XY, z, st); }));
+  SWSFT_TRY(run_stage(po, swsft::kStagePhaseCollapse, st, "phase_collapse", [&] {
+    return swsft::launch_phase_collapse(po, B, C, z, f2(prm->pc1_W1), f2(prm->pc1_W2),
+                                        f2(prm->pc1_b), z, st);
+  }));
+  SWSFT_TRY(run_stage(po, swsft::kStageDftFwd, st, "dft_fwd",
+                      [&] { return swsft::launch_dft_fwd(po, S, B, C, z, XY, st); }));
+  SWSFT_TRY(run_stage(po, swsft::kStageLatFwd, st, "lat_fwd",
+                      [&] { return swsft::launch_lat_fwd(po, B, C, XY, h, st); }));
+  SWSFT_TRY(run_stage(po, swsft::kStageMix, st, "mix",
+                      [&] { return swsft::launch_mix(po, B, C, C, h, prm->K2, g, st); }));
+  SWSFT_TRY(run_stage(po, swsft::kStageBatchNorm, st, "batch_norm", [&] {
+    return swsft::launch_batch_norm(po, B, C, g, prm->gamma2, f2(prm->beta2), prm->eps, nullptr,
+                                    prm->var2_out, a, g, bnws, st);
+  }));
+  SWSFT_TRY(run_stage(po, swsft::kStageLatInv, st, "lat_inv",
+                      [&] { return swsft::launch_lat_inv(po, B, C, g, XY, st); }));
+  SWSFT_TRY(run_stage(po, swsft::kStageDftInv, st, "dft_inv",
+                      [&] { return swsft::launch_dft_inv(po, S, B, C, XY, y, st); }));
+  return run_stage(po, swsft::kStagePhaseCollapse, st, "phase_collapse", [&] {
+    return swsft::launch_phase_collapse(po, B, C, y, f2(prm->pc2_W1), f2(prm->pc2_W2),
+                                        f2(prm->pc2_b), y, st);
+  });
 }
 
 swsft_status spin_sph_phase_collapse(swsft_plan p, int B, int C, const void* x, const void* W1,

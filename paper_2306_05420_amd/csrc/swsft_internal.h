@@ -24,7 +24,8 @@ enum Stage : int {
   kStageTables = 6,
   kStageFilterGrad = 7,
   kStageFilterAdjoint = 8,
-  kNumStages = 9
+  kStageBatchNorm = 9,
+  kNumStages = 10
 };
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
@@ -101,6 +102,12 @@ hipError_t launch_filter_adjoint(const Plan& p, int C_in, int C_out, const void*
 // where |s| > l or |t| > l; a [L^2][B][S_in][C_in], g [L^2][B][S_out][C_out]
 hipError_t launch_filter_grad(const Plan& p, int B, int C_in, int C_out, const void* a,
                               const void* g, void* gK, hipStream_t st);
+// Spectral batch norm on coefficients [L^2][B][S_out][C] of plan p's output
+// spins (batch_norm.hip); ws holds bn_workspace_bytes(p, B, C) bytes.
+size_t bn_workspace_bytes(const Plan& p, int B, int C);
+hipError_t launch_batch_norm(const Plan& p, int B, int C, const void* a, const float* gamma,
+                             const float2* beta, float eps, const float* var_in, float* var_out,
+                             const void* skip, void* out, void* ws, hipStream_t st);
 // bf16 latitude GEMMs fed by direct global -> LDS copies (see lat_dma.hip).
 bool lat_fwd_dma_supported(const Plan& p, int B, int C);
 bool lat_inv_dma_supported(const Plan& p, int B, int C);

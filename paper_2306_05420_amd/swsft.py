@@ -28,11 +28,20 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "swsft.h")
 
 OK, E_INVALID, E_UNSUPPORTED, E_ALLOC, E_HIP, E_WORKSPACE = range(6)
 F32, BF16 = 0, 1
-OP_FORWARD, OP_INVERSE, OP_CONV, OP_CONV_BACKWARD = 0, 1, 2, 3
+OP_FORWARD, OP_INVERSE, OP_CONV, OP_CONV_BACKWARD, OP_BATCH_NORM = 0, 1, 2, 3, 4
 STAGES = ("dft_fwd", "lat_fwd", "mix", "lat_inv", "dft_inv", "phase_collapse", "tables",
-          "filter_grad", "filter_adjoint")
+          "filter_grad", "filter_adjoint", "batch_norm")
 
 _lib = None
+
+
+class BlockParams(ctypes.Structure):
+    """swsft_block_params: device pointers of the residual block's parameters."""
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("K1", "K2", "gamma1", "beta1", "gamma2", "beta2", "pc1_W1", "pc1_W2", "pc1_b",
+                 "pc2_W1", "pc2_W2", "pc2_b")] + \
+               [("eps", ctypes.c_float), ("var1_out", ctypes.c_void_p),
+                ("var2_out", ctypes.c_void_p)]
 
 
 class SwsftError(RuntimeError):
@@ -61,6 +70,12 @@ def lib() -> ctypes.CDLL:
         "spin_sph_conv_forward": (i, [vp, i, i, i, vp, vp, vp, vp, sz, vp]),
         "spin_sph_conv_backward": (i, [vp, i, i, i, vp, vp, vp, vp, vp, vp, sz, vp]),
         "spin_sph_phase_collapse": (i, [vp, i, i, vp, vp, vp, vp, vp, vp]),
+        "spin_sph_mix": (i, [vp, i, i, i, vp, vp, vp, vp]),
+        "spin_sph_spectral_batch_norm": (i, [vp, i, i, vp, vp, vp, ctypes.c_float, vp, vp, vp,
+                                             vp, vp, sz, vp]),
+        "swsft_block_workspace_bytes": (sz, [vp, vp, i, i]),
+        "spin_sph_residual_block_forward": (i, [vp, vp, i, i, vp, ctypes.POINTER(BlockParams),
+                                                vp, vp, sz, vp]),
         "swsft_status_string": (ctypes.c_char_p, [i]),
         "swsft_last_error": (ctypes.c_char_p, []),
         "swsft_stage_timing": (i, [vp, i]),
@@ -82,6 +97,11 @@ def header_functions() -> list:
     text = open(HEADER_PATH).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return re.findall(r"^[A-Za-z_][\w \*]*?\b(\w+)\s*\(", text, flags=re.M)
+
+
+def _need(t: torch.Tensor, dtype, shape, name: str):
+    if t.dtype != dtype or not t.is_cuda or not t.is_contiguous() or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must be a contiguous {dtype} GPU tensor of shape {tuple(shape)}")
 
 
 def _check(status: int, what: str):
@@ -287,6 +307,56 @@ class Plan:
                                              _stream_handle(stream)), "spin_sph_phase_collapse")
         return y
 
+    def mix(self, coef: torch.Tensor, filters: torch.Tensor, out: torch.Tensor = None,
+            stream=None) -> torch.Tensor:
+        """Per-degree mixing: coef [L*L, B, S_in, C_in] -> [L*L, B, S_out, C_out]."""
+        cr = self.real_view(coef)
+        L2, B, S, Cin = cr.shape[:4]
+        self._shape(cr, (self.L * self.L, B, len(self.spins_in), Cin), "coef")
+        kr = self.real_view(filters)
+        Cout = kr.shape[2]
+        self._shape(kr, (self.L, len(self.spins_out), Cout, len(self.spins_in), Cin), "filters")
+        if out is None:
+            out = self.empty(L2, B, len(self.spins_out), Cout)
+        orr = self.real_view(out)
+        self._shape(orr, (L2, B, len(self.spins_out), Cout), "out")
+        _check(lib().spin_sph_mix(self._h, B, Cin, Cout, cr.data_ptr(), kr.data_ptr(),
+                                  orr.data_ptr(), _stream_handle(stream)), "spin_sph_mix")
+        return out
+
+    def batch_norm(self, coef: torch.Tensor, gamma: torch.Tensor, beta: torch.Tensor = None,
+                   eps: float = 1e-5, var: torch.Tensor = None, skip: torch.Tensor = None,
+                   out: torch.Tensor = None, stream=None):
+        """Spectral batch norm of coefficients [L*L, B, S_out, C] of the output
+        spins; gamma float32 [S_out, C], beta complex64 [C] or None, var
+        float32 [S_out, C] (given statistics) or None (batch statistics).
+        Returns (out, the variance used, float32 [S_out, C])."""
+        cr = self.real_view(coef)
+        L2, B, S, C = cr.shape[:4]
+        self._shape(cr, (self.L * self.L, B, len(self.spins_out), C), "coef")
+        _need(gamma, torch.float32, (S, C), "gamma")
+        if beta is not None:
+            _need(beta, torch.complex64, (C,), "beta")
+        if var is not None:
+            _need(var, torch.float32, (S, C), "var")
+        sk = None
+        if skip is not None:
+            sk = self.real_view(skip)
+            self._shape(sk, tuple(cr.shape[:-1]), "skip")
+        if out is None:
+            out = self.empty(*cr.shape[:-1])
+        orr = self.real_view(out)
+        self._shape(orr, tuple(cr.shape[:-1]), "out")
+        var_out = torch.empty((S, C), dtype=torch.float32, device=self.device)
+        ws = self.workspace(OP_BATCH_NORM, B, 1, C)
+        _check(lib().spin_sph_spectral_batch_norm(
+            self._h, B, C, cr.data_ptr(), gamma.data_ptr(),
+            None if beta is None else beta.data_ptr(), float(eps),
+            None if var is None else var.data_ptr(), var_out.data_ptr(),
+            None if sk is None else sk.data_ptr(), orr.data_ptr(), ws.data_ptr(), ws.numel(),
+            _stream_handle(stream)), "spin_sph_spectral_batch_norm")
+        return out, var_out
+
     # -- tables and timing -------------------------------------------------
     def table(self, which: int, spin_index: int) -> torch.Tensor:
         """Copy of a plan table on the host (float32 or bfloat16 tensor):
@@ -313,3 +383,78 @@ class Plan:
         cnt = (ctypes.c_longlong * n)()
         lib().swsft_stage_times(self._h, ms, cnt, n)
         return {STAGES[i]: (ms[i], cnt[i]) for i in range(n) if cnt[i]}
+
+
+class ResidualBlock:
+    """The residual block with a Fourier-space skip connection, run by
+    spin_sph_residual_block_forward: x on an H_in grid -> y on an H_out grid
+    (spectral pooling when H_out < H_in), bandlimit L = H_out / 2 unless given.
+
+    Parameters are device tensors: K1, K2 filters [L, S, C, S, C] in the
+    plans' storage type; gamma1, gamma2 float32 [S, C]; beta1, beta2 complex64
+    [C] or None; pc1, pc2 = (W1 [C, C], W2 [C, S*C], b [C]) complex64.
+    """
+
+    def __init__(self, H_in: int, H_out: int, spins, C: int, dtype: str = "f32", L: int = None):
+        self.L = int(L) if L is not None else H_out // 2
+        self.C = int(C)
+        self.spins = tuple(int(s) for s in spins)
+        self.p_in = Plan(H_in, H_in, self.L, self.spins, self.spins, dtype)
+        self.p_out = Plan(H_out, H_out, self.L, self.spins, self.spins, dtype)
+        self._ws = {}
+
+    def close(self):
+        self.p_in.close()
+        self.p_out.close()
+        self._ws = {}
+
+    def workspace(self, B: int) -> torch.Tensor:
+        ws = self._ws.get(B)
+        if ws is None:
+            n = int(lib().swsft_block_workspace_bytes(self.p_in._h, self.p_out._h, B, self.C))
+            if n == 0:
+                raise ValueError("invalid workspace request")
+            ws = torch.empty(n, dtype=torch.uint8, device=self.p_out.device)
+            self._ws[B] = ws
+        return ws
+
+    def forward(self, x, K1, K2, gamma1, beta1, gamma2, beta2, pc1, pc2, eps: float = 1e-5,
+                y: torch.Tensor = None, variances: bool = False, stream=None):
+        """y [B, S, C, H_out, H_out]; with variances=True also returns the two
+        batch-norm variances (float32 [S, C] each)."""
+        po = self.p_out
+        xr = self.p_in.real_view(x)
+        B = xr.shape[0]
+        S, C = len(self.spins), self.C
+        self.p_in._shape(xr, (B, S, C, self.p_in.H, self.p_in.W), "x")
+        kshape = (self.L, S, C, S, C)
+        k1, k2 = po.real_view(K1), po.real_view(K2)
+        po._shape(k1, kshape, "K1")
+        po._shape(k2, kshape, "K2")
+        _need(gamma1, torch.float32, (S, C), "gamma1")
+        _need(gamma2, torch.float32, (S, C), "gamma2")
+        for b, nm in ((beta1, "beta1"), (beta2, "beta2")):
+            if b is not None:
+                _need(b, torch.complex64, (C,), nm)
+        for (W1, W2, b), nm in ((pc1, "pc1"), (pc2, "pc2")):
+            _need(W1, torch.complex64, (C, C), nm + " W1")
+            _need(W2, torch.complex64, (C, S * C), nm + " W2")
+            _need(b, torch.complex64, (C,), nm + " b")
+        if y is None:
+            y = po.empty(B, S, C, po.H, po.W)
+        yr = po.real_view(y)
+        po._shape(yr, (B, S, C, po.H, po.W), "y")
+        v1 = torch.empty((S, C), dtype=torch.float32, device=po.device)
+        v2 = torch.empty((S, C), dtype=torch.float32, device=po.device)
+        ptr = lambda t: None if t is None else t.data_ptr()
+        prm = BlockParams(k1.data_ptr(), k2.data_ptr(), gamma1.data_ptr(), ptr(beta1),
+                          gamma2.data_ptr(), ptr(beta2), pc1[0].data_ptr(), pc1[1].data_ptr(),
+                          pc1[2].data_ptr(), pc2[0].data_ptr(), pc2[1].data_ptr(),
+                          pc2[2].data_ptr(), float(eps), v1.data_ptr(), v2.data_ptr())
+        ws = self.workspace(B)
+        _check(lib().spin_sph_residual_block_forward(self.p_in._h, po._h, B, C, xr.data_ptr(),
+                                                     ctypes.byref(prm), yr.data_ptr(),
+                                                     ws.data_ptr(), ws.numel(),
+                                                     _stream_handle(stream)),
+               "spin_sph_residual_block_forward")
+        return (y, v1, v2) if variances else y

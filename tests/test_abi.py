@@ -16,7 +16,7 @@ def L():
 
 def test_exports_every_declared_function(L):
     names = S.header_functions()
-    assert len(names) == 14
+    assert len(names) == 18
     for n in names:
         assert hasattr(L, n), n
 
@@ -60,6 +60,12 @@ def test_calls_reject_null_plan(L):
     assert L.spin_sph_conv_forward(None, 1, 1, 1, x, x, x, x, 1 << 30, None) == S.E_INVALID
     assert L.spin_sph_conv_backward(None, 1, 1, 1, x, x, x, x, x, x, 1 << 30, None) == S.E_INVALID
     assert L.spin_sph_phase_collapse(None, 1, 1, x, x, x, x, x, None) == S.E_INVALID
+    assert L.spin_sph_mix(None, 1, 1, 1, x, x, x, None) == S.E_INVALID
+    assert L.spin_sph_spectral_batch_norm(None, 1, 1, x, x, None, 0.0, None, None, None, x, x,
+                                          1 << 30, None) == S.E_INVALID
+    assert L.swsft_block_workspace_bytes(None, None, 1, 1) == 0
+    assert L.spin_sph_residual_block_forward(None, None, 1, 1, x, None, x, x, 1 << 30,
+                                             None) == S.E_INVALID
     assert L.swsft_stage_timing(None, 1) == S.E_INVALID
     assert L.swsft_workspace_bytes(None, 0, 1, 1, 1) == 0
     assert L.swsft_stage_times(None, None, None, 0) == 0
