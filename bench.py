@@ -448,8 +448,71 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
         r["stack2"] = {"us": round(t2 * 1e6, 2), "per_s": round(1.0 / t2, 1),
                        "TFLOP/s": round(2 * useful / t2 / 1e12, 2)}
         plan2.close()
+        r["block"] = {f"{hi}to{ho}": measure_block(w, hi, ho, gen, storage, steps, warmup)
+                      for hi, ho in ((w.H, w.H), (2 * w.H, w.H))}
     plan.close()
     return r
+
+
+def block_flops(w, H_in: int, H_out: int) -> int:
+    """Useful flops of one residual-block call on spins_out x C_out channels:
+    one forward-latitude contraction on the input grid, one on the output
+    grid, two inverse-latitude contractions and two mixings."""
+    L, B, C = w.L, w.B, w.C_out
+    lat = lambda H: sum(4 * H * B * C * (L * L - s * s) for s in w.spins_out)
+    mix = 0
+    for l in range(L):
+        k = C * sum(1 for s in w.spins_out if abs(s) <= l)
+        mix += 8 * B * (2 * l + 1) * k * k
+    return lat(H_in) + 3 * lat(H_out) + 2 * mix
+
+
+def measure_block(w, H_in: int, H_out: int, gen, storage, steps: int, warmup: int) -> dict:
+    """Time the residual block (spins_out -> spins_out, C_out channels) from an
+    H_in grid to an H_out grid (spectral pooling when H_out < H_in)."""
+    import torch
+
+    from paper_2306_05420_amd import swsft as S
+    from paper_2306_05420_amd import synthetic as syn
+
+    spins, C, B, L = w.spins_out, w.C_out, w.B, w.L
+    Sn = len(spins)
+    blk = S.ResidualBlock(H_in, H_out, spins, C, w.dtype, L=L)
+    x = storage(syn.torch_complex_normal(gen, (B, Sn, C, H_in, H_in)))
+    K1 = storage(syn.torch_random_filters(gen, L, spins, C, spins, C, w.filter_var))
+    K2 = storage(syn.torch_random_filters(gen, L, spins, C, spins, C, w.filter_var))
+    dev = x.device
+    g1 = torch.ones((Sn, C), dtype=torch.float32, device=dev)
+    g2 = torch.ones((Sn, C), dtype=torch.float32, device=dev)
+    b1 = syn.torch_complex_normal(gen, (C,), 0.01)
+    b2 = syn.torch_complex_normal(gen, (C,), 0.01)
+    pc = lambda: (syn.torch_complex_normal(gen, (C, C), 1.0 / C),
+                  syn.torch_complex_normal(gen, (C, Sn * C), 1.0 / (Sn * C)),
+                  syn.torch_complex_normal(gen, (C,), 0.01))
+    pc1, pc2 = pc(), pc()
+    y = blk.p_out.empty(B, Sn, C, H_out, H_out)
+    fn = lambda: blk.forward(x, K1, K2, g1, b1, g2, b2, pc1, pc2, 1e-5, y=y)
+    t = _time_calls(fn, steps, warmup)
+    blk.p_out.stage_timing(True)
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    times = blk.p_out.stage_times()
+    blk.p_out.stage_timing(False)
+    blk.close()
+    fl = block_flops(w, H_in, H_out)
+    e = 2 if w.dtype == "bf16" else 4
+    coef_b = L * L * B * Sn * C * 2 * e
+    stages = {k: {"us_per_call": round(ms * 1e3 / steps, 2), "launches_per_call": n // steps}
+              for k, (ms, n) in times.items()}
+    if "batch_norm" in stages:
+        # per call: two norms, each reading its input twice and writing once, the
+        # second also reading the skip coefficients
+        bn_bytes = 7 * coef_b
+        stages["batch_norm"]["GB/s"] = round(bn_bytes / (stages["batch_norm"]["us_per_call"] * 1e3), 1)
+    return {"grid": f"{H_in}x{H_in} -> {H_out}x{H_out}", "us": round(t * 1e6, 2),
+            "per_s": round(1.0 / t, 1), "TFLOP/s": round(fl / t / 1e12, 2),
+            "useful_gflop": round(fl / 1e9, 3), "stages": stages}
 
 
 def backward_flops(w) -> int:
@@ -513,6 +576,9 @@ def table_rows(cfg: int, r: dict):
     if "stack2" in r:
         t = r["stack2"]
         rows.append(f"| {cfg} {w.name} | 2 layers + phase collapse | {t['us']:.1f} | {t['per_s']:.0f} | "
+                    f"{t['TFLOP/s']:.1f} | {100 * t['TFLOP/s'] / peak:.1f} | — | — |")
+    for t in r.get("block", {}).values():
+        rows.append(f"| {cfg} {w.name} | residual block {t['grid']} | {t['us']:.1f} | {t['per_s']:.0f} | "
                     f"{t['TFLOP/s']:.1f} | {100 * t['TFLOP/s'] / peak:.1f} | — | — |")
     return rows
 

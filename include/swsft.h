@@ -225,6 +225,7 @@ swsft_status spin_sph_mix(swsft_plan p, int B, int C_in, int C_out, const void* 
  *  out      [L*L][B][S_out][C] complex; out == coef and out == skip are allowed.
  *  ws       >= swsft_workspace_bytes(p, SWSFT_OP_BATCH_NORM, B, 1, C) bytes.
  * The statistics are summed in float32 in a fixed order (deterministic).
+ * S_out * C above 2048 returns SWSFT_E_UNSUPPORTED.
  */
 swsft_status spin_sph_spectral_batch_norm(swsft_plan p, int B, int C, const void* coef,
                                           const float* gamma, const void* beta, float eps,
@@ -276,7 +277,8 @@ size_t swsft_block_workspace_bytes(swsft_plan p_in, swsft_plan p_out, int B, int
  *  x   [B][S][C][H_in][W_in] complex, read only.
  *  y   [B][S][C][H_out][W_out] complex, written; must not overlap x.
  *  ws  >= swsft_block_workspace_bytes(p_in, p_out, B, C) bytes.
- * Stage timing, if enabled, is recorded on p_out.
+ * Stage timing, if enabled, is recorded on p_out.  Channel limits: those of
+ * the phase collapse and of the batch norm (S * C <= 2048).
  */
 swsft_status spin_sph_residual_block_forward(swsft_plan p_in, swsft_plan p_out, int B, int C,
                                              const void* x, const swsft_block_params* params,

@@ -10,8 +10,8 @@
 //
 // Three launches, all deterministic (no atomics):
 //   bn_partial   each workgroup sums |a|^2 over a fixed range of rows for
-//                every column (threads across columns: coalesced rows);
-//   bn_finalize  per column: the partial sums in workgroup order -> var, scale;
+//                every column (threads across a row: coalesced);
+//   bn_finalize  per column: the partial sums in a fixed order -> var, scale;
 //   bn_apply     elementwise, 4 complex values per thread.
 #include "swsft_internal.h"
 
@@ -26,37 +26,102 @@ __device__ __forceinline__ float2 ld_c(const T* p, size_t i) {
   return make_float2((float)p[2 * i], (float)p[2 * i + 1]);
 }
 
+// Threads are (row lane, column lane): TPR = min(ncol, 256) rounded down to a
+// power of two threads share a row, 256 / TPR rows are read at once, and
+// each thread keeps the sums of its columns (col, col + TPR, ...) in
+// registers; the row lanes are combined through LDS at the end.
+constexpr int kMaxColsPerThread = 8;
+
 template <typename T>
 __global__ void __launch_bounds__(kNT) bn_partial_kernel(const T* __restrict__ a,
                                                          float* __restrict__ partial, int rows,
-                                                         int row_begin, int rows_per_blk, int ncol) {
+                                                         int row_begin, int rows_per_blk, int ncol,
+                                                         int tpr) {
+  __shared__ float red[kNT * kMaxColsPerThread];
+  const int rl = threadIdx.x / tpr, cl = threadIdx.x % tpr;
+  const int rsub = kNT / tpr;
+  const int ncpt = (ncol + tpr - 1) / tpr;  // columns per thread (<= kMaxColsPerThread)
   const int r0 = row_begin + blockIdx.x * rows_per_blk;
   const int r1 = min(r0 + rows_per_blk, rows);
-  for (int col = threadIdx.x; col < ncol; col += kNT) {
-    float acc = 0.f;
-    for (int r = r0; r < r1; ++r) {
-      const float2 v = ld_c(a, (size_t)r * ncol + col);
-      acc += v.x * v.x + v.y * v.y;
+  float acc[kMaxColsPerThread];
+#pragma unroll
+  for (int j = 0; j < kMaxColsPerThread; ++j) acc[j] = 0.f;
+  int r = r0 + rl;
+  // four rows in flight per thread
+  for (; r + 3 * rsub < r1; r += 4 * rsub) {
+#pragma unroll
+    for (int j = 0; j < kMaxColsPerThread; ++j) {
+      const int col = cl + j * tpr;
+      if (j < ncpt && col < ncol) {
+        const float2 v0 = ld_c(a, (size_t)r * ncol + col);
+        const float2 v1 = ld_c(a, (size_t)(r + rsub) * ncol + col);
+        const float2 v2 = ld_c(a, (size_t)(r + 2 * rsub) * ncol + col);
+        const float2 v3 = ld_c(a, (size_t)(r + 3 * rsub) * ncol + col);
+        acc[j] += (v0.x * v0.x + v0.y * v0.y) + (v1.x * v1.x + v1.y * v1.y) +
+                  (v2.x * v2.x + v2.y * v2.y) + (v3.x * v3.x + v3.y * v3.y);
+      }
     }
-    partial[(size_t)blockIdx.x * ncol + col] = acc;
+  }
+  for (; r < r1; r += rsub) {
+#pragma unroll
+    for (int j = 0; j < kMaxColsPerThread; ++j) {
+      const int col = cl + j * tpr;
+      if (j < ncpt && col < ncol) {
+        const float2 v = ld_c(a, (size_t)r * ncol + col);
+        acc[j] += v.x * v.x + v.y * v.y;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kMaxColsPerThread; ++j) red[j * kNT + threadIdx.x] = acc[j];
+  __syncthreads();
+  // thread (rl = 0, cl) sums the row lanes of its columns in a fixed order
+  if (rl == 0) {
+    for (int j = 0; j < ncpt; ++j) {
+      const int col = cl + j * tpr;
+      if (col >= ncol) break;
+      float sum = 0.f;
+      for (int q = 0; q < rsub; ++q) sum += red[j * kNT + q * tpr + cl];
+      partial[(size_t)blockIdx.x * ncol + col] = sum;
+    }
   }
 }
 
+// One workgroup per 32 columns: 8 lanes per column sum the partial rows
+// b = lane, lane + 8, ... (four loads in flight), then lane 0 adds the 8
+// lane sums in order.
 __global__ void __launch_bounds__(kNT) bn_finalize_kernel(const float* __restrict__ partial,
                                                           int nblk, int ncol, float inv_norm,
                                                           const float* __restrict__ var_in,
                                                           const float* __restrict__ gamma,
                                                           float eps, float* __restrict__ scale,
                                                           float* __restrict__ var_out) {
-  const int col = blockIdx.x * kNT + threadIdx.x;
-  if (col >= ncol) return;
+  __shared__ float red[kNT];
+  const int lane = threadIdx.x / 32, cc = threadIdx.x % 32;
+  const int col = blockIdx.x * 32 + cc;
+  float acc = 0.f;
+  if (var_in == nullptr && col < ncol) {
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+    int b = lane;
+    for (; b + 24 < nblk; b += 32) {
+      a0 += partial[(size_t)b * ncol + col];
+      a1 += partial[(size_t)(b + 8) * ncol + col];
+      a2 += partial[(size_t)(b + 16) * ncol + col];
+      a3 += partial[(size_t)(b + 24) * ncol + col];
+    }
+    for (; b < nblk; b += 8) a0 += partial[(size_t)b * ncol + col];
+    acc = (a0 + a1) + (a2 + a3);
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  if (lane != 0 || col >= ncol) return;
   float var;
   if (var_in != nullptr) {
     var = var_in[col];
   } else {
-    float acc = 0.f;
-    for (int b = 0; b < nblk; ++b) acc += partial[(size_t)b * ncol + col];
-    var = acc * inv_norm;
+    float sum = 0.f;
+    for (int q = 0; q < kNT / 32; ++q) sum += red[q * 32 + cc];
+    var = sum * inv_norm;
   }
   scale[col] = gamma[col] / sqrtf(var + eps);
   if (var_out != nullptr) var_out[col] = var;
@@ -90,12 +155,16 @@ __global__ void __launch_bounds__(kNT) bn_apply_kernel(const T* a,  // may be ou
     for (int e = 0; e < n; ++e) v[e] = ld_c(a, i0 + e);
   }
   float2 o[4];
+  long long row = i0 / ncol;
+  int col = (int)(i0 - row * ncol);
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
+  for (int e = 0; e < 4; ++e, ++col) {
     if (e >= n) break;
+    if (col == ncol) {
+      col = 0;
+      ++row;
+    }
     const long long i = i0 + e;
-    const int col = (int)(i % ncol);
-    const long long row = i / ncol;
     if (row < B) {  // degree 0: the bias for spin 0, else 0
       o[e] = (col / C == s0 && beta != nullptr) ? beta[col % C] : make_float2(0.f, 0.f);
     } else {
@@ -119,7 +188,20 @@ __global__ void __launch_bounds__(kNT) bn_apply_kernel(const T* a,  // may be ou
 int bn_partial_blocks(const Plan& p, int B) {
   const int rows = p.L * p.L * B - B;  // rows of degrees l >= 1
   int nblk = (rows + 63) / 64;         // at least 64 rows per workgroup
-  return nblk < 1 ? 1 : (nblk > 512 ? 512 : nblk);
+  return nblk < 1 ? 1 : (nblk > 256 ? 256 : nblk);
+}
+
+// threads per row: the largest power of two <= min(ncol, 256) that leaves
+// at most kMaxColsPerThread columns per thread
+int bn_threads_per_row(int ncol) {
+  int t = 1;
+  while (t * 2 <= ncol && t * 2 <= kNT) t *= 2;
+  return t;
+}
+
+bool bn_supported(const Plan& p, int C) {
+  const int ncol = p.n_out * C;
+  return (ncol + bn_threads_per_row(ncol) - 1) / bn_threads_per_row(ncol) <= kMaxColsPerThread;
 }
 
 size_t bn_workspace_bytes(const Plan& p, int B, int C) {
@@ -140,9 +222,9 @@ hipError_t bn_t(const Plan& p, int B, int C, const void* a, const float* gamma,
     const int body = rows - B;
     const int per = (body + nblk - 1) / nblk;
     hipLaunchKernelGGL(bn_partial_kernel<T>, dim3(nblk), dim3(kNT), 0, st, (const T*)a, partial,
-                       rows, B, per, ncol);
+                       rows, B, per, ncol, bn_threads_per_row(ncol));
   }
-  hipLaunchKernelGGL(bn_finalize_kernel, dim3((ncol + kNT - 1) / kNT), dim3(kNT), 0, st, partial,
+  hipLaunchKernelGGL(bn_finalize_kernel, dim3((ncol + 31) / 32), dim3(kNT), 0, st, partial,
                      nblk, ncol, kInv4Pi / (float)B, var_in, gamma, eps, scale, var_out);
   int s0 = -1;
   for (int i = 0; i < p.n_out; ++i)

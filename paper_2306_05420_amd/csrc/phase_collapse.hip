@@ -101,20 +101,33 @@ __global__ void __launch_bounds__(NTP) phase_collapse_mfma_kernel(
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const size_t map0 = (size_t)b * S * C;
-  for (int idx = tid; idx < SC * PM; idx += NTP) {
-    const int p = idx % PM, sc = idx / PM;
-    float2 v = make_float2(0.f, 0.f);  // points past the end stage zeros
-    const size_t e = (map0 + sc) * HW + p0 + p;
-    if (p < np) v = ld2(x, e);
-    zs[(2 * C + sc) * PM + zcol(2 * C + sc, p)] = sqrtf(v.x * v.x + v.y * v.y);
-    const int s = sc / C;
-    if (s == s0) {
-      const int c = sc - s0 * C;
-      zs[c * PM + zcol(c, p)] = v.x;
-      zs[(C + c) * PM + zcol(C + c, p)] = v.y;
-    } else if (copy_others && p < np) {
-      y[2 * e] = x[2 * e];
-      y[2 * e + 1] = x[2 * e + 1];
+  // staging: SB loads in flight per thread before any of them is used
+  constexpr int SB = 8;
+  for (int base = 0; base < SC * PM; base += SB * NTP) {
+    float2 v[SB];
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      const int idx = base + u * NTP + tid;
+      const int p = idx % PM, sc = idx / PM;
+      v[u] = make_float2(0.f, 0.f);  // points past the end stage zeros
+      if (idx < SC * PM && p < np) v[u] = ld2(x, (map0 + sc) * HW + p0 + p);
+    }
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      const int idx = base + u * NTP + tid;
+      if (idx >= SC * PM) break;
+      const int p = idx % PM, sc = idx / PM;
+      zs[(2 * C + sc) * PM + zcol(2 * C + sc, p)] = sqrtf(v[u].x * v[u].x + v[u].y * v[u].y);
+      const int s = sc / C;
+      if (s == s0) {
+        const int c = sc - s0 * C;
+        zs[c * PM + zcol(c, p)] = v[u].x;
+        zs[(C + c) * PM + zcol(C + c, p)] = v[u].y;
+      } else if (copy_others && p < np) {
+        const size_t e = (map0 + sc) * HW + p0 + p;
+        y[2 * e] = (T)v[u].x;
+        y[2 * e + 1] = (T)v[u].y;
+      }
     }
   }
   __syncthreads();

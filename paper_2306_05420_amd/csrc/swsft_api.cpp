@@ -514,6 +514,8 @@ swsft_status spin_sph_spectral_batch_norm(swsft_plan p, int B, int C, const void
       reinterpret_cast<uintptr_t>(beta) % 8 != 0)
     return fail(SWSFT_E_INVALID, "gamma, var_in, var_out must be 4-byte, beta 8-byte aligned");
   if (skip != nullptr) SWSFT_TRY(check_ptr(skip, "skip"));
+  if (!swsft::bn_supported(*p, C))
+    return fail(SWSFT_E_UNSUPPORTED, "S_out * C = %d exceeds 2048 columns", p->n_out * C);
   SWSFT_TRY(check_ws(*p, SWSFT_OP_BATCH_NORM, B, 1, C, ws, ws_bytes));
   {
     const size_t cs = swsft::coef_elems(*p, p->n_out, B, C) * p->elem;
@@ -582,6 +584,8 @@ swsft_status spin_sph_residual_block_forward(swsft_plan p_in, swsft_plan p_out, 
   if (C > swsft::phase_collapse_max_channels(S))
     return fail(SWSFT_E_UNSUPPORTED, "C = %d exceeds %d channels for %d spins", C,
                 swsft::phase_collapse_max_channels(S), S);
+  if (!swsft::bn_supported(po, C))
+    return fail(SWSFT_E_UNSUPPORTED, "S * C = %d exceeds 2048 columns", S * C);
   const size_t need = swsft_block_workspace_bytes(p_in, p_out, B, C);
   if (ws == nullptr || ws_bytes < need)
     return fail(SWSFT_E_WORKSPACE, "workspace: %zu bytes given, %zu needed",

@@ -105,6 +105,7 @@ hipError_t launch_filter_grad(const Plan& p, int B, int C_in, int C_out, const v
 // Spectral batch norm on coefficients [L^2][B][S_out][C] of plan p's output
 // spins (batch_norm.hip); ws holds bn_workspace_bytes(p, B, C) bytes.
 size_t bn_workspace_bytes(const Plan& p, int B, int C);
+bool bn_supported(const Plan& p, int C);  // S_out * C <= 2048
 hipError_t launch_batch_norm(const Plan& p, int B, int C, const void* a, const float* gamma,
                              const float2* beta, float eps, const float* var_in, float* var_out,
                              const void* skip, void* out, void* ws, hipStream_t st);
