@@ -73,6 +73,16 @@ typedef enum {
   SWSFT_BF16 = 1  /* bfloat16 storage, float accumulation (MFMA bf16)    */
 } swsft_dtype;
 
+/* Plan creation flags (swsft_plan_create_ex). */
+typedef enum {
+  /* Forward longitude stage as a dense DFT matrix product on MFMA (the route
+   * the paper takes on TPUs: Method, "Efficient TPU implementation"; appendix
+   * "FFT vs DFT", Table 8) instead of the register FFT.  Also admits any even
+   * W for swsft_forward; calls that need the inverse longitude stage then
+   * return SWSFT_E_UNSUPPORTED unless W is a power of two <= 512. */
+  SWSFT_PLAN_DFT_MATMUL = 1
+} swsft_plan_flags;
+
 typedef enum {
   SWSFT_OP_FORWARD = 0, /* swsft_forward          */
   SWSFT_OP_INVERSE = 1, /* swsft_inverse          */
@@ -85,8 +95,9 @@ typedef enum {
  * Create a plan for H x W grids with bandlimit L (Background, eqs. (2)-(3)).
  *  H, W        grid size; H == W (the transform needs equal sample counts on
  *              both axes, appendix "WeatherBench"), H even.  Implemented:
- *              W a power of two in [2, 512]; other even sizes return
- *              SWSFT_E_UNSUPPORTED.
+ *              W a power of two in [2, 512] (with SWSFT_PLAN_DFT_MATMUL
+ *              any even W up to 32 or multiple of 32 for the forward
+ *              transform); other sizes return SWSFT_E_UNSUPPORTED.
  *  L           bandlimit, 1 <= L <= H/2 (L < H/2 is spectral pooling:
  *              Method, "Spectral pooling").
  *  spins_in    host array of n_spins_in distinct spins, |s| < L, 1..8 of them.
@@ -100,6 +111,13 @@ typedef enum {
 swsft_status swsft_plan_create(int H, int W, int L, const int* spins_in, int n_spins_in,
                                const int* spins_out, int n_spins_out, int dtype,
                                swsft_plan* out);
+
+/* swsft_plan_create with creation flags (swsft_plan_flags; 0 is
+ * swsft_plan_create).  With SWSFT_PLAN_DFT_MATMUL the plan also holds the
+ * expanded DFT matrix, [2(2L-1)][2W] reals of the storage type. */
+swsft_status swsft_plan_create_ex(int H, int W, int L, const int* spins_in, int n_spins_in,
+                                  const int* spins_out, int n_spins_out, int dtype,
+                                  unsigned flags, swsft_plan* out);
 
 /* Free the plan's device tables.  NULL-safe.  The caller must make sure no
  * enqueued call still uses the plan. */

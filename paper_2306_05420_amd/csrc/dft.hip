@@ -435,6 +435,7 @@ hipError_t dispatch_inv(const Plan& p, int S, int B, int C, const void* Y, void*
 
 hipError_t launch_dft_fwd(const Plan& p, int S, int B, int C, const void* x, void* X,
                           hipStream_t st) {
+  if (p.flags & SWSFT_PLAN_DFT_MATMUL) return launch_dft_fwd_matmul(p, S, B, C, x, X, st);
   if (p.dtype == SWSFT_BF16) return dispatch_fwd<__bf16>(p, S, B, C, x, X, st);
   return dispatch_fwd<float>(p, S, B, C, x, X, st);
 }

@@ -138,6 +138,13 @@ hipError_t ensure_dynamic_lds(const void* kern, size_t bytes) {
 
 namespace {
 
+swsft_status check_inverse_stage(const Plan& p) {
+  if (!p.fft_ok)
+    return fail(SWSFT_E_UNSUPPORTED, "W = %d: the inverse longitude stage needs a power of two <= 512",
+                p.W);
+  return SWSFT_OK;
+}
+
 swsft_status check_device(const Plan& p) {
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
@@ -178,6 +185,7 @@ void free_plan(Plan* p) {
   if (p->tab_inv) (void)hipFree(p->tab_inv);
   if (p->tab_bwd_syn) (void)hipFree(p->tab_bwd_syn);
   if (p->tab_bwd_ana) (void)hipFree(p->tab_bwd_ana);
+  if (p->dft_mat) (void)hipFree(p->dft_mat);
   if (p->twiddle) (void)hipFree(p->twiddle);
   if (p->ev) {
     for (int i = 0; i < 2 * swsft::kMaxTimedLaunches; ++i)
@@ -216,6 +224,13 @@ const char* swsft_stage_name(int stage) {
 swsft_status swsft_plan_create(int H, int W, int L, const int* spins_in, int n_spins_in,
                                const int* spins_out, int n_spins_out, int dtype,
                                swsft_plan* out) {
+  return swsft_plan_create_ex(H, W, L, spins_in, n_spins_in, spins_out, n_spins_out, dtype, 0u,
+                              out);
+}
+
+swsft_status swsft_plan_create_ex(int H, int W, int L, const int* spins_in, int n_spins_in,
+                                  const int* spins_out, int n_spins_out, int dtype,
+                                  unsigned flags, swsft_plan* out) {
   g_last_error[0] = 0;
   if (out == nullptr) return fail(SWSFT_E_INVALID, "out is NULL");
   if (H != W) return fail(SWSFT_E_INVALID, "H = %d != W = %d (square grids only)", H, W);
@@ -225,8 +240,14 @@ swsft_status swsft_plan_create(int H, int W, int L, const int* spins_in, int n_s
     return fail(SWSFT_E_INVALID, "dtype %d is not a swsft_dtype", dtype);
   SWSFT_TRY(check_spins(spins_in, n_spins_in, L, "spins_in"));
   SWSFT_TRY(check_spins(spins_out, n_spins_out, L, "spins_out"));
-  if (!is_pow2(W) || W > 512)
-    return fail(SWSFT_E_UNSUPPORTED, "W = %d: only powers of two up to 512 are implemented", W);
+  if (flags & ~(unsigned)SWSFT_PLAN_DFT_MATMUL) return fail(SWSFT_E_INVALID, "unknown flags %#x", flags);
+  const bool fft_ok = is_pow2(W) && W <= 512;
+  if (H > 32 && H % 32 != 0)
+    return fail(SWSFT_E_UNSUPPORTED, "H = %d: grids above 32 take whole latitude tiles of 32 rows", H);
+  if (!fft_ok && !(flags & SWSFT_PLAN_DFT_MATMUL))
+    return fail(SWSFT_E_UNSUPPORTED,
+                "W = %d: the FFT longitude stage takes powers of two up to 512 "
+                "(SWSFT_PLAN_DFT_MATMUL takes any even W for the forward transform)", W);
 
   Plan* p = new (std::nothrow) swsft_plan_s();
   if (p == nullptr) return fail(SWSFT_E_ALLOC, "host allocation of the plan failed");
@@ -243,6 +264,8 @@ swsft_status swsft_plan_create(int H, int W, int L, const int* spins_in, int n_s
   for (int i = 0; i < n_spins_out; ++i) p->spins_out[i] = spins_out[i];
   p->dtype = dtype;
   p->elem = dtype == SWSFT_BF16 ? 2 : 4;
+  p->flags = flags;
+  p->fft_ok = fft_ok;
 
   hipError_t e = hipGetDevice(&p->device);
   if (e != hipSuccess) {
@@ -272,6 +295,22 @@ swsft_status swsft_plan_create(int H, int W, int L, const int* spins_in, int n_s
     free_plan(p);
     delete static_cast<swsft_plan_s*>(p);
     return hip_fail(e, "table generation");
+  }
+  if (flags & SWSFT_PLAN_DFT_MATMUL) {
+    const size_t db = (size_t)2 * p->M * 2 * W * p->elem;
+    if (hipMalloc(&p->dft_mat, db) != hipSuccess) {
+      (void)hipGetLastError();
+      p->dft_mat = nullptr;
+      free_plan(p);
+      delete static_cast<swsft_plan_s*>(p);
+      return fail(SWSFT_E_ALLOC, "hipMalloc of the %zu-byte DFT matrix failed", db);
+    }
+    if ((e = swsft::launch_dft_matrix(*p, nullptr)) != hipSuccess ||
+        (e = hipDeviceSynchronize()) != hipSuccess) {
+      free_plan(p);
+      delete static_cast<swsft_plan_s*>(p);
+      return hip_fail(e, "DFT matrix generation");
+    }
   }
   *out = static_cast<swsft_plan_s*>(p);
   return SWSFT_OK;
@@ -316,6 +355,7 @@ swsft_status swsft_inverse(swsft_plan p, int B, int C, const void* coef, void* y
   SWSFT_TRY(check_bc(B, C, "C"));
   SWSFT_TRY(check_ptr(coef, "coef"));
   SWSFT_TRY(check_ptr(y, "y"));
+  SWSFT_TRY(check_inverse_stage(*p));
   SWSFT_TRY(check_ws(*p, SWSFT_OP_INVERSE, B, 1, C, ws, ws_bytes));
   SWSFT_TRY(check_device(*p));
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -337,6 +377,7 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
   SWSFT_TRY(check_ptr(x, "x"));
   SWSFT_TRY(check_ptr(filters, "filters"));
   SWSFT_TRY(check_ptr(y, "y"));
+  SWSFT_TRY(check_inverse_stage(*p));
   SWSFT_TRY(check_ws(*p, SWSFT_OP_CONV, B, C_in, C_out, ws, ws_bytes));
   {
     const char* xb = static_cast<const char*>(x);
@@ -380,6 +421,7 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
   if (grad_x == nullptr && grad_filters == nullptr)
     return fail(SWSFT_E_INVALID, "neither grad_x nor grad_filters requested");
   SWSFT_TRY(check_ptr(grad_y, "grad_y"));
+  SWSFT_TRY(check_inverse_stage(*p));
   if (grad_filters != nullptr) {
     SWSFT_TRY(check_ptr(x, "x"));
     SWSFT_TRY(check_ptr(grad_filters, "grad_filters"));
@@ -580,6 +622,7 @@ swsft_status spin_sph_residual_block_forward(swsft_plan p_in, swsft_plan p_out, 
     has0 |= po.spins_out[i] == 0;
   }
   if (!same) return fail(SWSFT_E_INVALID, "both plans must map the same spin list to itself");
+  SWSFT_TRY(check_inverse_stage(po));
   if (!has0) return fail(SWSFT_E_INVALID, "the spin list must contain spin 0");
   if (C > swsft::phase_collapse_max_channels(S))
     return fail(SWSFT_E_UNSUPPORTED, "C = %d exceeds %d channels for %d spins", C,

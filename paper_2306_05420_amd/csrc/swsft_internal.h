@@ -50,6 +50,11 @@ struct Plan {
   void* tab_bwd_syn = nullptr;  // [n_in][M][Hp][Lp]
   void* tab_bwd_ana = nullptr;  // [n_out][M][L][Hp]
   float2* twiddle = nullptr;  // [W]: exp(-2 pi i r / W)
+  // creation flags (SWSFT_PLAN_*); with SWSFT_PLAN_DFT_MATMUL the forward
+  // longitude stage is a dense DFT GEMM against dft_mat [2M][2W]
+  unsigned flags = 0;
+  void* dft_mat = nullptr;
+  bool fft_ok = true;  // W is a size of the register FFT (a power of two <= 512)
   // stage timing
   bool timing = false;
   int n_timed = 0;
@@ -82,6 +87,10 @@ hipError_t launch_tables(const Plan& p, hipStream_t st);
 // x [B][S][C][H][W] -> X [S][M][H/JT][B*C][2][JT]
 hipError_t launch_dft_fwd(const Plan& p, int S, int B, int C, const void* x, void* X,
                           hipStream_t st);
+// the dense-DFT forward longitude stage (dft_mm.hip) and its plan-time matrix
+hipError_t launch_dft_fwd_matmul(const Plan& p, int S, int B, int C, const void* x, void* X,
+                                 hipStream_t st);
+hipError_t launch_dft_matrix(const Plan& p, hipStream_t st);
 // Y [S][M][H/JT][B*C][2][JT] -> y [B][S][C][H][W]
 hipError_t launch_dft_inv(const Plan& p, int S, int B, int C, const void* Y, void* y,
                           hipStream_t st);

@@ -27,6 +27,7 @@ LIB_PATH = os.environ.get("SWSFT_LIBRARY") or os.path.join(_PKG, "libswsft.so")
 HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "swsft.h")
 
 OK, E_INVALID, E_UNSUPPORTED, E_ALLOC, E_HIP, E_WORKSPACE = range(6)
+PLAN_DFT_MATMUL = 1
 F32, BF16 = 0, 1
 OP_FORWARD, OP_INVERSE, OP_CONV, OP_CONV_BACKWARD, OP_BATCH_NORM = 0, 1, 2, 3, 4
 STAGES = ("dft_fwd", "lat_fwd", "mix", "lat_inv", "dft_inv", "phase_collapse", "tables",
@@ -63,6 +64,8 @@ def lib() -> ctypes.CDLL:
     ip = ctypes.POINTER(ctypes.c_int)
     sigs = {
         "swsft_plan_create": (i, [i, i, i, ip, i, ip, i, i, ctypes.POINTER(vp)]),
+        "swsft_plan_create_ex": (i, [i, i, i, ip, i, ip, i, i, ctypes.c_uint,
+                                     ctypes.POINTER(vp)]),
         "swsft_plan_destroy": (None, [vp]),
         "swsft_workspace_bytes": (sz, [vp, i, i, i, i]),
         "swsft_forward": (i, [vp, i, i, vp, vp, vp, sz, vp]),
@@ -117,13 +120,16 @@ def _stream_handle(stream) -> int:
 
 
 class Plan:
-    """A transform plan: grid H x W, bandlimit L, input/output spins, dtype.
+    """A transform plan: grid H x W, bandlimit L, input/output spins, dtype,
+    and the forward longitude stage ("fft": register FFT; "matmul": dense DFT
+    matrix product on MFMA, which also takes widths that are not powers of two).
 
     Owns the device tables built by swsft_plan_create; workspaces are cached
     per call shape (allocated through torch, i.e. by the caller of the C ABI).
     """
 
-    def __init__(self, H: int, W: int, L: int, spins_in, spins_out, dtype: str = "f32"):
+    def __init__(self, H: int, W: int, L: int, spins_in, spins_out, dtype: str = "f32",
+                 longitude: str = "fft"):
         self.H, self.W, self.L = int(H), int(W), int(L)
         self.spins_in = tuple(int(s) for s in spins_in)
         self.spins_out = tuple(int(s) for s in spins_out)
@@ -134,9 +140,14 @@ class Plan:
         si = (ctypes.c_int * len(self.spins_in))(*self.spins_in)
         so = (ctypes.c_int * len(self.spins_out))(*self.spins_out)
         h = ctypes.c_void_p()
-        _check(lib().swsft_plan_create(self.H, self.W, self.L, si, len(self.spins_in), so,
-                                       len(self.spins_out), self._code, ctypes.byref(h)),
-               "swsft_plan_create")
+        if longitude not in ("fft", "matmul"):
+            raise ValueError("longitude must be 'fft' or 'matmul'")
+        self.longitude = longitude
+        flags = PLAN_DFT_MATMUL if longitude == "matmul" else 0
+        _check(lib().swsft_plan_create_ex(self.H, self.W, self.L, si, len(self.spins_in), so,
+                                          len(self.spins_out), self._code, flags,
+                                          ctypes.byref(h)),
+               "swsft_plan_create_ex")
         self._h = h
         self._ws = {}
         self.device = torch.device("cuda", torch.cuda.current_device())

@@ -16,7 +16,7 @@ def L():
 
 def test_exports_every_declared_function(L):
     names = S.header_functions()
-    assert len(names) == 18
+    assert len(names) == 19
     for n in names:
         assert hasattr(L, n), n
 
@@ -45,6 +45,18 @@ def _create(L, H, W, Lb, si, so, dtype=0, out=True):
 def test_plan_create_validation(L, args, status):
     assert _create(L, *args) == status
     assert L.swsft_last_error().decode() != ""
+
+
+def test_plan_create_flags(L):
+    a = (ctypes.c_int * 1)(0)
+    h = ctypes.c_void_p()
+    # unknown flag bits
+    assert L.swsft_plan_create_ex(16, 16, 8, a, 1, a, 1, 0, 4, ctypes.byref(h)) == S.E_INVALID
+    # a width that is not a power of two needs the DFT-matrix longitude stage
+    assert L.swsft_plan_create_ex(96, 96, 48, a, 1, a, 1, 0, 0, ctypes.byref(h)) == S.E_UNSUPPORTED
+    assert L.swsft_plan_create(96, 96, 48, a, 1, a, 1, 0, ctypes.byref(h)) == S.E_UNSUPPORTED
+    # grids above 32 take whole latitude tiles of 32 rows
+    assert L.swsft_plan_create_ex(48, 48, 24, a, 1, a, 1, 0, 1, ctypes.byref(h)) == S.E_UNSUPPORTED
 
 
 def test_plan_create_bad_dtype_and_null_out(L):
