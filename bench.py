@@ -209,6 +209,9 @@ def main(argv=None):
                     help="also run a plain 1 GiB device copy (for counter calibration)")
     ap.add_argument("--table", action="store_true",
                     help="measure every workload and print markdown table rows")
+    ap.add_argument("--dft-vs-fft", action="store_true",
+                    help="compare the FFT and the DFT-matrix forward longitude stages at "
+                         "256^2, 512^2 and 768^2 (B = 1, spins {0,1}, C = 256, bf16)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic_<workload>.json from two counter runs and exit")
     args = ap.parse_args(argv)
@@ -228,6 +231,13 @@ def main(argv=None):
         return 1
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    if args.dft_vs_fft:
+        print(DFT_HEAD)
+        for H in (256, 512, 768):
+            for method in ("fft", "matmul"):
+                print(dft_vs_fft_row(H, method, min(args.steps, 50), min(args.warmup, 5)),
+                      flush=True)
+        return 0
     if args.table:
         from paper_2306_05420_amd import synthetic as syn
         print(TABLE_HEAD)
@@ -452,6 +462,60 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
                       for hi, ho in ((w.H, w.H), (2 * w.H, w.H))}
     plan.close()
     return r
+
+
+DFT_HEAD = ("| grid | forward longitude stage | longitude µs | GB/s | DFT-matmul TFLOP/s | "
+            "% bf16 peak | whole forward transform µs | same GEMM in torch.matmul µs |\n"
+            "|---|---|---|---|---|---|---|---|")
+
+
+def dft_vs_fft_row(H: int, method: str, steps: int, warmup: int) -> str:
+    """Forward transform of one batch item (spins {0,1}, C = 256, bf16) on an
+    H x H grid with bandlimit H/2, with the register-FFT or the DFT-matrix
+    longitude stage: the longitude stage alone (HIP events) and the whole
+    swsft_forward.  The FFT route takes powers of two up to 512 only."""
+    import torch
+
+    from paper_2306_05420_amd import swsft as S
+    from paper_2306_05420_amd import synthetic as syn
+
+    B, spins, C, L = 1, (0, 1), 256, H // 2
+    pow2 = H & (H - 1) == 0 and H <= 512
+    if method == "fft" and not pow2:
+        return f"| {H}² | register FFT | — (no FFT of this width) | — | — | — | — | — |"
+    plan = S.Plan(H, H, L, spins, spins, "bf16", longitude=method)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(H)
+    x = torch.view_as_real(syn.torch_complex_normal(gen, (B, 2, C, H, H))).to(
+        torch.bfloat16).contiguous()
+    coef = plan.forward(x)
+    t = _time_calls(lambda: plan.forward(x, coef), steps, warmup)
+    plan.stage_timing(True)
+    for _ in range(steps):
+        plan.forward(x, coef)
+    torch.cuda.synchronize()
+    st = plan.stage_times()
+    plan.stage_timing(False)
+    plan.close()
+    lon = st["dft_fwd"][0] / st["dft_fwd"][1] / 1e3  # seconds
+    M = 2 * L - 1
+    lib = "—"
+    if method == "matmul":
+        # the same real GEMM [rows x 2W] . [2W x 2M] through the vendor library
+        # (row-major output, without the scatter into the K-tiled spectrum)
+        Ft = torch.randn((2 * H, 2 * M), generator=gen, device="cuda").to(torch.bfloat16)
+        xm = x.view(B * 2 * C * H, 2 * H)
+        out = torch.empty((xm.shape[0], 2 * M), dtype=torch.bfloat16, device="cuda")
+        lib = f"{_time_calls(lambda: torch.matmul(xm, Ft, out=out), steps, warmup) * 1e6:.1f}"
+        del Ft, out
+    rows = B * 2 * C * H
+    byt = rows * H * 4 + 2 * M * B * C * H * 4        # x in, X out (bf16 pairs)
+    fl = 2.0 * rows * (2 * H) * (2 * M)                # the dense real GEMM
+    name = "register FFT (VALU)" if method == "fft" else "DFT matrix (MFMA bf16)"
+    tf = f"{fl / lon / 1e12:.0f}" if method == "matmul" else "—"
+    pk = f"{100 * fl / lon / 1e12 / PEAK_TFLOPS['bf16']:.1f}" if method == "matmul" else "—"
+    return (f"| {H}² | {name} | {lon * 1e6:.1f} | {byt / lon / 1e9:.0f} | {tf} | {pk} | "
+            f"{t * 1e6:.1f} | {lib} |")
 
 
 def block_flops(w, H_in: int, H_out: int) -> int:
