@@ -16,6 +16,8 @@ ICML 2023):
   are products of spin-weighted harmonic coefficients; Fig. 2's "*K");
 * the phase-collapse nonlinearity (Method, "Phase collapse nonlinearity");
 * the backward pass of the layer (adjoints of the linear maps above);
+* the transforms by the paper's Wigner-Delta route, eqs. (4)-(6), with and
+  without the J / G symmetries;
 * spectral batch normalization, spectral pooling and the residual block with
   its skip connection between Fourier coefficients (Method, "Spectral batch
   normalization", "Spectral pooling and efficient residual block", Fig. 2);
@@ -61,6 +63,9 @@ __all__ = [
     "mix_adjoint",
     "filter_grad",
     "conv_backward",
+    "delta_matrix",
+    "forward_delta",
+    "inverse_delta",
     "phase_collapse",
     "spectral_batch_norm",
     "residual_block",
@@ -491,6 +496,102 @@ def conv_backward(x: np.ndarray, K: np.ndarray, grad_y: np.ndarray, L: int, spin
     grad_K = filter_grad(g_out, a, spins_in, spins_out)
     grad_x = forward_adjoint(mix_adjoint(g_out, K, spins_in, spins_out), H, W, spins_in)
     return grad_x, grad_K
+
+
+# --------------------------------------------------------------------------
+# The Wigner-Delta route of eqs. (4)-(6) (Background, "Computing generalized
+# convolutions"): Delta = d(pi/2) and Fourier sums in theta
+# --------------------------------------------------------------------------
+
+def delta_matrix(L: int) -> np.ndarray:
+    """D[l, m' + L - 1, m + L - 1] = Delta^l_{m'm} = d^l_{m'm}(pi/2), zero
+    where |m'| > l or |m| > l.
+    Pinned by: the Delta identities of eqs. (4) and (6) against the
+    harmonics and the symmetry used by eq. (5) (tests/test_oracle_wigner.py,
+    tests/test_oracle_delta.py)."""
+    D = np.zeros((L, 2 * L - 1, 2 * L - 1))
+    for mp in range(-(L - 1), L):
+        for m in range(-(L - 1), L):
+            D[:, mp + L - 1, m + L - 1] = wigner_d(L, mp, m, np.pi / 2)[:, 0]
+    return D
+
+
+def forward_delta(x: np.ndarray, L: int, spins, symmetric: bool = False) -> np.ndarray:
+    """Forward SWSFT by eq. (4):
+        a_lm = (-1)^s i^(m+s) N_l sum_{m'=-l..l} Delta^l_{m'm} Delta^l_{m'(-s)} I_{m'm},
+        I_{m'm} = sum_j q_j e^{-i m' theta_j} X_m(theta_j),
+    with X_m(theta_j) = sum_k x e^{-i m phi_k} and q_j = (2 pi / W) w_j, so that
+    I is the quadrature of eq. (2)'s inner product on the grid.  With
+    `symmetric`, eq. (5): the sum runs over m' = 0..l with
+    J_{m'm} = I_{m'm} + (-1)^(m+s) I_{-m'm} (m' > 0), J_{0m} = I_{0m}.
+    Pinned by: equality with `forward` on non-band-limited input
+    (tests/test_oracle_delta.py)."""
+    x = np.asarray(x, dtype=np.complex128)
+    B, S, C, H, W = x.shape
+    spins = list(spins)
+    theta, _ = grid(H, W)
+    q = (2.0 * np.pi / W) * dh_weights(H)
+    E = _lon_dft_matrix(W, L, -1)
+    X = (x.reshape(-1, W) @ E).reshape(B, S, C, H, 2 * L - 1)     # [..., j, m]
+    mp = _orders(L)
+    Eth = q[None, :] * np.exp(-1j * np.outer(mp, theta))           # [m', j]
+    I = np.einsum("pj,bscjm->bscpm", Eth, X)                        # [b, s, c, m', m]
+    D = delta_matrix(L)
+    coef = np.zeros((L * L, B, S, C), dtype=np.complex128)
+    for si, s in enumerate(spins):
+        for m in range(-(L - 1), L):
+            ph = ((-1.0) ** s) * (1j ** ((m + s) % 4))
+            for l in range(max(abs(m), abs(s)), L):
+                if symmetric:
+                    acc = 0.0
+                    for p in range(0, l + 1):
+                        if p == 0:
+                            J = I[:, si, :, L - 1, m + L - 1]
+                        else:
+                            J = (I[:, si, :, L - 1 + p, m + L - 1]
+                                 + (-1.0) ** (m + s) * I[:, si, :, L - 1 - p, m + L - 1])
+                        acc = acc + D[l, L - 1 + p, m + L - 1] * D[l, L - 1 + p, -s + L - 1] * J
+                else:
+                    idx = np.arange(L - 1 - l, L + l)                 # m' = -l..l
+                    w = D[l, idx, m + L - 1] * D[l, idx, -s + L - 1]
+                    acc = np.einsum("p,bcp->bc", w, I[:, si, :, idx, m + L - 1].transpose(1, 2, 0))
+                coef[coef_index(l, m), :, si, :] = ph * _norm(l) * acc
+    return coef
+
+
+def inverse_delta(coef: np.ndarray, H: int, W: int, spins, symmetric: bool = False) -> np.ndarray:
+    """Inverse SWSFT by eq. (6):
+        f(theta, phi) = sum_{m'} sum_m e^{i m' theta} e^{i m phi} G_{m'm},
+        G_{m'm} = (-1)^s i^(m+s) sum_l N_l Delta^l_{(-m')(-s)} Delta^l_{(-m')m} a_lm,
+    evaluated on the grid.  With `symmetric`, only G_{m'm} for m' >= 0 is
+    computed and G_{(-m')m} = (-1)^(m+s) G_{m'm} fills the rest.
+    Pinned by: equality with `inverse` (tests/test_oracle_delta.py)."""
+    coef = np.asarray(coef, dtype=np.complex128)
+    L2, B, S, C = coef.shape
+    L = int(round(math.sqrt(L2)))
+    spins = list(spins)
+    theta, _ = grid(H, W)
+    D = delta_matrix(L)
+    mps = _orders(L)
+    Y = np.zeros((B, S, C, H, 2 * L - 1), dtype=np.complex128)      # [..., j, m]
+    for si, s in enumerate(spins):
+        for m in range(-(L - 1), L):
+            lo = max(abs(m), abs(s))
+            if lo >= L:
+                continue
+            ph = ((-1.0) ** s) * (1j ** ((m + s) % 4))
+            G = np.zeros((2 * L - 1, B, C), dtype=np.complex128)
+            for p in (range(0, L) if symmetric else mps):
+                for l in range(max(lo, abs(p)), L):
+                    G[p + L - 1] += (_norm(l) * D[l, -p + L - 1, -s + L - 1]
+                                     * D[l, -p + L - 1, m + L - 1]) * coef[coef_index(l, m), :, si, :]
+            if symmetric:
+                for p in range(1, L):
+                    G[L - 1 - p] = (-1.0) ** (m + s) * G[L - 1 + p]
+            Eth = np.exp(1j * np.outer(theta, mps))                  # [j, m']
+            Y[:, si, :, :, m + L - 1] = ph * np.einsum("jp,pbc->bcj", Eth, G)
+    E = _lon_dft_matrix(W, L, +1)                                    # [k, m]
+    return (Y.reshape(-1, 2 * L - 1) @ E.T).reshape(B, S, C, H, W)
 
 
 # --------------------------------------------------------------------------
