@@ -212,6 +212,9 @@ def main(argv=None):
     ap.add_argument("--dft-vs-fft", action="store_true",
                     help="compare the FFT and the DFT-matrix forward longitude stages at "
                          "256^2, 512^2 and 768^2 (B = 1, spins {0,1}, C = 256, bf16)")
+    ap.add_argument("--delta-routes", action="store_true",
+                    help="compare the latitude stages: direct d(theta) tables vs the Wigner-Delta "
+                         "route with and without its symmetries (wx128 and wx256 workloads)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic_<workload>.json from two counter runs and exit")
     args = ap.parse_args(argv)
@@ -231,6 +234,13 @@ def main(argv=None):
         return 1
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    if args.delta_routes:
+        print(DELTA_HEAD)
+        for name in ("wx128", "wx256"):
+            for route in ("direct", "delta_sym", "delta"):
+                print(delta_route_row(name, route, min(args.steps, 50), min(args.warmup, 5)),
+                      flush=True)
+        return 0
     if args.dft_vs_fft:
         print(DFT_HEAD)
         for H in (256, 512, 768):
@@ -462,6 +472,54 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
                       for hi, ho in ((w.H, w.H), (2 * w.H, w.H))}
     plan.close()
     return r
+
+
+DELTA_HEAD = ("| workload | latitude route | swsft_forward µs | swsft_inverse µs | layer µs | "
+              "latitude-stage µs (fwd + inv, incl. theta GEMMs) | vs direct (layer) |\n"
+              "|---|---|---|---|---|---|---|")
+_DELTA_BASE = {}
+
+
+def delta_route_row(name: str, route: str, steps: int, warmup: int) -> str:
+    """Forward, inverse and layer times of a workload with the latitude stages
+    by the direct d(theta) tables or by the Wigner-Delta route (eqs. (4)-(6))
+    without ("delta") or with ("delta_sym") its J / G symmetries."""
+    import torch
+
+    from paper_2306_05420_amd import swsft as S
+    from paper_2306_05420_amd import synthetic as syn
+
+    w = syn.workload(name)
+    plan = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_out, w.dtype, latitude=route)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(w.seed)
+
+    def storage(t):
+        return torch.view_as_real(t).to(torch.bfloat16).contiguous() if w.dtype == "bf16" else t
+
+    x = storage(syn.torch_complex_normal(gen, (w.B, len(w.spins_in), w.C_in, w.H, w.W)))
+    K = storage(syn.torch_random_filters(gen, w.L, w.spins_in, w.C_in, w.spins_out, w.C_out,
+                                         w.filter_var))
+    a = storage(syn.torch_random_coefficients(gen, w.L, w.B, w.spins_out, w.C_out, 1.0))
+    coef = plan.forward(x)
+    y = plan.inverse(a)
+    yc = plan.conv(x, K)
+    t_f = _time_calls(lambda: plan.forward(x, coef), steps, warmup)
+    t_i = _time_calls(lambda: plan.inverse(a, y), steps, warmup)
+    t_c = _time_calls(lambda: plan.conv(x, K, yc), steps, warmup)
+    plan.stage_timing(True)
+    for _ in range(steps):
+        plan.conv(x, K, yc)
+    torch.cuda.synchronize()
+    st = plan.stage_times()
+    plan.stage_timing(False)
+    plan.close()
+    lat = sum(st[k][0] for k in ("lat_fwd", "lat_inv", "delta_theta") if k in st) * 1e3 / steps
+    if route == "direct":
+        _DELTA_BASE[name] = t_c
+    rel = f"{t_c / _DELTA_BASE[name]:.2f}×" if name in _DELTA_BASE else "—"
+    return (f"| {name} | {route} | {t_f * 1e6:.1f} | {t_i * 1e6:.1f} | {t_c * 1e6:.1f} | "
+            f"{lat:.1f} | {rel} |")
 
 
 DFT_HEAD = ("| grid | forward longitude stage | longitude µs | GB/s | DFT-matmul TFLOP/s | "

@@ -80,7 +80,16 @@ typedef enum {
    * "FFT vs DFT", Table 8) instead of the register FFT.  Also admits any even
    * W for swsft_forward; calls that need the inverse longitude stage then
    * return SWSFT_E_UNSUPPORTED unless W is a power of two <= 512. */
-  SWSFT_PLAN_DFT_MATMUL = 1
+  SWSFT_PLAN_DFT_MATMUL = 1,
+  /* Latitude stages by the paper's Wigner-Delta route (Background, eqs.
+   * (4)-(6)): a Fourier sum in theta on the grid (quadrature weights folded
+   * in) followed by the Delta^l_{m'm} Delta^l_{m'(-s)} contraction, both as
+   * MFMA GEMMs, for swsft_forward, swsft_inverse and spin_sph_conv_forward.
+   * DELTA sums all m' in [-l, l] (eq. (4), eq. (6) for every G_{m'm});
+   * DELTA_SYM uses the J / G symmetries (eq. (5): m' >= 0 only).  Needs L a
+   * multiple of 32; not with the backward pass or the residual block. */
+  SWSFT_PLAN_DELTA = 2,
+  SWSFT_PLAN_DELTA_SYM = 4
 } swsft_plan_flags;
 
 typedef enum {

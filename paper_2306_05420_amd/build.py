@@ -21,7 +21,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libswsft.so")
 INCLUDE = os.path.join(os.path.dirname(PKG), "include")
 
-SOURCES = ["tables.hip", "dft.hip", "dft_mm.hip", "gemm.hip", "mix_dma.hip", "lat_dma.hip",
+SOURCES = ["tables.hip", "delta.hip", "dft.hip", "dft_mm.hip", "gemm.hip", "mix_dma.hip", "lat_dma.hip",
            "phase_collapse.hip", "batch_norm.hip", "backward.hip", "swsft_api.cpp"]
 ARCH = "gfx950"
 

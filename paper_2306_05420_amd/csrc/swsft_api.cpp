@@ -75,14 +75,18 @@ size_t ws_need(const Plan& p, int op, int B, int Cin, int Cout) {
   const size_t e = p.elem;
   switch (op) {
     case SWSFT_OP_FORWARD:
-      return align_up(swsft::xy_elems(p, p.n_in, B, Cin) * e);
+      return align_up(swsft::xy_elems(p, p.n_in, B, Cin) * e) +
+             align_up(swsft::delta_elems(p, p.n_in, B, Cin) * e);
     case SWSFT_OP_INVERSE:
-      return align_up(swsft::xy_elems(p, p.n_out, B, Cout) * e);
+      return align_up(swsft::xy_elems(p, p.n_out, B, Cout) * e) +
+             align_up(swsft::delta_elems(p, p.n_out, B, Cout) * e);
     case SWSFT_OP_CONV: {
       size_t xin = swsft::xy_elems(p, p.n_in, B, Cin), xout = swsft::xy_elems(p, p.n_out, B, Cout);
+      size_t din = swsft::delta_elems(p, p.n_in, B, Cin), dout = swsft::delta_elems(p, p.n_out, B, Cout);
       return align_up((xin > xout ? xin : xout) * e) +
              align_up(swsft::coef_elems(p, p.n_in, B, Cin) * e) +
-             align_up(swsft::coef_elems(p, p.n_out, B, Cout) * e);
+             align_up(swsft::coef_elems(p, p.n_out, B, Cout) * e) +
+             align_up((din > dout ? din : dout) * e);
     }
     case SWSFT_OP_CONV_BACKWARD: {
       size_t xin = swsft::xy_elems(p, p.n_in, B, Cin), xout = swsft::xy_elems(p, p.n_out, B, Cout);
@@ -186,6 +190,10 @@ void free_plan(Plan* p) {
   if (p->tab_bwd_syn) (void)hipFree(p->tab_bwd_syn);
   if (p->tab_bwd_ana) (void)hipFree(p->tab_bwd_ana);
   if (p->dft_mat) (void)hipFree(p->dft_mat);
+  if (p->delta_theta_fwd) (void)hipFree(p->delta_theta_fwd);
+  if (p->delta_theta_inv) (void)hipFree(p->delta_theta_inv);
+  if (p->delta_fwd) (void)hipFree(p->delta_fwd);
+  if (p->delta_inv) (void)hipFree(p->delta_inv);
   if (p->twiddle) (void)hipFree(p->twiddle);
   if (p->ev) {
     for (int i = 0; i < 2 * swsft::kMaxTimedLaunches; ++i)
@@ -216,7 +224,8 @@ const char* swsft_last_error(void) { return g_last_error; }
 const char* swsft_stage_name(int stage) {
   static const char* names[swsft::kNumStages] = {"dft_fwd", "lat_fwd", "mix", "lat_inv",
                                                  "dft_inv", "phase_collapse", "tables",
-                                                 "filter_grad", "filter_adjoint", "batch_norm"};
+                                                 "filter_grad", "filter_adjoint", "batch_norm",
+                                                 "delta_theta"};
   if (stage < 0 || stage >= swsft::kNumStages) return "";
   return names[stage];
 }
@@ -240,7 +249,12 @@ swsft_status swsft_plan_create_ex(int H, int W, int L, const int* spins_in, int 
     return fail(SWSFT_E_INVALID, "dtype %d is not a swsft_dtype", dtype);
   SWSFT_TRY(check_spins(spins_in, n_spins_in, L, "spins_in"));
   SWSFT_TRY(check_spins(spins_out, n_spins_out, L, "spins_out"));
-  if (flags & ~(unsigned)SWSFT_PLAN_DFT_MATMUL) return fail(SWSFT_E_INVALID, "unknown flags %#x", flags);
+  const unsigned known = SWSFT_PLAN_DFT_MATMUL | SWSFT_PLAN_DELTA | SWSFT_PLAN_DELTA_SYM;
+  if (flags & ~known) return fail(SWSFT_E_INVALID, "unknown flags %#x", flags);
+  if ((flags & SWSFT_PLAN_DELTA) && (flags & SWSFT_PLAN_DELTA_SYM))
+    return fail(SWSFT_E_INVALID, "SWSFT_PLAN_DELTA and SWSFT_PLAN_DELTA_SYM exclude each other");
+  if ((flags & (SWSFT_PLAN_DELTA | SWSFT_PLAN_DELTA_SYM)) && (L % 32 != 0 || H % 32 != 0))
+    return fail(SWSFT_E_UNSUPPORTED, "the Delta route needs L and H multiples of 32 (L = %d)", L);
   const bool fft_ok = is_pow2(W) && W <= 512;
   if (H > 32 && H % 32 != 0)
     return fail(SWSFT_E_UNSUPPORTED, "H = %d: grids above 32 take whole latitude tiles of 32 rows", H);
@@ -296,6 +310,30 @@ swsft_status swsft_plan_create_ex(int H, int W, int L, const int* spins_in, int 
     delete static_cast<swsft_plan_s*>(p);
     return hip_fail(e, "table generation");
   }
+  if (swsft::is_delta(*p)) {
+    const size_t e1 = swsft::delta_fwd_theta_elems(*p) * p->elem;
+    const size_t e2 = swsft::delta_inv_theta_elems(*p) * p->elem;
+    const size_t e3 = (size_t)p->n_in * swsft::delta_fwd_table_elems(*p) * p->elem;
+    const size_t e4 = (size_t)p->n_out * swsft::delta_inv_table_elems(*p) * p->elem;
+    if (hipMalloc(&p->delta_theta_fwd, e1) != hipSuccess ||
+        hipMalloc(&p->delta_theta_inv, e2) != hipSuccess ||
+        hipMalloc(&p->delta_fwd, e3) != hipSuccess || hipMalloc(&p->delta_inv, e4) != hipSuccess) {
+      (void)hipGetLastError();
+      free_plan(p);
+      delete static_cast<swsft_plan_s*>(p);
+      return fail(SWSFT_E_ALLOC, "hipMalloc of %zu Delta-route table bytes failed", e1 + e2 + e3 + e4);
+    }
+    if ((e = hipMemset(p->delta_theta_fwd, 0, e1)) != hipSuccess ||
+        (e = hipMemset(p->delta_theta_inv, 0, e2)) != hipSuccess ||
+        (e = hipMemset(p->delta_fwd, 0, e3)) != hipSuccess ||
+        (e = hipMemset(p->delta_inv, 0, e4)) != hipSuccess ||
+        (e = swsft::launch_delta_tables(*p, nullptr)) != hipSuccess ||
+        (e = hipDeviceSynchronize()) != hipSuccess) {
+      free_plan(p);
+      delete static_cast<swsft_plan_s*>(p);
+      return hip_fail(e, "Delta-route table generation");
+    }
+  }
   if (flags & SWSFT_PLAN_DFT_MATMUL) {
     const size_t db = (size_t)2 * p->M * 2 * W * p->elem;
     if (hipMalloc(&p->dft_mat, db) != hipSuccess) {
@@ -330,6 +368,58 @@ size_t swsft_workspace_bytes(swsft_plan p, int op, int B, int C_in, int C_out) {
   return ws_need(*p, op, B, C_in, C_out);
 }
 
+namespace {
+
+// The forward transform x -> coef: longitude stage into X, then the latitude
+// stage directly (d tables) or by the Delta route (theta GEMM into D, then
+// the Delta contraction by the latitude kernels on a plan view whose "grid"
+// is the R rows of D).
+swsft_status forward_stages(Plan& p, int B, int C, const void* x, void* X, void* D, void* coef,
+                            hipStream_t st) {
+  SWSFT_TRY(run_stage(p, swsft::kStageDftFwd, st, "dft_fwd",
+                      [&] { return swsft::launch_dft_fwd(p, p.n_in, B, C, x, X, st); }));
+  if (!swsft::is_delta(p))
+    return run_stage(p, swsft::kStageLatFwd, st, "lat_fwd",
+                     [&] { return swsft::launch_lat_fwd(p, B, C, X, coef, st); });
+  SWSFT_TRY(run_stage(p, swsft::kStageDeltaTheta, st, "delta_theta",
+                      [&] { return swsft::launch_delta_theta_fwd(p, B, C, X, D, st); }));
+  Plan v = p;
+  v.H = v.Hp = swsft::delta_rows(p);
+  v.JT = 32;
+  v.tab_fwd = p.delta_fwd;
+  return run_stage(p, swsft::kStageLatFwd, st, "lat_fwd",
+                   [&] { return swsft::launch_lat_fwd(v, B, C, D, coef, st); });
+}
+
+// The inverse transform coef -> y (see forward_stages).
+swsft_status inverse_stages(Plan& p, int B, int C, const void* coef, void* Y, void* D, void* y,
+                            hipStream_t st) {
+  if (!swsft::is_delta(p)) {
+    SWSFT_TRY(run_stage(p, swsft::kStageLatInv, st, "lat_inv",
+                        [&] { return swsft::launch_lat_inv(p, B, C, coef, Y, st); }));
+  } else {
+    Plan v = p;
+    v.H = v.Hp = swsft::delta_rows(p);
+    v.JT = 32;
+    v.tab_inv = p.delta_inv;
+    SWSFT_TRY(run_stage(p, swsft::kStageLatInv, st, "lat_inv",
+                        [&] { return swsft::launch_lat_inv(v, B, C, coef, D, st); }));
+    SWSFT_TRY(run_stage(p, swsft::kStageDeltaTheta, st, "delta_theta",
+                        [&] { return swsft::launch_delta_theta_inv(p, B, C, D, Y, st); }));
+  }
+  return run_stage(p, swsft::kStageDftInv, st, "dft_inv",
+                   [&] { return swsft::launch_dft_inv(p, p.n_out, B, C, Y, y, st); });
+}
+
+swsft_status reject_delta(const Plan& p, const char* what) {
+  if (swsft::is_delta(p))
+    return fail(SWSFT_E_UNSUPPORTED, "%s has no Delta-route variant: use a plan without "
+                "SWSFT_PLAN_DELTA / SWSFT_PLAN_DELTA_SYM", what);
+  return SWSFT_OK;
+}
+
+}  // namespace
+
 swsft_status swsft_forward(swsft_plan p, int B, int C, const void* x, void* coef, void* ws,
                            size_t ws_bytes, void* stream) {
   g_last_error[0] = 0;
@@ -340,12 +430,9 @@ swsft_status swsft_forward(swsft_plan p, int B, int C, const void* x, void* coef
   SWSFT_TRY(check_ws(*p, SWSFT_OP_FORWARD, B, C, 1, ws, ws_bytes));
   SWSFT_TRY(check_device(*p));
   hipStream_t st = static_cast<hipStream_t>(stream);
-  void* X = ws;
-  SWSFT_TRY(run_stage(*p, swsft::kStageDftFwd, st, "dft_fwd",
-                      [&] { return swsft::launch_dft_fwd(*p, p->n_in, B, C, x, X, st); }));
-  SWSFT_TRY(run_stage(*p, swsft::kStageLatFwd, st, "lat_fwd",
-                      [&] { return swsft::launch_lat_fwd(*p, B, C, X, coef, st); }));
-  return SWSFT_OK;
+  char* X = static_cast<char*>(ws);
+  void* D = X + align_up(swsft::xy_elems(*p, p->n_in, B, C) * p->elem);
+  return forward_stages(*p, B, C, x, X, D, coef, st);
 }
 
 swsft_status swsft_inverse(swsft_plan p, int B, int C, const void* coef, void* y, void* ws,
@@ -359,12 +446,9 @@ swsft_status swsft_inverse(swsft_plan p, int B, int C, const void* coef, void* y
   SWSFT_TRY(check_ws(*p, SWSFT_OP_INVERSE, B, 1, C, ws, ws_bytes));
   SWSFT_TRY(check_device(*p));
   hipStream_t st = static_cast<hipStream_t>(stream);
-  void* Y = ws;
-  SWSFT_TRY(run_stage(*p, swsft::kStageLatInv, st, "lat_inv",
-                      [&] { return swsft::launch_lat_inv(*p, B, C, coef, Y, st); }));
-  SWSFT_TRY(run_stage(*p, swsft::kStageDftInv, st, "dft_inv",
-                      [&] { return swsft::launch_dft_inv(*p, p->n_out, B, C, Y, y, st); }));
-  return SWSFT_OK;
+  char* Y = static_cast<char*>(ws);
+  void* D = Y + align_up(swsft::xy_elems(*p, p->n_out, B, C) * p->elem);
+  return inverse_stages(*p, B, C, coef, Y, D, y, st);
 }
 
 swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, const void* x,
@@ -396,19 +480,13 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
   void* coef = w;
   w += align_up(swsft::coef_elems(*p, p->n_in, B, C_in) * p->elem);
   void* coef2 = w;
-  SWSFT_TRY(run_stage(*p, swsft::kStageDftFwd, st, "dft_fwd",
-                      [&] { return swsft::launch_dft_fwd(*p, p->n_in, B, C_in, x, XY, st); }));
-  SWSFT_TRY(run_stage(*p, swsft::kStageLatFwd, st, "lat_fwd",
-                      [&] { return swsft::launch_lat_fwd(*p, B, C_in, XY, coef, st); }));
+  w += align_up(swsft::coef_elems(*p, p->n_out, B, C_out) * p->elem);
+  void* D = w;
+  SWSFT_TRY(forward_stages(*p, B, C_in, x, XY, D, coef, st));
   SWSFT_TRY(run_stage(*p, swsft::kStageMix, st, "mix", [&] {
     return swsft::launch_mix(*p, B, C_in, C_out, coef, filters, coef2, st);
   }));
-  SWSFT_TRY(run_stage(*p, swsft::kStageLatInv, st, "lat_inv",
-                      [&] { return swsft::launch_lat_inv(*p, B, C_out, coef2, XY, st); }));
-  SWSFT_TRY(run_stage(*p, swsft::kStageDftInv, st, "dft_inv", [&] {
-    return swsft::launch_dft_inv(*p, p->n_out, B, C_out, XY, y, st);
-  }));
-  return SWSFT_OK;
+  return inverse_stages(*p, B, C_out, coef2, XY, D, y, st);
 }
 
 swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, const void* x,
@@ -422,6 +500,7 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
     return fail(SWSFT_E_INVALID, "neither grad_x nor grad_filters requested");
   SWSFT_TRY(check_ptr(grad_y, "grad_y"));
   SWSFT_TRY(check_inverse_stage(*p));
+  SWSFT_TRY(reject_delta(*p, "spin_sph_conv_backward"));
   if (grad_filters != nullptr) {
     SWSFT_TRY(check_ptr(x, "x"));
     SWSFT_TRY(check_ptr(grad_filters, "grad_filters"));
@@ -623,6 +702,8 @@ swsft_status spin_sph_residual_block_forward(swsft_plan p_in, swsft_plan p_out, 
   }
   if (!same) return fail(SWSFT_E_INVALID, "both plans must map the same spin list to itself");
   SWSFT_TRY(check_inverse_stage(po));
+  SWSFT_TRY(reject_delta(pi, "spin_sph_residual_block_forward"));
+  SWSFT_TRY(reject_delta(po, "spin_sph_residual_block_forward"));
   if (!has0) return fail(SWSFT_E_INVALID, "the spin list must contain spin 0");
   if (C > swsft::phase_collapse_max_channels(S))
     return fail(SWSFT_E_UNSUPPORTED, "C = %d exceeds %d channels for %d spins", C,

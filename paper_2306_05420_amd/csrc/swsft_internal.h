@@ -25,7 +25,8 @@ enum Stage : int {
   kStageFilterGrad = 7,
   kStageFilterAdjoint = 8,
   kStageBatchNorm = 9,
-  kNumStages = 10
+  kStageDeltaTheta = 10,
+  kNumStages = 11
 };
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
@@ -54,6 +55,12 @@ struct Plan {
   // longitude stage is a dense DFT GEMM against dft_mat [2M][2W]
   unsigned flags = 0;
   void* dft_mat = nullptr;
+  // Wigner-Delta route (SWSFT_PLAN_DELTA / SWSFT_PLAN_DELTA_SYM): theta tables
+  // and Delta tables, layouts in delta.hip
+  void* delta_theta_fwd = nullptr;
+  void* delta_theta_inv = nullptr;
+  void* delta_fwd = nullptr;  // [n_in][M][L][R]
+  void* delta_inv = nullptr;  // [n_out][M][R][Lp]
   bool fft_ok = true;  // W is a size of the register FFT (a power of two <= 512)
   // stage timing
   bool timing = false;
@@ -91,6 +98,24 @@ hipError_t launch_dft_fwd(const Plan& p, int S, int B, int C, const void* x, voi
 hipError_t launch_dft_fwd_matmul(const Plan& p, int S, int B, int C, const void* x, void* X,
                                  hipStream_t st);
 hipError_t launch_dft_matrix(const Plan& p, hipStream_t st);
+// the Wigner-Delta route (delta.hip): R = L rows (with the symmetries) or 2L
+int delta_rows(const Plan& p);
+size_t delta_fwd_theta_elems(const Plan& p);
+size_t delta_inv_theta_elems(const Plan& p);
+size_t delta_fwd_table_elems(const Plan& p);
+size_t delta_inv_table_elems(const Plan& p);
+hipError_t launch_delta_tables(const Plan& p, hipStream_t st);
+hipError_t launch_delta_theta_fwd(const Plan& p, int B, int C, const void* X, void* CS,
+                                  hipStream_t st);
+hipError_t launch_delta_theta_inv(const Plan& p, int B, int C, const void* G, void* Y,
+                                  hipStream_t st);
+inline bool is_delta(const Plan& p) {
+  return (p.flags & (SWSFT_PLAN_DELTA | SWSFT_PLAN_DELTA_SYM)) != 0;
+}
+// [S][M][R/32][2 B C][32] intermediate of the Delta route (0 without it)
+inline size_t delta_elems(const Plan& p, int S, int B, int C) {
+  return is_delta(p) ? (size_t)S * p.M * delta_rows(p) * 2 * (size_t)B * C : 0;
+}
 // Y [S][M][H/JT][B*C][2][JT] -> y [B][S][C][H][W]
 hipError_t launch_dft_inv(const Plan& p, int S, int B, int C, const void* Y, void* y,
                           hipStream_t st);

@@ -15,6 +15,7 @@
 // One thread per (spin, m, j) runs the three-term recurrence in l from the
 // single-term seed at l0 = max(|m|, |s|).
 #include "swsft_internal.h"
+#include "wigner.h"
 
 namespace swsft {
 namespace {
@@ -28,27 +29,6 @@ __device__ __forceinline__ __bf16 to_storage<__bf16>(double v) {
   // double -> float is exact enough here (|v| <= 1, relative 2^-24), then
   // round-to-nearest-even to bfloat16.
   return (__bf16)(float)v;
-}
-
-// d^{l0}_{m n}(theta) at l0 = max(|m|, |n|): sqrt(C(2 l0, a)) c^a s^b times a
-// sign, c = cos(theta/2), s = sin(theta/2), a + b = 2 l0.  Evaluated as a
-// running product so no factorial or power is formed on its own.
-__device__ double wigner_seed(int m, int n, double c, double s) {
-  const int am = m < 0 ? -m : m, an = n < 0 ? -n : n;
-  const int l0 = am > an ? am : an;
-  int a, b;
-  bool neg;
-  if (am >= an) {
-    if (m == l0) { a = l0 + n; b = l0 - n; neg = (b & 1); }   // d_{l,n}
-    else         { a = l0 - n; b = l0 + n; neg = false; }     // d_{-l,n}
-  } else {
-    if (n == l0) { a = l0 + m; b = l0 - m; neg = false; }     // d_{m,l}
-    else         { a = l0 - m; b = l0 + m; neg = (b & 1); }   // d_{m,-l}
-  }
-  double v = 1.0;
-  for (int i = 1; i <= a; ++i) v *= c * sqrt((double)(b + i) / (double)i);
-  for (int i = 0; i < b; ++i) v *= s;
-  return neg ? -v : v;
 }
 
 // weighted: include (2 pi / W) w_j; l_rows: layout [l][Hp] per (s, m), else [Hp][Lp]

@@ -27,11 +27,11 @@ LIB_PATH = os.environ.get("SWSFT_LIBRARY") or os.path.join(_PKG, "libswsft.so")
 HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "swsft.h")
 
 OK, E_INVALID, E_UNSUPPORTED, E_ALLOC, E_HIP, E_WORKSPACE = range(6)
-PLAN_DFT_MATMUL = 1
+PLAN_DFT_MATMUL, PLAN_DELTA, PLAN_DELTA_SYM = 1, 2, 4
 F32, BF16 = 0, 1
 OP_FORWARD, OP_INVERSE, OP_CONV, OP_CONV_BACKWARD, OP_BATCH_NORM = 0, 1, 2, 3, 4
 STAGES = ("dft_fwd", "lat_fwd", "mix", "lat_inv", "dft_inv", "phase_collapse", "tables",
-          "filter_grad", "filter_adjoint", "batch_norm")
+          "filter_grad", "filter_adjoint", "batch_norm", "delta_theta")
 
 _lib = None
 
@@ -121,15 +121,18 @@ def _stream_handle(stream) -> int:
 
 class Plan:
     """A transform plan: grid H x W, bandlimit L, input/output spins, dtype,
-    and the forward longitude stage ("fft": register FFT; "matmul": dense DFT
-    matrix product on MFMA, which also takes widths that are not powers of two).
+    the forward longitude stage ("fft": register FFT; "matmul": dense DFT
+    matrix product on MFMA, which also takes widths that are not powers of two)
+    and the latitude stages ("direct": precomputed d^l(theta_j) tables;
+    "delta" / "delta_sym": the Wigner-Delta route of eqs. (4)-(6), without /
+    with the J and G symmetries).
 
     Owns the device tables built by swsft_plan_create; workspaces are cached
     per call shape (allocated through torch, i.e. by the caller of the C ABI).
     """
 
     def __init__(self, H: int, W: int, L: int, spins_in, spins_out, dtype: str = "f32",
-                 longitude: str = "fft"):
+                 longitude: str = "fft", latitude: str = "direct"):
         self.H, self.W, self.L = int(H), int(W), int(L)
         self.spins_in = tuple(int(s) for s in spins_in)
         self.spins_out = tuple(int(s) for s in spins_out)
@@ -143,7 +146,11 @@ class Plan:
         if longitude not in ("fft", "matmul"):
             raise ValueError("longitude must be 'fft' or 'matmul'")
         self.longitude = longitude
+        if latitude not in ("direct", "delta", "delta_sym"):
+            raise ValueError("latitude must be 'direct', 'delta' or 'delta_sym'")
+        self.latitude = latitude
         flags = PLAN_DFT_MATMUL if longitude == "matmul" else 0
+        flags |= {"direct": 0, "delta": PLAN_DELTA, "delta_sym": PLAN_DELTA_SYM}[latitude]
         _check(lib().swsft_plan_create_ex(self.H, self.W, self.L, si, len(self.spins_in), so,
                                           len(self.spins_out), self._code, flags,
                                           ctypes.byref(h)),

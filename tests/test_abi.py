@@ -50,8 +50,11 @@ def test_plan_create_validation(L, args, status):
 def test_plan_create_flags(L):
     a = (ctypes.c_int * 1)(0)
     h = ctypes.c_void_p()
-    # unknown flag bits
-    assert L.swsft_plan_create_ex(16, 16, 8, a, 1, a, 1, 0, 4, ctypes.byref(h)) == S.E_INVALID
+    # unknown flag bits; the two Delta routes together
+    assert L.swsft_plan_create_ex(16, 16, 8, a, 1, a, 1, 0, 8, ctypes.byref(h)) == S.E_INVALID
+    assert L.swsft_plan_create_ex(64, 64, 32, a, 1, a, 1, 0, 6, ctypes.byref(h)) == S.E_INVALID
+    # the Delta route takes L a multiple of 32
+    assert L.swsft_plan_create_ex(32, 32, 16, a, 1, a, 1, 0, 4, ctypes.byref(h)) == S.E_UNSUPPORTED
     # a width that is not a power of two needs the DFT-matrix longitude stage
     assert L.swsft_plan_create_ex(96, 96, 48, a, 1, a, 1, 0, 0, ctypes.byref(h)) == S.E_UNSUPPORTED
     assert L.swsft_plan_create(96, 96, 48, a, 1, a, 1, 0, ctypes.byref(h)) == S.E_UNSUPPORTED
