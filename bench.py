@@ -205,6 +205,9 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="wx256")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--forward-only", action="store_true",
+                    help="time the layer and the transforms only (no backward or graph replay "
+                         "timing): the launches that profiling runs attribute to the layer")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (for counter calibration)")
     ap.add_argument("--table", action="store_true",
@@ -257,7 +260,8 @@ def main(argv=None):
                 print(row, flush=True)
         return 0
 
-    r = measure(args.workload, args.steps, args.warmup, dev, args.copy_calibration)
+    r = measure(args.workload, args.steps, args.warmup, dev, args.copy_calibration,
+                extras=not args.forward_only)
     w = r["w"]
     out = {
         "metric": METRIC,
@@ -287,9 +291,10 @@ def main(argv=None):
         "stages": r["stages"],
         "roofline": r["roofline"],
         "transforms": r["transforms"],
-        "backward": r["backward"],
-        "graph": r["graph"],
     }
+    for k in ("backward", "graph"):
+        if k in r:
+            out[k] = r[k]
     if "stack2" in r:
         out["stack2"] = r["stack2"]
     if not args.no_cpu_baseline:
@@ -336,7 +341,8 @@ def _time_graph(fn, steps: int, warmup: int):
     return t
 
 
-def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = False) -> dict:
+def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = False,
+            extras: bool = True) -> dict:
     """Time one workload: the layer (with per-stage HIP events and the
     roofline of its dominant stage), the forward and inverse transforms alone,
     and for the molecule workload the two-layer stack with phase collapse."""
@@ -433,8 +439,11 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
                              "TFLOP/s": round(fl / t / 1e12, 2)}
     r = {"w": w, "value": 1.0 / t_layer, "ms_per_step": t_layer * 1e3,
          "tflops": useful / t_layer / 1e12, "useful": useful, "stages": stages,
-         "roofline": roof, "transforms": transforms,
-         "backward": measure_backward(plan, w, x, K, y, steps, warmup)}
+         "roofline": roof, "transforms": transforms}
+    if not extras:
+        plan.close()
+        return r
+    r["backward"] = measure_backward(plan, w, x, K, y, steps, warmup)
     # launch overhead removed: one layer call (and one backward call) per
     # replay of a captured graph
     gx = plan.empty(w.B, len(w.spins_in), w.C_in, w.H, w.W)
