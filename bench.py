@@ -396,19 +396,23 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
     useful = sum(v["flops"] for v in work.values())
     stages = {}
     for sname, (ms, n) in times.items():
-        avg_s = ms / 1e3 / n
-        rec = {"avg_us": round(avg_s * 1e6, 2), "launches": n}
+        # a stage may run as several launches per call (the inverse stages over
+        # batch ranges): avg_us is per launch, us_per_call per layer call
+        call_s = ms / 1e3 / steps
+        rec = {"avg_us": round(ms * 1e3 / n, 2), "launches_per_call": round(n / steps, 3),
+               "us_per_call": round(call_s * 1e6, 2)}
         wk = work.get(sname)
         if wk:
-            rec["GB/s"] = round(wk["bytes"] / avg_s / 1e9, 1)
-            rec["hbm_frac"] = round(wk["bytes"] / avg_s / 1e9 / HBM_PEAK_GBS, 4)
+            rec["GB/s"] = round(wk["bytes"] / call_s / 1e9, 1)
+            rec["hbm_frac"] = round(wk["bytes"] / call_s / 1e9 / HBM_PEAK_GBS, 4)
             if wk["flops"]:
-                rec["TFLOP/s"] = round(wk["flops"] / avg_s / 1e12, 2)
-                rec["mfma_frac"] = round(wk["flops"] / avg_s / 1e12 / PEAK_TFLOPS[w.dtype], 4)
+                rec["TFLOP/s"] = round(wk["flops"] / call_s / 1e12, 2)
+                rec["mfma_frac"] = round(wk["flops"] / call_s / 1e12 / PEAK_TFLOPS[w.dtype], 4)
         stages[sname] = rec
-    dom = max((k for k in stages if k in work), key=lambda k: stages[k]["avg_us"])
-    avg_s = stages[dom]["avg_us"] / 1e6
-    wk = work[dom]
+    dom = max((k for k in stages if k in work), key=lambda k: stages[k]["us_per_call"])
+    lpc = times[dom][1] / steps
+    avg_s = stages[dom]["avg_us"] / 1e6          # one launch
+    wk = {k: v / lpc for k, v in work[dom].items()}  # one launch's share of the stage
     flops_per_byte = wk["flops"] / wk["bytes"]
     ridge = PEAK_TFLOPS[w.dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
     if wk["flops"] and flops_per_byte > ridge:
@@ -420,8 +424,9 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     roof["traffic"] = measured_traffic(dom) if name == "wx256" else None
     roof["kernel"] = dom
-    roof["algorithmic_bytes_per_launch"] = wk["bytes"]
-    roof["algorithmic_flops_per_launch"] = wk["flops"]
+    roof["algorithmic_bytes_per_launch"] = int(wk["bytes"])
+    roof["algorithmic_flops_per_launch"] = int(wk["flops"])
+    roof["launches_per_call"] = round(lpc, 3)
 
     # the transforms alone: forward on x (input spins), inverse on a
     # coefficient set of the output spins

@@ -347,7 +347,7 @@ template <typename T, int BM, int BN, int BK, int WM, int WN, bool kVec>
 __global__ void __launch_bounds__(NT) lat_inv_kernel(const T* __restrict__ coef,
                                                      const T* __restrict__ tab,
                                                      T* __restrict__ Y, int L, int H, int Hp,
-                                                     int JT, int Lp, int B, int C, int S,
+                                                     int JT, int Lp, int B, int Bc, int C, int S,
                                                      SpinList sout_, int n_tiles_n) {
   using Tile = MfmaTile<T, BM, BN, BK, WM, WN>;
   using G = GemmLds<T, BM, BN, BK>;
@@ -375,7 +375,7 @@ __global__ void __launch_bounds__(NT) lat_inv_kernel(const T* __restrict__ coef,
   CoefTLoader<T, BM, BK, kVec> la;
   la.coef = coef;
   la.m = m;
-  la.B = B;
+  la.B = Bc;  // rows of the coefficient array hold Bc batch items
   la.S = S;
   la.si = si;
   la.twoC = 2 * C;
@@ -489,7 +489,8 @@ hipError_t lat_inv_cfg(const Plan& p, int B, int C, const void* coef, void* Y, h
   auto kern = ((2 * C) % VEC == 0) ? lat_inv_kernel<T, BM, BN, kBK<T, SWSFT_BK_LAT_INV>, WM, WN, true>
                                    : lat_inv_kernel<T, BM, BN, kBK<T, SWSFT_BK_LAT_INV>, WM, WN, false>;
   hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(NT), 0, st, (const T*)coef,
-                     (const T*)p.tab_inv, (T*)Y, p.L, p.H, p.Hp, p.JT, p.Lp, B, C, p.n_out,
+                     (const T*)p.tab_inv, (T*)Y, p.L, p.H, p.Hp, p.JT, p.Lp, B,
+                     p.coef_ldb > 0 ? p.coef_ldb : B, C, p.n_out,
                      make_spins(p.spins_out, p.n_out), nnt);
   return hipGetLastError();
 }

@@ -230,7 +230,7 @@ __device__ __forceinline__ v4s tr_read(const unsigned char* tile, int pitch, int
 template <int RA, int RB, int ST>
 __global__ void __launch_bounds__((InvGeom<RA, RB, ST>::NT))
     lat_inv_dma_kernel(const __bf16* __restrict__ coef, const __bf16* __restrict__ tab,
-                       __bf16* __restrict__ Y, int L, int H, int Lp, int B, int C, int S,
+                       __bf16* __restrict__ Y, int L, int H, int Lp, int B, int Bc, int C, int S,
                        SpinList sout_, int n_tiles_n) {
   using G = InvGeom<RA, RB, ST>;
   constexpr int BK = G::BK;
@@ -262,7 +262,7 @@ __global__ void __launch_bounds__((InvGeom<RA, RB, ST>::NT))
   // the step; degrees below lo or past L are clamped to a row that exists
   // (the table is zero there); copies g >= NI_A: table rows j
   const __bf16* csrc = coef + (size_t)b0 * S * twoC + (size_t)si * twoC + (n0 - b0 * twoC);
-  const size_t row_elems = (size_t)B * S * twoC;  // elements per coefficient row (l, m)
+  const size_t row_elems = (size_t)Bc * S * twoC;  // elements per coefficient row (l, m)
   int ka[G::PER_WAVE], ca[G::PER_WAVE];
   const __bf16* bsrc[G::PER_WAVE];
 #pragma unroll
@@ -394,8 +394,8 @@ hipError_t inv_geom(const Plan& p, int B, int C, const void* coef, void* Y, hipS
   for (int i = 0; i < p.n_out; ++i) so.s[i] = p.spins_out[i];
   hipLaunchKernelGGL((lat_inv_dma_kernel<RA, RB, ST>), dim3(xcd_grid(blocks)),
                      dim3(InvGeom<RA, RB, ST>::NT), 0, st, (const __bf16*)coef,
-                     (const __bf16*)p.tab_inv, (__bf16*)Y, p.L, p.H, p.Lp, B, C, p.n_out, so,
-                     nnt);
+                     (const __bf16*)p.tab_inv, (__bf16*)Y, p.L, p.H, p.Lp, B,
+                     p.coef_ldb > 0 ? p.coef_ldb : B, C, p.n_out, so, nnt);
   return hipGetLastError();
 }
 

@@ -391,12 +391,42 @@ swsft_status forward_stages(Plan& p, int B, int C, const void* x, void* X, void*
                    [&] { return swsft::launch_lat_fwd(v, B, C, D, coef, st); });
 }
 
-// The inverse transform coef -> y (see forward_stages).
+// Spectra of at most this many bytes stay in the 256 MiB Infinity Cache of an
+// MI355X between the latitude synthesis that writes them and the inverse
+// longitude DFT that reads them.
+constexpr size_t kCacheResidentBytes = size_t(128) << 20;
+
+// The inverse transform coef -> y (see forward_stages).  When the spectrum Y
+// of the whole batch exceeds kCacheResidentBytes, synthesis and inverse DFT
+// alternate over batch ranges whose Y fits, so the DFT reads Y from the
+// cache instead of HBM.
 swsft_status inverse_stages(Plan& p, int B, int C, const void* coef, void* Y, void* D, void* y,
                             hipStream_t st) {
   if (!swsft::is_delta(p)) {
-    SWSFT_TRY(run_stage(p, swsft::kStageLatInv, st, "lat_inv",
-                        [&] { return swsft::launch_lat_inv(p, B, C, coef, Y, st); }));
+    const size_t per_item = swsft::xy_elems(p, p.n_out, 1, C) * p.elem;
+    int bc = per_item == 0 ? B : (int)(kCacheResidentBytes / per_item);
+    bc = bc < 1 ? 1 : (bc > B ? B : bc);
+    if (((size_t)p.n_out * 2 * C * p.elem) % 16 != 0) bc = B;  // batch offsets keep 16-byte rows
+    if (bc >= B) {
+      SWSFT_TRY(run_stage(p, swsft::kStageLatInv, st, "lat_inv",
+                          [&] { return swsft::launch_lat_inv(p, B, C, coef, Y, st); }));
+      return run_stage(p, swsft::kStageDftInv, st, "dft_inv",
+                       [&] { return swsft::launch_dft_inv(p, p.n_out, B, C, Y, y, st); });
+    }
+    Plan v = p;
+    v.coef_ldb = B;
+    const size_t coef_step = (size_t)p.n_out * 2 * C * p.elem;  // one batch item of a row
+    const size_t y_step = (size_t)p.n_out * C * p.H * p.W * 2 * p.elem;
+    for (int b0 = 0; b0 < B; b0 += bc) {
+      const int n = B - b0 < bc ? B - b0 : bc;
+      const void* cb = static_cast<const char*>(coef) + b0 * coef_step;
+      void* yb = static_cast<char*>(y) + b0 * y_step;
+      SWSFT_TRY(run_stage(p, swsft::kStageLatInv, st, "lat_inv",
+                          [&] { return swsft::launch_lat_inv(v, n, C, cb, Y, st); }));
+      SWSFT_TRY(run_stage(p, swsft::kStageDftInv, st, "dft_inv",
+                          [&] { return swsft::launch_dft_inv(p, p.n_out, n, C, Y, yb, st); }));
+    }
+    return SWSFT_OK;
   } else {
     Plan v = p;
     v.H = v.Hp = swsft::delta_rows(p);

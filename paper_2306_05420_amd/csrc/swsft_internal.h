@@ -53,6 +53,9 @@ struct Plan {
   float2* twiddle = nullptr;  // [W]: exp(-2 pi i r / W)
   // creation flags (SWSFT_PLAN_*); with SWSFT_PLAN_DFT_MATMUL the forward
   // longitude stage is a dense DFT GEMM against dft_mat [2M][2W]
+  // batch count of the coefficient array the latitude synthesis reads (0: the
+  // call's B): lets lat_inv run on a batch range of a larger array
+  int coef_ldb = 0;
   unsigned flags = 0;
   void* dft_mat = nullptr;
   // Wigner-Delta route (SWSFT_PLAN_DELTA / SWSFT_PLAN_DELTA_SYM): theta tables
