@@ -19,6 +19,7 @@
 // consecutive channels, 4 consecutive k each), one dword per lane for fp32.
 #include <type_traits>
 
+#include "lds_dma.h"
 #include "mfma_tile.h"
 #include "swsft_internal.h"
 #include "xcd.h"
@@ -350,9 +351,219 @@ Spins to_spins(const int* s, int n) {
   return r;
 }
 
+// ---------------------------------------------------------------- bf16 filter gradient, DMA
+// The same gradient as one real GEMM over the interleaved values as stored:
+//   P[(t',rho)][(s',sigma)] = sum_k g_rho[k][t'] a_sigma[k][s'],
+//   gK[t'][s'] = (P[re][re] + P[im][im], P[im][re] - P[re][im]),
+// rows from g and columns from a, both K-major (row k = one coefficient row
+// (m, b), channels contiguous), so their tiles are copied global -> LDS
+// unchanged ([k][cols], 16-byte chunks swizzled by k), fragments are read
+// with ds_read_b64_tr_b16 on both sides, and the 2 x 2 blocks are combined
+// in registers (rows 2q, 2q+1 are registers r, r+1 of a lane; columns
+// 2p, 2p+1 are neighbouring lanes).  Contraction rows past (2l+1) B are
+// copied from a clamped row and zeroed in LDS before use.
+template <int RA, int RB, int TN, int ST>
+struct GradDmaGeom {
+  static constexpr int BK = 32;  // contraction rows per K step
+  static constexpr int TM = 2;   // 32-row MFMA tiles per wave (64 rows)
+  static constexpr int WM = RA / (32 * TM), WN = RB / (32 * TN);
+  static constexpr int NW = WM * WN, NT = 64 * NW;
+  static constexpr int PITCH_A = 2 * RA, PITCH_B = 2 * RB;  // bytes per k row
+  static constexpr int RPI_A = 1024 / PITCH_A, LPR_A = 64 / RPI_A;
+  static constexpr int RPI_B = 1024 / PITCH_B, LPR_B = 64 / RPI_B;
+  static constexpr int A_BYTES = BK * PITCH_A, B_BYTES = BK * PITCH_B;
+  static constexpr int NI_A = A_BYTES / 1024, NI = NI_A + B_BYTES / 1024;
+  static constexpr int PER_WAVE = NI / NW;
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int SMEM = ST * STAGE;
+  static_assert(RA % 128 == 0 && RB % 128 == 0 && NI % NW == 0 && RPI_A >= 1 && RPI_B >= 1 &&
+                    ST >= 2 && (ST - 2) * PER_WAVE < 64,
+                "tile shape");
+};
+
+__device__ __forceinline__ v4s tr_read_t(const unsigned char* tile, int pitch, int k, int col) {
+  const unsigned char* p = tile + k * pitch + swz_t(k, col >> 3) * 16 + (col & 7) * 2;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4s*)((__attribute__((address_space(3))) unsigned char*)p));
+}
+
+template <int RA, int RB, int TN, int ST>
+__global__ void __launch_bounds__((GradDmaGeom<RA, RB, TN, ST>::NT))
+    filter_grad_dma_kernel(const __bf16* __restrict__ a, const __bf16* __restrict__ g,
+                           __bf16* __restrict__ gK, int L, int B, int Cin, int Cout, int n_in,
+                           int n_out, Spins sin_, Spins sout_, int tiles_r, int tiles_c) {
+  using G = GradDmaGeom<RA, RB, TN, ST>;
+  constexpr int BK = G::BK, TM = G::TM;
+  __shared__ __align__(16) unsigned char smem[G::SMEM];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / G::WN, wn = wave % G::WN;
+  const int per_l = tiles_r * tiles_c;
+  const int lb = xcd_logical_block();
+  if (lb >= L * per_l) return;
+  const int l = paired_degree(lb / per_l, L);
+  const int tile = lb % per_l;
+  const int Nc = n_out * Cout, Kc = n_in * Cin;
+  const int R2 = 2 * Nc, Q2 = 2 * Kc;  // real rows (from g) and columns (from a)
+  const int r0 = (tile / tiles_c) * RA, c0 = (tile % tiles_c) * RB;
+  const int Kl = (2 * l + 1) * B;
+  const size_t row0 = (size_t)l * l * B;
+
+  bool rows_dead = true, cols_dead = true;
+  for (int t = (r0 / 2) / Cout; t <= (min(r0 + RA, R2) / 2 - 1) / Cout; ++t)
+    if (iabs_(sout_.s[t]) <= l) rows_dead = false;
+  for (int q = (c0 / 2) / Cin; q <= (min(c0 + RB, Q2) / 2 - 1) / Cin; ++q)
+    if (iabs_(sin_.s[q]) <= l) cols_dead = false;
+
+  v16f acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  if (!rows_dead && !cols_dead) {
+    // copy u of this wave: g rows (A tile) for copy index < NI_A, else a rows;
+    // lane -> (k row of the step, 16-byte slot), source chunk swizzled by k
+    const __bf16* src[G::PER_WAVE];
+    int krow[G::PER_WAVE], pitch[G::PER_WAVE];
+#pragma unroll
+    for (int u = 0; u < G::PER_WAVE; ++u) {
+      const int gi = wave * G::PER_WAVE + u;
+      if (gi < G::NI_A) {
+        const int k = gi * G::RPI_A + lane / G::LPR_A;
+        const int col = min(r0 + swz_t(k, lane % G::LPR_A) * 8, R2 - 8);
+        src[u] = g + col;
+        krow[u] = k;
+        pitch[u] = R2;
+      } else {
+        const int gb = gi - G::NI_A;
+        const int k = gb * G::RPI_B + lane / G::LPR_B;
+        const int col = min(c0 + swz_t(k, lane % G::LPR_B) * 8, Q2 - 8);
+        src[u] = a + col;
+        krow[u] = k;
+        pitch[u] = Q2;
+      }
+    }
+    const unsigned ring = lds_addr(smem);
+    auto issue = [&](int i, int stage) {
+      const unsigned base = ring + stage * G::STAGE + wave * G::PER_WAVE * 1024;
+#pragma unroll
+      for (int u = 0; u < G::PER_WAVE; ++u) {
+        const int k = min(i * BK + krow[u], Kl - 1);  // past the degree: a row that exists
+        dma16(src[u] + (row0 + k) * (size_t)pitch[u], base + u * 1024);
+      }
+    };
+    const int nk = (Kl + BK - 1) / BK;
+#pragma unroll
+    for (int st = 0; st < ST - 1; ++st)
+      if (st < nk) issue(st, st);
+    const int kh = lane >> 5, q4 = (lane & 15) >> 2, c4 = 4 * (lane & 3);
+    const int rr0 = 16 * ((lane >> 4) & 1);
+    for (int i = 0; i < nk; ++i) {
+      const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
+      wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
+      __builtin_amdgcn_s_barrier();
+      if (i + ST - 1 < nk) issue(i + ST - 1, (i + ST - 1) % ST);
+      unsigned char* As = smem + (i % ST) * G::STAGE;
+      unsigned char* Bs = As + G::A_BYTES;
+      const int kv = Kl - i * BK;  // valid rows of this step
+      if (kv < BK) {
+        // the clamped rows of the last step hold other data: zero them
+        const int zb = (BK - kv) * G::PITCH_A, zc = (BK - kv) * G::PITCH_B;
+        for (int o = tid * 16; o < zb; o += G::NT * 16)
+          *reinterpret_cast<uint4*>(As + kv * G::PITCH_A + o) = make_uint4(0, 0, 0, 0);
+        for (int o = tid * 16; o < zc; o += G::NT * 16)
+          *reinterpret_cast<uint4*>(Bs + kv * G::PITCH_B + o) = make_uint4(0, 0, 0, 0);
+        __syncthreads();
+      }
+#pragma unroll
+      for (int kk = 0; kk < BK / 16; ++kk) {
+        const int kbase = kk * 16 + 8 * kh + q4;
+        v8bf fa[TM], fb[TN];
+#pragma unroll
+        for (int ii = 0; ii < TM; ++ii) {
+          const int col = wm * 32 * TM + ii * 32 + rr0 + c4;
+          const v4s lo4 = tr_read_t(As, G::PITCH_A, kbase, col);
+          const v4s hi4 = tr_read_t(As, G::PITCH_A, kbase + 4, col);
+          fa[ii] = __builtin_bit_cast(v8bf, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+#pragma unroll
+        for (int jj = 0; jj < TN; ++jj) {
+          const int col = wn * 32 * TN + jj * 32 + rr0 + c4;
+          const v4s lo4 = tr_read_t(Bs, G::PITCH_B, kbase, col);
+          const v4s hi4 = tr_read_t(Bs, G::PITCH_B, kbase + 4, col);
+          fb[jj] = __builtin_bit_cast(v8bf, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+#pragma unroll
+        for (int ii = 0; ii < TM; ++ii)
+#pragma unroll
+          for (int jj = 0; jj < TN; ++jj)
+            acc[ii][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ii], fb[jj], acc[ii][jj], 0, 0, 0);
+      }
+    }
+    wait_vmcnt<0>();
+  }
+
+  // epilogue: rows 2q, 2q+1 of a column are registers r, r+1 of one lane;
+  // columns 2p, 2p+1 are lanes 2p', 2p'+1: the even lane combines
+  //   re = P[2q][2p] + P[2q+1][2p+1],  im = P[2q+1][2p] - P[2q][2p+1]
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  __bf16* out = gK + (size_t)l * Nc * Kc * 2;
+#pragma unroll
+  for (int ii = 0; ii < TM; ++ii)
+#pragma unroll
+    for (int jj = 0; jj < TN; ++jj) {
+      float x[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) x[r] = __shfl_xor(acc[ii][jj][r], 1);
+      const int col = c0 + wn * 32 * TN + jj * 32 + (lane & 31);
+      if ((lane & 1) || col >= Q2) continue;
+      const int sc = col >> 1;
+      const bool col_live = iabs_(sin_.s[sc / Cin]) <= l;
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) {
+        const int row = r0 + wm * 32 * TM + ii * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (row >= R2) continue;
+        const int tc = row >> 1;
+        const bool live = col_live && iabs_(sout_.s[tc / Cout]) <= l;
+        const float re = live ? acc[ii][jj][r] + x[r + 1] : 0.f;
+        const float im = live ? acc[ii][jj][r + 1] - x[r] : 0.f;
+        *reinterpret_cast<bf16x2*>(out + ((size_t)tc * Kc + sc) * 2) =
+            __builtin_convertvector((f32x2){re, im}, bf16x2);
+      }
+    }
+}
+
+// rows (from g) x columns (from a) per workgroup, 32-column MFMA tiles per
+// wave, stages: measured best of 256x256x4x2, 256x256x2x2, 256x256x4x3, 256x128x2x3
+#ifndef SWSFT_GRAD_DMA
+#define SWSFT_GRAD_DMA 256, 128, 2, 3
+#endif
+
+template <int RA, int RB, int TN, int ST>
+hipError_t filter_grad_dma_t(const Plan& p, int B, int Cin, int Cout, const void* a,
+                             const void* g, void* gK, hipStream_t st) {
+  const int R2 = 2 * p.n_out * Cout, Q2 = 2 * p.n_in * Cin;
+  const int tiles_r = (R2 + RA - 1) / RA, tiles_c = (Q2 + RB - 1) / RB;
+  const long long blocks = (long long)p.L * tiles_r * tiles_c;
+  hipLaunchKernelGGL((filter_grad_dma_kernel<RA, RB, TN, ST>), dim3(xcd_grid(blocks)),
+                     dim3(GradDmaGeom<RA, RB, TN, ST>::NT), 0, st, (const __bf16*)a,
+                     (const __bf16*)g, (__bf16*)gK, p.L, B, Cin, Cout, p.n_in, p.n_out,
+                     to_spins(p.spins_in, p.n_in), to_spins(p.spins_out, p.n_out), tiles_r,
+                     tiles_c);
+  return hipGetLastError();
+}
+
 template <typename T>
 hipError_t filter_grad_t(const Plan& p, int B, int Cin, int Cout, const void* a, const void* g,
                          void* gK, hipStream_t st) {
+  if constexpr (std::is_same<T, __bf16>::value) {
+    // interleaved rows as 16-byte chunks: channel counts with 2 S C % 8 == 0
+    if ((2 * p.n_out * Cout) % 8 == 0 && (2 * p.n_in * Cin) % 8 == 0)
+      return filter_grad_dma_t<SWSFT_GRAD_DMA>(p, B, Cin, Cout, a, g, gK, st);
+  }
   using G = GradGeom<T>;
   const int Nc = p.n_out * Cout, Kc = p.n_in * Cin;
   const int tiles_r = (Nc + GBM - 1) / GBM, tiles_c = (Kc + GBN - 1) / GBN;
