@@ -66,6 +66,11 @@ def stage_work(w):
         n = Co * sum(1 for t in w.spins_out if abs(t) <= l)
         mix += 8 * B * (2 * l + 1) * k * n
     return {
+        # small grids: whole transforms per map (the synthesis also mixes when
+        # the layer runs without a separate mixing stage)
+        "small_fwd": {"flops": lat_f, "bytes": x_b + tab_i + a_b},
+        "small_inv": {"flops": lat_i, "bytes": a2_b + tab_o + y_b},
+        "small_inv_mix": {"flops": lat_i + mix, "bytes": a_b + K_b + tab_o + y_b},
         "dft_fwd": {"flops": 0, "bytes": x_b + X_b},
         "lat_fwd": {"flops": lat_f, "bytes": X_b + tab_i + a_b},
         "mix": {"flops": mix, "bytes": a_b + K_b + a2_b},
@@ -393,7 +398,9 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
     plan.stage_timing(False)
 
     work = stage_work(w)
-    useful = sum(v["flops"] for v in work.values())
+    useful = sum(work[k]["flops"] for k in ("lat_fwd", "mix", "lat_inv"))
+    if "mix" not in times:  # small grids: the synthesis kernel mixes as well
+        work["small_inv"] = work["small_inv_mix"]
     stages = {}
     for sname, (ms, n) in times.items():
         # a stage may run as several launches per call (the inverse stages over
@@ -435,8 +442,10 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
     t_fwd = _time_calls(lambda: plan.forward(x, coef_f), steps, warmup)
     t_inv = _time_calls(lambda: plan.inverse(coef_out, y_i), steps, warmup)
     transforms = {}
-    for tname, t, keys in (("forward", t_fwd, ("dft_fwd", "lat_fwd")),
-                           ("inverse", t_inv, ("lat_inv", "dft_inv"))):
+    work = stage_work(w)
+    small = "small_fwd" in times
+    for tname, t, keys in (("forward", t_fwd, ("small_fwd",) if small else ("dft_fwd", "lat_fwd")),
+                           ("inverse", t_inv, ("small_inv",) if small else ("lat_inv", "dft_inv"))):
         byt = sum(work[k]["bytes"] for k in keys)
         fl = sum(work[k]["flops"] for k in keys)
         transforms[tname] = {"us": round(t * 1e6, 2), "per_s": round(1.0 / t, 1),
@@ -694,7 +703,10 @@ TABLE_HEAD = ("| Cfg | Op | median µs | calls/s | useful TFLOP/s | % MFMA peak 
 def table_rows(cfg: int, r: dict):
     w, st = r["w"], r["stages"]
     peak = PEAK_TFLOPS[w.dtype]
-    dft = f"{st['dft_fwd']['GB/s']:.0f} / {st['dft_inv']['GB/s']:.0f}"
+    if "dft_fwd" in st:
+        dft = f"{st['dft_fwd']['GB/s']:.0f} / {st['dft_inv']['GB/s']:.0f}"
+    else:
+        dft = f"{st['small_fwd']['GB/s']:.0f} / {st['small_inv']['GB/s']:.0f} (whole transforms)"
     roof = f"{100 * r['roofline']['frac']:.1f} ({r['roofline']['kernel']})"
     rows = [f"| {cfg} {w.name} | layer | {r['ms_per_step'] * 1e3:.1f} | {r['value']:.0f} | "
             f"{r['tflops']:.1f} | {100 * r['tflops'] / peak:.1f} | {dft} | {roof} |"]

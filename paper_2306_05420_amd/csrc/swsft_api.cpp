@@ -225,7 +225,7 @@ const char* swsft_stage_name(int stage) {
   static const char* names[swsft::kNumStages] = {"dft_fwd", "lat_fwd", "mix", "lat_inv",
                                                  "dft_inv", "phase_collapse", "tables",
                                                  "filter_grad", "filter_adjoint", "batch_norm",
-                                                 "delta_theta"};
+                                                 "delta_theta", "small_fwd", "small_inv"};
   if (stage < 0 || stage >= swsft::kNumStages) return "";
   return names[stage];
 }
@@ -376,6 +376,9 @@ namespace {
 // is the R rows of D).
 swsft_status forward_stages(Plan& p, int B, int C, const void* x, void* X, void* D, void* coef,
                             hipStream_t st) {
+  if (swsft::small_path(p, 1))
+    return run_stage(p, swsft::kStageSmallFwd, st, "small_fwd",
+                     [&] { return swsft::launch_small_fwd(p, B, C, x, coef, st); });
   SWSFT_TRY(run_stage(p, swsft::kStageDftFwd, st, "dft_fwd",
                       [&] { return swsft::launch_dft_fwd(p, p.n_in, B, C, x, X, st); }));
   if (!swsft::is_delta(p))
@@ -402,6 +405,10 @@ constexpr size_t kCacheResidentBytes = size_t(128) << 20;
 // cache instead of HBM.
 swsft_status inverse_stages(Plan& p, int B, int C, const void* coef, void* Y, void* D, void* y,
                             hipStream_t st) {
+  if (swsft::small_path(p, 1))
+    return run_stage(p, swsft::kStageSmallInv, st, "small_inv", [&] {
+      return swsft::launch_small_inv(p, B, 1, C, coef, nullptr, y, st);
+    });
   if (!swsft::is_delta(p)) {
     const size_t per_item = swsft::xy_elems(p, p.n_out, 1, C) * p.elem;
     int bc = per_item == 0 ? B : (int)(kCacheResidentBytes / per_item);
@@ -512,6 +519,13 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
   void* coef2 = w;
   w += align_up(swsft::coef_elems(*p, p->n_out, B, C_out) * p->elem);
   void* D = w;
+  if (swsft::small_path(*p, C_in)) {
+    // small grids: the mixing runs inside the synthesis, per output map
+    SWSFT_TRY(forward_stages(*p, B, C_in, x, XY, D, coef, st));
+    return run_stage(*p, swsft::kStageSmallInv, st, "small_inv", [&] {
+      return swsft::launch_small_inv(*p, B, C_in, C_out, coef, filters, y, st);
+    });
+  }
   SWSFT_TRY(forward_stages(*p, B, C_in, x, XY, D, coef, st));
   SWSFT_TRY(run_stage(*p, swsft::kStageMix, st, "mix", [&] {
     return swsft::launch_mix(*p, B, C_in, C_out, coef, filters, coef2, st);

@@ -26,7 +26,9 @@ enum Stage : int {
   kStageFilterAdjoint = 8,
   kStageBatchNorm = 9,
   kStageDeltaTheta = 10,
-  kNumStages = 11
+  kStageSmallFwd = 11,
+  kStageSmallInv = 12,
+  kNumStages = 13
 };
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
@@ -119,6 +121,12 @@ inline bool is_delta(const Plan& p) {
 inline size_t delta_elems(const Plan& p, int S, int B, int C) {
   return is_delta(p) ? (size_t)S * p.M * delta_rows(p) * 2 * (size_t)B * C : 0;
 }
+// small grids (small.hip): whole transforms per map in one launch each
+bool small_path(const Plan& p, int Cin);
+hipError_t launch_small_fwd(const Plan& p, int B, int C, const void* x, void* coef,
+                            hipStream_t st);
+hipError_t launch_small_inv(const Plan& p, int B, int C_in, int C_out, const void* coef,
+                            const void* K, void* y, hipStream_t st);
 // Y [S][M][H/JT][B*C][2][JT] -> y [B][S][C][H][W]
 hipError_t launch_dft_inv(const Plan& p, int S, int B, int C, const void* Y, void* y,
                           hipStream_t st);

@@ -31,7 +31,7 @@ PLAN_DFT_MATMUL, PLAN_DELTA, PLAN_DELTA_SYM = 1, 2, 4
 F32, BF16 = 0, 1
 OP_FORWARD, OP_INVERSE, OP_CONV, OP_CONV_BACKWARD, OP_BATCH_NORM = 0, 1, 2, 3, 4
 STAGES = ("dft_fwd", "lat_fwd", "mix", "lat_inv", "dft_inv", "phase_collapse", "tables",
-          "filter_grad", "filter_adjoint", "batch_norm", "delta_theta")
+          "filter_grad", "filter_adjoint", "batch_norm", "delta_theta", "small_fwd", "small_inv")
 
 _lib = None
 
