@@ -290,6 +290,7 @@ def main(argv=None):
             "bandlimit": w.L,
             "parallelism": "single GPU",
         },
+        "latency_us": r["latency_us"],
         "tflops": round(r["tflops"], 2),
         "mfma_peak_frac": round(r["tflops"] / PEAK_TFLOPS[w.dtype], 4),
         "useful_gflop_per_fwd": round(r["useful"] / 1e9, 3),
@@ -388,6 +389,17 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
 
     # timed region: K layer calls
     t_layer = _time_calls(lambda: plan.conv(x, K, y), steps, warmup)
+    # per-call latency distribution (a separate pass, one event pair per call)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    for e0, e1 in evs:
+        e0.record()
+        plan.conv(x, K, y)
+        e1.record()
+    torch.cuda.synchronize()
+    per_call = sorted(e0.elapsed_time(e1) * 1e3 for e0, e1 in evs)
+    pct = lambda q: round(per_call[min(len(per_call) - 1, int(q * len(per_call)))], 2)
+    latency = {"p10": pct(0.1), "p50": pct(0.5), "p90": pct(0.9)}
 
     # per-stage HIP events over a second pass of K layer calls
     plan.stage_timing(True)
@@ -451,7 +463,7 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
         transforms[tname] = {"us": round(t * 1e6, 2), "per_s": round(1.0 / t, 1),
                              "GB/s": round(byt / t / 1e9, 1),
                              "TFLOP/s": round(fl / t / 1e12, 2)}
-    r = {"w": w, "value": 1.0 / t_layer, "ms_per_step": t_layer * 1e3,
+    r = {"w": w, "value": 1.0 / t_layer, "ms_per_step": t_layer * 1e3, "latency_us": latency,
          "tflops": useful / t_layer / 1e12, "useful": useful, "stages": stages,
          "roofline": roof, "transforms": transforms}
     if not extras:
