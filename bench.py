@@ -702,9 +702,13 @@ def measure_backward(plan, w, x, K, grad_y, steps: int, warmup: int) -> dict:
     # per call: stage -> (microseconds, launches)
     stages = {k: {"us_per_call": round(ms * 1e3 / steps, 2), "launches_per_call": n // steps}
               for k, (ms, n) in times.items()}
+    # training: the forward saves the input's coefficients, the backward reuses them
+    _, cx = plan.conv(x, K, coef_x=True)
+    t_saved = _time_calls(lambda: plan.conv_backward(x, K, grad_y, grad_x=gx, grad_filters=gk,
+                                                     coef_x=cx), steps, warmup)
     return {"us": round(t * 1e6, 2), "per_s": round(1.0 / t, 1),
             "TFLOP/s": round(fl / t / 1e12, 2), "useful_gflop": round(fl / 1e9, 3),
-            "stages": stages}
+            "stages": stages, "us_with_saved_coefficients": round(t_saved * 1e6, 2)}
 
 
 TABLE_HEAD = ("| Cfg | Op | median µs | calls/s | useful TFLOP/s | % MFMA peak | "

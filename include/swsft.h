@@ -185,7 +185,11 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
  * with g = G^H grad_y (the analysis sum of eq. (2) without quadrature
  * weights), a = F x, and zeros where |s| > l or |t| > l.  F^H is the
  * synthesis of eq. (3) weighted by (2 pi / W) w_j; K^H applies conj(K).
- *  x             [B][S_in][C_in][H][W] complex; read when grad_filters != NULL.
+ *  x             [B][S_in][C_in][H][W] complex; read when grad_filters != NULL
+ *                and coef_x is NULL.
+ *  coef_x        [L*L][B][S_in][C_in] complex, the input's coefficients F x as
+ *                saved by spin_sph_conv_forward_train (or swsft_forward), or
+ *                NULL to compute them from x (one more forward transform).
  *  filters       [L][S_out][C_out][S_in][C_in] complex; read when grad_x != NULL.
  *  grad_y        [B][S_out][C_out][H][W] complex, read only.
  *  grad_x        [B][S_in][C_in][H][W] complex, written; NULL: not computed.
@@ -198,8 +202,20 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
  *  ws  workspace of ws_bytes >= swsft_workspace_bytes(p, SWSFT_OP_CONV_BACKWARD, B, C_in, C_out).
  */
 swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, const void* x,
-                                    const void* filters, const void* grad_y, void* grad_x,
-                                    void* grad_filters, void* ws, size_t ws_bytes, void* stream);
+                                    const void* coef_x, const void* filters, const void* grad_y,
+                                    void* grad_x, void* grad_filters, void* ws, size_t ws_bytes,
+                                    void* stream);
+
+/*
+ * spin_sph_conv_forward that also writes the input's coefficients F x
+ * (eq. (2); [L*L][B][S_in][C_in] complex, the layout of swsft_forward) to
+ * coef_x, for the backward pass to reuse: training saves them instead of
+ * transforming x again.  Same workspace as spin_sph_conv_forward; coef_x must
+ * not overlap any other argument.
+ */
+swsft_status spin_sph_conv_forward_train(swsft_plan p, int B, int C_in, int C_out, const void* x,
+                                         const void* filters, void* y, void* coef_x, void* ws,
+                                         size_t ws_bytes, void* stream);
 
 /*
  * Phase-collapse nonlinearity (Method, "Phase collapse nonlinearity") on a

@@ -488,9 +488,13 @@ swsft_status swsft_inverse(swsft_plan p, int B, int C, const void* coef, void* y
   return inverse_stages(*p, B, C, coef, Y, D, y, st);
 }
 
-swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, const void* x,
-                                   const void* filters, void* y, void* ws, size_t ws_bytes,
-                                   void* stream) {
+namespace {
+
+// The layer; with coef_x != NULL the input's coefficients are written there
+// (for the backward pass) instead of to the workspace.
+swsft_status conv_forward(swsft_plan p, int B, int C_in, int C_out, const void* x,
+                          const void* filters, void* y, void* coef_x, void* ws, size_t ws_bytes,
+                          void* stream) {
   g_last_error[0] = 0;
   if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
   SWSFT_TRY(check_bc(B, C_in, "C_in"));
@@ -498,15 +502,17 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
   SWSFT_TRY(check_ptr(x, "x"));
   SWSFT_TRY(check_ptr(filters, "filters"));
   SWSFT_TRY(check_ptr(y, "y"));
+  if (coef_x != nullptr) SWSFT_TRY(check_ptr(coef_x, "coef_x"));
   SWSFT_TRY(check_inverse_stage(*p));
   SWSFT_TRY(check_ws(*p, SWSFT_OP_CONV, B, C_in, C_out, ws, ws_bytes));
-  {
-    const char* xb = static_cast<const char*>(x);
-    const char* yb = static_cast<const char*>(y);
-    const size_t xs = (size_t)B * p->n_in * C_in * p->H * p->W * 2 * p->elem;
-    const size_t ys = (size_t)B * p->n_out * C_out * p->H * p->W * 2 * p->elem;
-    if (xb < yb + ys && yb < xb + xs) return fail(SWSFT_E_INVALID, "x and y overlap");
-  }
+  const size_t xs = (size_t)B * p->n_in * C_in * p->H * p->W * 2 * p->elem;
+  const size_t ys = (size_t)B * p->n_out * C_out * p->H * p->W * 2 * p->elem;
+  const size_t cs = swsft::coef_elems(*p, p->n_in, B, C_in) * p->elem;
+  const size_t ks = filter_elems(*p, C_in, C_out) * p->elem;
+  if (overlaps(x, xs, y, ys)) return fail(SWSFT_E_INVALID, "x and y overlap");
+  if (overlaps(coef_x, cs, x, xs) || overlaps(coef_x, cs, y, ys) ||
+      overlaps(coef_x, cs, filters, ks) || overlaps(coef_x, cs, ws, ws_bytes))
+    return fail(SWSFT_E_INVALID, "coef_x overlaps another argument");
   SWSFT_TRY(check_device(*p));
   hipStream_t st = static_cast<hipStream_t>(stream);
   const size_t xin = swsft::xy_elems(*p, p->n_in, B, C_in);
@@ -514,7 +520,7 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
   char* w = static_cast<char*>(ws);
   void* XY = w;
   w += align_up((xin > xout ? xin : xout) * p->elem);
-  void* coef = w;
+  void* coef = coef_x != nullptr ? coef_x : static_cast<void*>(w);
   w += align_up(swsft::coef_elems(*p, p->n_in, B, C_in) * p->elem);
   void* coef2 = w;
   w += align_up(swsft::coef_elems(*p, p->n_out, B, C_out) * p->elem);
@@ -533,9 +539,28 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
   return inverse_stages(*p, B, C_out, coef2, XY, D, y, st);
 }
 
+}  // namespace
+
+swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, const void* x,
+                                   const void* filters, void* y, void* ws, size_t ws_bytes,
+                                   void* stream) {
+  return conv_forward(p, B, C_in, C_out, x, filters, y, nullptr, ws, ws_bytes, stream);
+}
+
+swsft_status spin_sph_conv_forward_train(swsft_plan p, int B, int C_in, int C_out, const void* x,
+                                         const void* filters, void* y, void* coef_x, void* ws,
+                                         size_t ws_bytes, void* stream) {
+  if (coef_x == nullptr) {
+    g_last_error[0] = 0;
+    return fail(SWSFT_E_INVALID, "coef_x is NULL");
+  }
+  return conv_forward(p, B, C_in, C_out, x, filters, y, coef_x, ws, ws_bytes, stream);
+}
+
 swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, const void* x,
-                                    const void* filters, const void* grad_y, void* grad_x,
-                                    void* grad_filters, void* ws, size_t ws_bytes, void* stream) {
+                                    const void* coef_x, const void* filters, const void* grad_y,
+                                    void* grad_x, void* grad_filters, void* ws, size_t ws_bytes,
+                                    void* stream) {
   g_last_error[0] = 0;
   if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
   SWSFT_TRY(check_bc(B, C_in, "C_in"));
@@ -546,7 +571,8 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
   SWSFT_TRY(check_inverse_stage(*p));
   SWSFT_TRY(reject_delta(*p, "spin_sph_conv_backward"));
   if (grad_filters != nullptr) {
-    SWSFT_TRY(check_ptr(x, "x"));
+    if (coef_x != nullptr) SWSFT_TRY(check_ptr(coef_x, "coef_x"));
+    else SWSFT_TRY(check_ptr(x, "x"));
     SWSFT_TRY(check_ptr(grad_filters, "grad_filters"));
   }
   if (grad_x != nullptr) {
@@ -560,7 +586,11 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
     const size_t ys = (size_t)B * p->n_out * C_out * p->H * p->W * 2 * p->elem;
     const size_t ks = filter_elems(*p, C_in, C_out) * p->elem;
     struct R { const void* a; size_t n; };
-    const R ins[3] = {{grad_filters ? x : nullptr, xs}, {grad_x ? filters : nullptr, ks}, {grad_y, ys}};
+    const size_t cs = swsft::coef_elems(*p, p->n_in, B, C_in) * p->elem;
+    const R ins[4] = {{grad_filters && !coef_x ? x : nullptr, xs},
+                      {grad_filters ? coef_x : nullptr, cs},
+                      {grad_x ? filters : nullptr, ks},
+                      {grad_y, ys}};
     const R outs[2] = {{grad_x, xs}, {grad_filters, ks}};
     for (const R& o : outs) {
       if (o.a == nullptr) continue;
@@ -616,12 +646,15 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
   SWSFT_TRY(run_stage(*p, swsft::kStageLatFwd, st, "lat_fwd",
                       [&] { return swsft::launch_lat_fwd(ana, B, C_out, XY, g_out, st); }));
   if (grad_filters != nullptr) {
-    SWSFT_TRY(run_stage(*p, swsft::kStageDftFwd, st, "dft_fwd",
-                        [&] { return swsft::launch_dft_fwd(*p, p->n_in, B, C_in, x, XY, st); }));
-    SWSFT_TRY(run_stage(*p, swsft::kStageLatFwd, st, "lat_fwd",
-                        [&] { return swsft::launch_lat_fwd(*p, B, C_in, XY, a_in, st); }));
+    const void* a = coef_x;  // F x as saved by the forward pass, or computed here
+    if (a == nullptr) {
+      // the forward transform exactly as the layer computes it (same kernels,
+      // so saved and recomputed coefficients agree bit for bit)
+      SWSFT_TRY(forward_stages(*p, B, C_in, x, XY, nullptr, a_in, st));
+      a = a_in;
+    }
     SWSFT_TRY(run_stage(*p, swsft::kStageFilterGrad, st, "filter_grad", [&] {
-      return swsft::launch_filter_grad(*p, B, C_in, C_out, a_in, g_out, grad_filters, st);
+      return swsft::launch_filter_grad(*p, B, C_in, C_out, a, g_out, grad_filters, st);
     }));
   }
   if (grad_x != nullptr) {

@@ -71,7 +71,8 @@ def lib() -> ctypes.CDLL:
         "swsft_forward": (i, [vp, i, i, vp, vp, vp, sz, vp]),
         "swsft_inverse": (i, [vp, i, i, vp, vp, vp, sz, vp]),
         "spin_sph_conv_forward": (i, [vp, i, i, i, vp, vp, vp, vp, sz, vp]),
-        "spin_sph_conv_backward": (i, [vp, i, i, i, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "spin_sph_conv_backward": (i, [vp, i, i, i, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "spin_sph_conv_forward_train": (i, [vp, i, i, i, vp, vp, vp, vp, vp, sz, vp]),
         "spin_sph_phase_collapse": (i, [vp, i, i, vp, vp, vp, vp, vp, vp]),
         "spin_sph_mix": (i, [vp, i, i, i, vp, vp, vp, vp]),
         "spin_sph_spectral_batch_norm": (i, [vp, i, i, vp, vp, vp, ctypes.c_float, vp, vp, vp,
@@ -246,9 +247,11 @@ class Plan:
         return y
 
     def conv(self, x: torch.Tensor, filters: torch.Tensor, y: torch.Tensor = None,
-             stream=None) -> torch.Tensor:
+             stream=None, coef_x: torch.Tensor = None):
         """The layer: x [B, S_in, C_in, H, W], filters [L, S_out, C_out, S_in, C_in]
-        -> y [B, S_out, C_out, H, W]."""
+        -> y [B, S_out, C_out, H, W].  With coef_x (a [L*L, B, S_in, C_in]
+        tensor, or True to allocate one) the input's coefficients are saved
+        for the backward pass and (y, coef_x) is returned."""
         xr = self.real_view(x)
         B, S, Cin = xr.shape[:3]
         self._shape(xr, (B, len(self.spins_in), Cin, self.H, self.W), "x")
@@ -260,17 +263,32 @@ class Plan:
         yr = self.real_view(y)
         self._shape(yr, (B, len(self.spins_out), Cout, self.H, self.W), "y")
         ws = self.workspace(OP_CONV, B, Cin, Cout)
-        _check(lib().spin_sph_conv_forward(self._h, B, Cin, Cout, xr.data_ptr(), kr.data_ptr(),
-                                           yr.data_ptr(), ws.data_ptr(), ws.numel(),
-                                           _stream_handle(stream)), "spin_sph_conv_forward")
-        return y
+        if coef_x is None or coef_x is False:
+            _check(lib().spin_sph_conv_forward(self._h, B, Cin, Cout, xr.data_ptr(),
+                                               kr.data_ptr(), yr.data_ptr(), ws.data_ptr(),
+                                               ws.numel(), _stream_handle(stream)),
+                   "spin_sph_conv_forward")
+            return y
+        if coef_x is True:
+            coef_x = self.empty(self.L * self.L, B, S, Cin)
+        cr = self.real_view(coef_x)
+        self._shape(cr, (self.L * self.L, B, S, Cin), "coef_x")
+        _check(lib().spin_sph_conv_forward_train(self._h, B, Cin, Cout, xr.data_ptr(),
+                                                 kr.data_ptr(), yr.data_ptr(), cr.data_ptr(),
+                                                 ws.data_ptr(), ws.numel(),
+                                                 _stream_handle(stream)),
+               "spin_sph_conv_forward_train")
+        return y, coef_x
 
     def conv_backward(self, x: torch.Tensor, filters: torch.Tensor, grad_y: torch.Tensor,
                       need_x: bool = True, need_filters: bool = True, grad_x: torch.Tensor = None,
-                      grad_filters: torch.Tensor = None, stream=None):
+                      grad_filters: torch.Tensor = None, stream=None,
+                      coef_x: torch.Tensor = None):
         """Gradients of the layer for a real loss with dL = Re sum conj(grad_y) dy:
         returns (grad_x [B, S_in, C_in, H, W] or None,
-                 grad_filters [L, S_out, C_out, S_in, C_in] or None)."""
+                 grad_filters [L, S_out, C_out, S_in, C_in] or None).
+        coef_x: the input's coefficients saved by conv(..., coef_x=True), so
+        that x is not transformed again."""
         if not (need_x or need_filters):
             raise ValueError("request grad_x, grad_filters or both")
         xr = self.real_view(x)
@@ -298,10 +316,15 @@ class Plan:
             gk_ptr = gkr.data_ptr()
         else:
             grad_filters = None
+        cx_ptr = None
+        if coef_x is not None:
+            cr = self.real_view(coef_x)
+            self._shape(cr, (self.L * self.L, B, S, Cin), "coef_x")
+            cx_ptr = cr.data_ptr()
         ws = self.workspace(OP_CONV_BACKWARD, B, Cin, Cout)
-        _check(lib().spin_sph_conv_backward(self._h, B, Cin, Cout, xr.data_ptr(), kr.data_ptr(),
-                                            gr.data_ptr(), gx_ptr, gk_ptr, ws.data_ptr(),
-                                            ws.numel(), _stream_handle(stream)),
+        _check(lib().spin_sph_conv_backward(self._h, B, Cin, Cout, xr.data_ptr(), cx_ptr,
+                                            kr.data_ptr(), gr.data_ptr(), gx_ptr, gk_ptr,
+                                            ws.data_ptr(), ws.numel(), _stream_handle(stream)),
                "spin_sph_conv_backward")
         return grad_x, grad_filters
 

@@ -80,6 +80,27 @@ def test_backward_outputs_independent_and_deterministic():
     plan.close()
 
 
+@pytest.mark.parametrize("name", ["tiny", "small", "mol"])
+def test_saved_coefficients(name):
+    """conv(..., coef_x=True) returns the layer and F x; the backward with the
+    saved coefficients equals the backward that transforms x again."""
+    w = syn.workload(name)
+    x, K, _ = workload_inputs(w)
+    rng = np.random.default_rng(w.seed + 3)
+    gy = _grad_y(rng, w.B, w.spins_out, w.C_out, w.H, w.W, w.dtype)
+    plan = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_out, w.dtype)
+    xd, Kd, gd = to_device(x, w.dtype), to_device(K, w.dtype), to_device(gy, w.dtype)
+    y_plain = plan.conv(xd, Kd).clone()
+    y, cx = plan.conv(xd, Kd, coef_x=True)
+    assert torch.equal(y, y_plain)
+    assert torch.equal(cx, plan.forward(xd))
+    gx0, gk0 = plan.conv_backward(xd, Kd, gd)
+    gx0, gk0 = gx0.clone(), gk0.clone()
+    gx1, gk1 = plan.conv_backward(xd, Kd, gd, coef_x=cx)
+    assert torch.equal(gx0, gx1) and torch.equal(gk0, gk1)
+    plan.close()
+
+
 BACKWARD_EDGE = [
     # H, L, spins_in, spins_out, B, C_in, C_out, dtype
     (16, 5, (0,), (0,), 1, 1, 1, "f32"),               # one channel, L < H/2
@@ -145,7 +166,8 @@ def test_backward_call_validation():
     need = plan.workspace_bytes(S.OP_CONV_BACKWARD, 1, 4, 4)
     assert need > plan.workspace_bytes(S.OP_CONV, 1, 4, 4)
     ws = torch.empty(need, dtype=torch.uint8, device="cuda")
-    call = lambda *a: L.spin_sph_conv_backward(plan._h, 1, 4, 4, *a, ws.data_ptr(), need, None)
+    call = lambda x_, *a: L.spin_sph_conv_backward(plan._h, 1, 4, 4, x_, None, *a, ws.data_ptr(),
+                                                   need, None)
     assert call(p(x), p(K), p(y), None, None) == S.E_INVALID            # nothing requested
     assert call(p(x), p(K), None, p(gx), p(gk)) == S.E_INVALID         # no grad_y
     assert call(None, p(K), p(y), None, p(gk)) == S.E_INVALID          # grad_filters needs x
@@ -154,8 +176,14 @@ def test_backward_call_validation():
     assert call(p(x), p(K), p(y), p(gx), p(K)) == S.E_INVALID          # grad_filters overlaps filters
     assert call(p(x), p(K), p(y), None, p(x)) == S.E_INVALID           # grad_filters overlaps x
     assert call(p(x), p(K), p(y), p(gx), p(gx)) == S.E_INVALID         # the outputs overlap
-    assert L.spin_sph_conv_backward(plan._h, 1, 4, 4, p(x), p(K), p(y), p(gx), p(gk),
+    assert L.spin_sph_conv_backward(plan._h, 1, 4, 4, p(x), None, p(K), p(y), p(gx), p(gk),
                                     ws.data_ptr(), need - 1, None) == S.E_WORKSPACE
+    # saved input coefficients replace x for the filter gradient
+    c = plan.empty(64, 1, 1, 4)
+    assert L.spin_sph_conv_backward(plan._h, 1, 4, 4, None, p(c), p(K), p(y), None, p(gk),
+                                    ws.data_ptr(), need, None) == S.OK
+    assert L.spin_sph_conv_backward(plan._h, 1, 4, 4, None, p(c), p(K), p(y), None, p(c),
+                                    ws.data_ptr(), need, None) == S.E_INVALID   # overlaps coef_x
     assert call(None, p(K), p(y), p(gx), None) == S.OK                  # x unused for grad_x only
     assert call(p(x), None, p(y), None, p(gk)) == S.OK                  # filters unused
     torch.cuda.synchronize()
