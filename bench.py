@@ -301,12 +301,35 @@ def main(argv=None):
     for k in ("backward", "graph"):
         if k in r:
             out[k] = r[k]
+    if not args.forward_only:
+        out["measured_peaks"] = measured_peaks()
     if "stack2" in r:
         out["stack2"] = r["stack2"]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out), flush=True)
     return 0
+
+
+def measured_peaks() -> dict:
+    """Achievable peaks on this GPU in the same run, for context next to the
+    datasheet figures: a plain 1 GiB device-to-device copy (bytes read +
+    written per second) and a large bf16 GEMM through the vendor library."""
+    import torch
+
+    src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    t_copy = _time_calls(lambda: dst.copy_(src), 10, 3)
+    del src, dst
+    n = 8192
+    a = torch.randn((n, n), device="cuda").to(torch.bfloat16)
+    b = torch.randn((n, n), device="cuda").to(torch.bfloat16)
+    c = torch.empty((n, n), device="cuda", dtype=torch.bfloat16)
+    t_mm = _time_calls(lambda: torch.matmul(a, b, out=c), 10, 3)
+    del a, b, c
+    return {"copy_GB/s": round(2 * (1 << 30) / t_copy / 1e9, 1),
+            "bf16_gemm_TFLOP/s": round(2.0 * n ** 3 / t_mm / 1e12, 1),
+            "gemm": f"torch.matmul bf16 {n}x{n}x{n}"}
 
 
 def _time_calls(fn, steps: int, warmup: int):
