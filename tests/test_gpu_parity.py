@@ -140,9 +140,13 @@ def test_two_layer_stack_with_phase_collapse():
 PC_CASES = [
     # H, L, spins_out, C, dtype
     (32, 16, (1, 0), 5, "f32"),        # C % 16 != 0: per-output loop kernel; spin 0 second
-    (4, 2, (1, 0, -1), 32, "f32"),     # MFMA kernel; 16 points (< one 64-point workgroup)
-    (32, 16, (0, 1), 64, "f32"),       # MFMA kernel at the molecule workload's width
+    (4, 2, (1, 0, -1), 32, "f32"),     # register form; 16 points (< one 32-point tile)
+    (32, 16, (0, 1), 64, "f32"),       # register form at the molecule workload's width
     (32, 16, (0, 1), 32, "bf16"),      # bf16 storage
+    (6, 3, (0,), 16, "f32"),           # register form, 36 points: a ragged 32-point tile
+    (6, 3, (2, 0), 48, "f32"),         # register form, three row tiles (odd), ragged
+    (8, 4, (0, 1, -1), 64, "f32"),     # LDS-staged MFMA kernel (no register form)
+    (10, 5, (0,), 80, "bf16"),         # LDS-staged MFMA kernel, 100 points (ragged)
 ]
 
 
@@ -152,7 +156,10 @@ def test_phase_collapse_in_place_and_passthrough(case):
     rng = np.random.default_rng(5 + C)
     x = round_to(syn.complex_normal(rng, (3, len(so), C, H, H)), dt)
     W1, W2, b = (np.asarray(t, np.complex64) for t in syn.phase_collapse_parameters(rng, len(so), C))
-    plan = S.Plan(H, H, L, (0,), so, dt)
+    # grids whose width is not a power of two need the matrix longitude route
+    # to make a plan; the phase collapse itself does not depend on it
+    lon = "fft" if H & (H - 1) == 0 else "matmul"
+    plan = S.Plan(H, H, L, (0,), so, dt, longitude=lon)
     xd = to_device(x, dt)
     tW = [torch.from_numpy(t).cuda() for t in (W1, W2, b)]
     y = from_device(plan.phase_collapse(xd, *tW))
