@@ -207,8 +207,8 @@ __global__ void __launch_bounds__(NT) mix_kernel(const T* __restrict__ coef,
                                                  int L, int B, int Cin, int Cout, int Sin,
                                                  int Sout, SpinList sin_, SpinList sout_) {
   using Tile = MfmaTile<T, BM, BN, BK, WM, WN>;
-  using G = GemmLds<T, BM, BN, BK>;
-  __shared__ __align__(16) T smem[G::bytes / sizeof(T)];
+  extern __shared__ __align__(16) unsigned char mix_smem[];  // GemmLds<T, BM, BN, BK>::bytes
+  T* smem = reinterpret_cast<T*>(mix_smem);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   // logical block = ((l, row tile), column tile), largest degrees first: all
@@ -450,32 +450,52 @@ hipError_t lat_fwd_t(const Plan& p, int B, int C, const void* X, void* coef, hip
   return lat_fwd_cfg<T, 32, 128, 1, 4>(p, B, C, X, coef, st);
 }
 
+// Workgroups of the mixing GEMM with BM x BN tiles.
+long long mix_blocks(const Plan& p, int B, int Cout, int BM, int BN) {
+  long long tiles = 0;
+  for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + BM - 1) / BM;
+  return tiles * ((2 * p.n_out * Cout + BN - 1) / BN);
+}
+
+// K step of the float mixing GEMM (bf16 uses SWSFT_BK_MIX).
+#ifndef SWSFT_BK_MIX_F32
+#define SWSFT_BK_MIX_F32 32
+#endif
+
 template <typename T, int BM, int BN, int WM, int WN>
 hipError_t mix_cfg(const Plan& p, int B, int Cin, int Cout, const void* coef, const void* K,
                    void* out, hipStream_t st) {
-  int tiles = 0;
-  for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + BM - 1) / BM;
   const int Np = 2 * p.n_out * Cout, Kp = 2 * p.n_in * Cin;
-  const long long blocks = (long long)tiles * ((Np + BN - 1) / BN);
+  const long long blocks = mix_blocks(p, B, Cout, BM, BN);
   constexpr int VEC = 16 / sizeof(T);
-  auto kern = (Kp % VEC == 0 && Np % VEC == 0) ? mix_kernel<T, BM, BN, kBK<T, SWSFT_BK_MIX>, WM, WN, true>
-                                               : mix_kernel<T, BM, BN, kBK<T, SWSFT_BK_MIX>, WM, WN, false>;
-  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(NT), 0, st, (const T*)coef, (const T*)K,
+  constexpr int BK = sizeof(T) == 2 ? SWSFT_BK_MIX : SWSFT_BK_MIX_F32;
+  auto kern = (Kp % VEC == 0 && Np % VEC == 0) ? mix_kernel<T, BM, BN, BK, WM, WN, true>
+                                               : mix_kernel<T, BM, BN, BK, WM, WN, false>;
+  const size_t lds = GemmLds<T, BM, BN, BK>::bytes;
+  const hipError_t e = ensure_dynamic_lds((const void*)kern, lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(NT), lds, st, (const T*)coef, (const T*)K,
                      (T*)out, p.L, B, Cin, Cout, p.n_in, p.n_out, make_spins(p.spins_in, p.n_in),
                      make_spins(p.spins_out, p.n_out));
   return hipGetLastError();
 }
 
-// Tile of the large-channel mixing GEMM (rows x columns, waves per dim).
-#ifndef SWSFT_MIX_TILE
-#define SWSFT_MIX_TILE 128, 128, 2, 2
-#endif
-
+// Tile of the large-channel mixing GEMM (rows x columns, waves per dim): the
+// largest of 128 x 128, 64 x 128 and 64 x 64 that still gives two
+// workgroups per CU (the degrees are few and short at small bandlimits, and
+// a 128 x 128 tiling then leaves CUs idle).
 template <typename T>
 hipError_t mix_t(const Plan& p, int B, int Cin, int Cout, const void* coef, const void* K,
                  void* out, hipStream_t st) {
   const int Np = 2 * p.n_out * Cout;
-  if (Np >= 128) return mix_cfg<T, SWSFT_MIX_TILE>(p, B, Cin, Cout, coef, K, out, st);
+  constexpr long long kWant = 2LL * 256;
+  if (Np >= 128) {
+    if (mix_blocks(p, B, Cout, 128, 128) >= kWant)
+      return mix_cfg<T, 128, 128, 2, 2>(p, B, Cin, Cout, coef, K, out, st);
+    if (mix_blocks(p, B, Cout, 64, 128) >= kWant)
+      return mix_cfg<T, 64, 128, 2, 2>(p, B, Cin, Cout, coef, K, out, st);
+    return mix_cfg<T, 64, 64, 2, 2>(p, B, Cin, Cout, coef, K, out, st);
+  }
   return mix_cfg<T, 128, 32, 4, 1>(p, B, Cin, Cout, coef, K, out, st);
 }
 

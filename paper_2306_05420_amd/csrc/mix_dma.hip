@@ -1,5 +1,6 @@
-// Per-degree mixing GEMM for bfloat16 storage, fed by direct global -> LDS
-// loads (global_load_lds_dwordx4) into a ring of LDS stages.
+// Per-degree mixing GEMM fed by direct global -> LDS loads
+// (global_load_lds_dwordx4) into a ring of LDS stages: bfloat16 storage
+// first, the float form below.
 //
 //   coef'[l][(m,b)][(t,c')] = sum_(s,c) coef[l][(m,b)][(s,c)] K[l][(t,c')][(s,c)]
 //
@@ -16,8 +17,8 @@
 // expanded GEMM rows) x RB filter rows (complex outputs) per workgroup, ST
 // K steps resident in LDS.  Each wave owns 64 expanded rows x 64 outputs.
 //
-// Preconditions (checked by the launcher): bf16, K' = 2 S_in C_in with each
-// input spin's channel block a whole number of BK-wide K steps, C_out % 4 == 0.
+// Preconditions (checked by the launcher): K' = 2 S_in C_in with each input
+// spin's channel block a whole number of K steps; bf16 also C_out % 4 == 0.
 #include "lds_dma.h"
 #include "mfma_tile.h"
 #include "swsft_internal.h"
@@ -221,6 +222,198 @@ hipError_t launch_geom(const Plan& p, int B, int Cin, int Cout, const void* coef
   return hipGetLastError();
 }
 
+// Float form.  K steps of 32 floats (16 complex entries: one 128-byte line
+// per row and copy).  Each of the 4 waves owns one block of 32 expanded rows
+// (16 coefficient rows) x two blocks of 32 outputs, MFMA 32x32x2 f32; the
+// workgroup covers WM x WN such wave tiles, i.e. 16 WM coefficient rows x
+// 64 WN outputs.  A lane's A value for row 2i (re, -im) / 2i+1 (im, re) is
+// picked from the 16-byte chunk of coefficient row i (two complex entries,
+// two MFMA steps) by the parity of its row and its K half; the filter rows
+// enter as stored (re, im).
+template <int WM, int WN, int ST>
+struct MixGeomF {
+  static constexpr int BK = 32;                 // floats per row per K step
+  static constexpr int PITCH = 4 * BK;          // bytes per tile row
+  static constexpr int CPR = PITCH / 16;        // 16-byte chunks per row
+  static constexpr int RPI = 1024 / PITCH;      // rows per 1 KiB copy
+  static constexpr int LPR = 64 / RPI;          // lanes per row
+  static constexpr int NW = WM * WN, NT = 64 * NW;
+  static constexpr int RA = 16 * WM, RB = 64 * WN;
+  static constexpr int NI = (RA + RB) / RPI;    // copies per stage
+  static constexpr int PER_WAVE = NI / NW;
+  static constexpr int STAGE = (RA + RB) * PITCH;
+  static constexpr int SMEM = ST * STAGE;
+  static constexpr int MAX_KT = kMaxKp / BK;
+  static_assert((RA + RB) % RPI == 0 && NI % NW == 0, "tile shape");
+  static_assert(ST >= 2 && (ST - 2) * PER_WAVE < 64, "stages");
+};
+
+template <int WM, int WN, int ST>
+__global__ void __launch_bounds__((MixGeomF<WM, WN, ST>::NT))
+    mix_dma_f32_kernel(const float* __restrict__ coef, const float* __restrict__ K,
+                       float* __restrict__ out, int L, int B, int Cin, int Cout, int Sin,
+                       int Sout, Spins sin_, Spins sout_) {
+  using G = MixGeomF<WM, WN, ST>;
+  constexpr int RA = G::RA, RB = G::RB, BK = G::BK;
+  extern __shared__ __align__(16) unsigned char smem[];  // G::SMEM bytes: the ring
+  __shared__ int live[G::MAX_KT];
+  __shared__ int n_live_s;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int Kc = Sin * Cin, Nc = Sout * Cout;
+  const int Kp = 2 * Kc;
+  const int n_tiles_n = (Nc + RB - 1) / RB;
+
+  // logical block = ((l, row tile), column tile), largest degrees first
+  const int lbk = xcd_logical_block();
+  const int ntile = lbk % n_tiles_n;
+  int t = lbk / n_tiles_n;
+  int l = L - 1;
+  for (; l >= 0; --l) {
+    const int ntl = ((2 * l + 1) * B + RA - 1) / RA;
+    if (t < ntl) break;
+    t -= ntl;
+  }
+  if (l < 0) return;
+  const int Mrows = (2 * l + 1) * B;
+  const int row0 = t * RA;
+  const int q0 = ntile * RB;
+
+  // K steps of input spins that exist at this degree (whole channel blocks)
+  if (tid == 0) {
+    const int per_spin = 2 * Cin / BK;
+    int n = 0;
+    for (int si = 0; si < Sin; ++si)
+      if (iabs_(sin_.s[si]) <= l)
+        for (int k = 0; k < per_spin; ++k) live[n++] = si * per_spin + k;
+    n_live_s = n;
+  }
+  __syncthreads();
+  const int nk = n_live_s;
+
+  const float* A0 = coef + (size_t)l * l * B * Kp;  // rows (m, b) of degree l
+  const float* K0 = K + (size_t)l * Nc * Kp;        // filter rows q of degree l
+  const unsigned ring_base = lds_addr(smem);
+
+  // copy g = wave * PER_WAVE + u moves tile rows [g RPI, (g + 1) RPI) of the
+  // stage [A rows; B rows]; rows past the end of a matrix are clamped to its
+  // last row (their products are discarded)
+  const float* gsrc[G::PER_WAVE];
+#pragma unroll
+  for (int u = 0; u < G::PER_WAVE; ++u) {
+    const int g = wave * G::PER_WAVE + u;
+    const int tr = g * G::RPI + lane / G::LPR;
+    const int slot = lane % G::LPR;
+    if (tr < RA) {
+      const int row = row0 + tr < Mrows ? row0 + tr : Mrows - 1;
+      gsrc[u] = A0 + (size_t)row * Kp + swz<G::CPR>(tr, slot) * 4;
+    } else {
+      const int rb = tr - RA;
+      const int q = q0 + rb < Nc ? q0 + rb : Nc - 1;
+      gsrc[u] = K0 + (size_t)q * Kp + swz<G::CPR>(rb, slot) * 4;
+    }
+  }
+  auto issue = [&](int i, int stage) {
+    const int koff = live[i] * BK;
+    const unsigned base = ring_base + stage * G::STAGE + wave * G::PER_WAVE * 1024;
+#pragma unroll
+    for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + koff, base + u * 1024);
+  };
+
+  v16f acc[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+
+#pragma unroll
+  for (int s = 0; s < ST - 1; ++s)
+    if (s < nk) issue(s, s);
+
+  const int r32 = lane & 31, kh = lane >> 5;
+  const int cr = wm * 16 + (r32 >> 1);      // coefficient row of this lane's A row
+  const bool sel_im = ((r32 & 1) ^ kh) != 0;  // (re, -im) / (im, re): which part
+  const float sgn = ((r32 & 1) == 0 && kh == 1) ? -1.f : 1.f;
+  for (int i = 0; i < nk; ++i) {
+    const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
+    wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
+    __builtin_amdgcn_s_barrier();  // every wave's copies of step i landed; step i-1 is consumed
+    if (i + ST - 1 < nk) issue(i + ST - 1, (i + ST - 1) % ST);
+    const unsigned char* As = smem + (i % ST) * G::STAGE;
+    const unsigned char* Bs = As + RA * G::PITCH;
+    auto lda = [&](int cc) {
+      return *reinterpret_cast<const float4*>(As + cr * G::PITCH + swz<G::CPR>(cr, cc) * 16);
+    };
+    auto ldb = [&](int jj, int cc) {
+      const int q = wn * 64 + jj * 32 + r32;
+      return *reinterpret_cast<const float4*>(Bs + q * G::PITCH + swz<G::CPR>(q, cc) * 16);
+    };
+    // chunk cc + 1 is read while the MFMAs of chunk cc run
+    float4 av = lda(0), bv0 = ldb(0, 0), bv1 = ldb(1, 0);
+#pragma unroll
+    for (int cc = 0; cc < G::CPR; ++cc) {  // two complex entries = two MFMA steps
+      float4 nav = av, nb0 = bv0, nb1 = bv1;
+      if (cc + 1 < G::CPR) {
+        nav = lda(cc + 1);
+        nb0 = ldb(0, cc + 1);
+        nb1 = ldb(1, cc + 1);
+      }
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const float a = sgn * (sel_im ? (e ? av.w : av.y) : (e ? av.z : av.x));
+        const float b0 = kh ? (e ? bv0.w : bv0.y) : (e ? bv0.z : bv0.x);
+        const float b1 = kh ? (e ? bv1.w : bv1.y) : (e ? bv1.z : bv1.x);
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b0, acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b1, acc[1], 0, 0, 0);
+      }
+      av = nav;
+      bv0 = nb0;
+      bv1 = nb1;
+      if (cc + 1 < G::CPR) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);  // LDS reads
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                       // MFMA
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  wait_vmcnt<0>();
+
+  // registers r and r + 1 (r even) of a lane hold expanded rows 2i and 2i + 1
+  // of its column q: the real and imaginary part of output (row0 + i, q0 + q)
+  const int col_l = lane & 31, row_l = 4 * (lane >> 5);
+#pragma unroll
+  for (int jj = 0; jj < 2; ++jj) {
+    const int q = q0 + wn * 64 + jj * 32 + col_l;
+    const bool qok = q < Nc;
+    const bool tok = qok && iabs_(sout_.s[(qok ? q : 0) / Cout]) <= l;
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) {
+      const int er = wm * 32 + 8 * (r >> 2) + row_l + (r & 3);  // even
+      const int row = row0 + (er >> 1);
+      if (!qok || row >= Mrows) continue;
+      const float2 v = tok ? make_float2(acc[jj][r], acc[jj][r + 1]) : make_float2(0.f, 0.f);
+      *reinterpret_cast<float2*>(out + ((size_t)l * l * B + row) * (2 * Nc) + 2 * q) = v;
+    }
+  }
+}
+
+template <int WM, int WN, int ST>
+hipError_t launch_geom_f32(const Plan& p, int B, int Cin, int Cout, const void* coef,
+                           const void* K, void* out, hipStream_t st) {
+  using G = MixGeomF<WM, WN, ST>;
+  Spins si{}, so{};
+  for (int i = 0; i < p.n_in; ++i) si.s[i] = p.spins_in[i];
+  for (int i = 0; i < p.n_out; ++i) so.s[i] = p.spins_out[i];
+  long long tiles = 0;
+  for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + G::RA - 1) / G::RA;
+  const int Nc = p.n_out * Cout;
+  const long long blocks = tiles * ((Nc + G::RB - 1) / G::RB);
+  const hipError_t e = ensure_dynamic_lds((const void*)mix_dma_f32_kernel<WM, WN, ST>, G::SMEM);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((mix_dma_f32_kernel<WM, WN, ST>), dim3(xcd_grid(blocks)), dim3(G::NT), G::SMEM, st,
+                     (const float*)coef, (const float*)K, (float*)out, p.L, B, Cin, Cout, p.n_in,
+                     p.n_out, si, so);
+  return hipGetLastError();
+}
+
 // Tile shape: 128 coefficient rows x 128 outputs, two 64-wide K steps
 // resident (two workgroups of 8 waves per CU); channel counts that are a
 // multiple of 16 but not of 32 take 32-wide K steps.
@@ -240,12 +433,17 @@ hipError_t launch_geom(const Plan& p, int B, int Cin, int Cout, const void* coef
 }  // namespace
 
 bool mix_dma_supported(const Plan& p, int Cin, int Cout) {
+  // float: outputs of at least 128 (narrower ones run as fast register-staged)
+  if (p.dtype == SWSFT_F32)
+    return (2 * Cin) % 32 == 0 && 2 * p.n_in * Cin <= kMaxKp && p.n_out * Cout >= 128;
   return p.dtype == SWSFT_BF16 && (2 * Cin) % 32 == 0 && 2 * p.n_in * Cin <= kMaxKp &&
          Cout % 4 == 0;
 }
 
 hipError_t launch_mix_dma(const Plan& p, int B, int Cin, int Cout, const void* coef,
                           const void* K, void* out, hipStream_t st) {
+  // float: 32 coefficient rows x 128 outputs, 3 K steps resident
+  if (p.dtype == SWSFT_F32) return launch_geom_f32<2, 2, 3>(p, B, Cin, Cout, coef, K, out, st);
   if ((2 * Cin) % SWSFT_MIX_DMA_BK == 0)
     return launch_geom<SWSFT_MIX_DMA_BK, SWSFT_MIX_DMA_RA, SWSFT_MIX_DMA_RB, SWSFT_MIX_DMA_STAGES>(
         p, B, Cin, Cout, coef, K, out, st);

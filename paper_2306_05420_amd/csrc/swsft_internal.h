@@ -161,7 +161,7 @@ hipError_t launch_lat_fwd_dma(const Plan& p, int B, int C, const void* X, void* 
                               hipStream_t st);
 hipError_t launch_lat_inv_dma(const Plan& p, int B, int C, const void* coef, void* Y,
                               hipStream_t st);
-// bf16 mixing fed by direct global -> LDS copies (see mix_dma.hip).
+// Mixing fed by direct global -> LDS copies (bf16 and float; see mix_dma.hip).
 bool mix_dma_supported(const Plan& p, int C_in, int C_out);
 hipError_t launch_mix_dma(const Plan& p, int B, int C_in, int C_out, const void* coef,
                           const void* K, void* coef_out, hipStream_t st);
