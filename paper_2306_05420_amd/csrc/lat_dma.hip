@@ -1,6 +1,6 @@
-// Latitude stages of the transform for bfloat16 storage, as GEMMs whose
-// operands are copied global -> LDS directly (global_load_lds_dwordx4; see
-// lds_dma.h) into a ring of K steps.
+// Latitude stages of the transform (bfloat16 storage; the forward also for
+// float storage), as GEMMs whose operands are copied global -> LDS directly
+// (global_load_lds_dwordx4; see lds_dma.h) into a ring of K steps.
 //
 //   forward  coef[l][m][b][s][c] = sum_j Tf[s][m][l][j] X[s][m][j][b c]      (eq. (4))
 //   inverse  Y[s][m][j][b c]     = sum_l Ti[s][m][j][l] coef'[l][m][b][s][c]  (eq. (3))
@@ -196,6 +196,163 @@ __global__ void __launch_bounds__((FwdGeom<BK, RA, RB, ST>::NT))
   }
 }
 
+// Float forward: K steps of 32 latitudes (128 bytes per row and copy); each
+// of the 4 waves owns 32 rows l x 64 columns n' (two MFMA 32x32x2 chains, a
+// lane's two K values of a step taken from one 16-byte chunk); the
+// workgroup covers 32 WM rows x 64 WN columns.
+template <int WM, int WN, int ST>
+struct FwdGeomF {
+  static constexpr int BK = 32, PITCH = 4 * BK, CPR = PITCH / 16;
+  static constexpr int RPI = 1024 / PITCH, LPR = 64 / RPI;
+  static constexpr int NW = WM * WN, NT = 64 * NW;
+  static constexpr int RA = 32 * WM, RB = 64 * WN;
+  static constexpr int NI = (RA + RB) / RPI, PER_WAVE = NI / NW;
+  static constexpr int STAGE = (RA + RB) * PITCH;
+  static constexpr int LDC = RB + 4;  // floats per row of the output tile
+  static constexpr int RING = ST * STAGE, CTILE = RA * LDC * 4;
+  static constexpr int SMEM = RING > CTILE ? RING : CTILE;
+  static_assert(BK == kJT && (RA + RB) % RPI == 0 && NI % NW == 0 && ST >= 1 &&
+                    (ST - 2) * PER_WAVE < 64,
+                "tile shape");
+};
+
+template <int WM, int WN, int ST>
+__global__ void __launch_bounds__((FwdGeomF<WM, WN, ST>::NT))
+    lat_fwd_dma_f32_kernel(const float* __restrict__ X, const float* __restrict__ tab,
+                           float* __restrict__ coef, int L, int H, int B, int C, int S,
+                           int n_row_tiles, int n_tiles_n) {
+  using G = FwdGeomF<WM, WN, ST>;
+  constexpr int RA = G::RA, RB = G::RB, BK = G::BK;
+  extern __shared__ __align__(16) unsigned char smem[];  // G::SMEM bytes
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int M = 2 * L - 1;
+  // logical block = ((s, order, row tile), column tile), as for bf16
+  int lbk = xcd_logical_block();
+  if (lbk >= S * M * n_row_tiles * n_tiles_n) return;
+  const int nt = lbk % n_tiles_n;
+  lbk /= n_tiles_n;
+  const int rt = lbk % n_row_tiles;
+  lbk /= n_row_tiles;
+  const int mi = mixed_order(lbk % M, L), si = lbk / M;
+  const int m = mi - (L - 1);
+  const int l_begin = iabs_(m) + rt * RA;
+  if (l_begin >= L) return;
+  const int Np = 2 * B * C;
+  const int n0 = nt * RB;
+  const float* A0 = tab + (size_t)(si * M + mi) * L * H;  // rows l of H latitudes
+  const float* B0 = X + (size_t)(si * M + mi) * Np * H;   // [H/32][Np][32]
+
+  const float* src[G::PER_WAVE];
+  int step[G::PER_WAVE];  // elements between consecutive K steps
+#pragma unroll
+  for (int u = 0; u < G::PER_WAVE; ++u) {
+    const int g = wave * G::PER_WAVE + u;
+    const int tr = g * G::RPI + lane / G::LPR, slot = lane % G::LPR;
+    if (tr < RA) {
+      const int l = imin_(l_begin + tr, L - 1);
+      src[u] = A0 + (size_t)l * H + swz<G::CPR>(tr, slot) * 4;
+      step[u] = BK;
+    } else {
+      const int rb = tr - RA;
+      const int np = imin_(n0 + rb, Np - 1);
+      src[u] = B0 + (size_t)np * kJT + swz<G::CPR>(rb, slot) * 4;
+      step[u] = Np * kJT;
+    }
+  }
+  const unsigned ring = lds_addr(smem);
+  auto issue = [&](int i, int stage) {
+    const unsigned base = ring + stage * G::STAGE + wave * G::PER_WAVE * 1024;
+#pragma unroll
+    for (int u = 0; u < G::PER_WAVE; ++u) dma16(src[u] + (size_t)i * step[u], base + u * 1024);
+  };
+
+  v16f acc[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+  const int nk = H / BK;
+#pragma unroll
+  for (int s = 0; s < ST - 1; ++s)
+    if (s < nk) issue(s, s);
+  const int r32 = lane & 31, kh = lane >> 5;
+  const int ra = wm * 32 + r32;
+  if constexpr (ST == 1) issue(0, 0);  // one stage: a single K step (checked by the launcher)
+  for (int i = 0; i < nk; ++i) {
+    if constexpr (ST == 1) {
+      wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+    } else {
+      const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
+      wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
+      __builtin_amdgcn_s_barrier();  // step i landed for every wave; step i-1 is consumed
+      if (i + ST - 1 < nk) issue(i + ST - 1, (i + ST - 1) % ST);
+    }
+    const unsigned char* As = smem + (i % ST) * G::STAGE;
+    const unsigned char* Bs = As + RA * G::PITCH;
+    auto lda = [&](int cc) {
+      return *reinterpret_cast<const float4*>(As + ra * G::PITCH + swz<G::CPR>(ra, cc) * 16);
+    };
+    auto ldb = [&](int jj, int cc) {
+      const int r = wn * 64 + jj * 32 + r32;
+      return *reinterpret_cast<const float4*>(Bs + r * G::PITCH + swz<G::CPR>(r, cc) * 16);
+    };
+    // chunk cc + 1 is read while the MFMAs of chunk cc run
+    float4 av = lda(0), bv0 = ldb(0, 0), bv1 = ldb(1, 0);
+#pragma unroll
+    for (int cc = 0; cc < G::CPR; ++cc) {  // four latitudes = two MFMA steps
+      float4 nav = av, nb0 = bv0, nb1 = bv1;
+      if (cc + 1 < G::CPR) {
+        nav = lda(cc + 1);
+        nb0 = ldb(0, cc + 1);
+        nb1 = ldb(1, cc + 1);
+      }
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const float a = kh ? (e ? av.w : av.y) : (e ? av.z : av.x);
+        const float b0 = kh ? (e ? bv0.w : bv0.y) : (e ? bv0.z : bv0.x);
+        const float b1 = kh ? (e ? bv1.w : bv1.y) : (e ? bv1.z : bv1.x);
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b0, acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b1, acc[1], 0, 0, 0);
+      }
+      av = nav;
+      bv0 = nb0;
+      bv1 = nb1;
+      if (cc + 1 < G::CPR) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);  // LDS reads
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                       // MFMA
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  // epilogue: rows l, columns n' = (b, c, re/im) through LDS; 4 columns stay
+  // inside one b because 2C is a multiple of 4
+  float* cs = reinterpret_cast<float*>(smem);
+  {
+    const int col_l = lane & 31, row_l = 4 * (lane >> 5);
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        cs[(wm * 32 + 8 * (r >> 2) + row_l + (r & 3)) * G::LDC + wn * 64 + jj * 32 + col_l] =
+            acc[jj][r];
+  }
+  __syncthreads();
+  const int twoC = 2 * C;
+  constexpr int VPR = RB / 4;
+  for (int idx = tid; idx < RA * VPR; idx += G::NT) {
+    const int row = idx / VPR, col = (idx % VPR) * 4;
+    const int l = l_begin + row, np = n0 + col;
+    if (l >= L || np >= Np) continue;
+    const int b = np / twoC, rem = np - b * twoC;
+    *reinterpret_cast<float4*>(&coef[((size_t)(l * l + l + m) * B + b) * S * twoC +
+                                     (size_t)si * twoC + rem]) =
+        *reinterpret_cast<const float4*>(&cs[row * G::LDC + col]);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // inverse
 // ---------------------------------------------------------------------------
@@ -385,6 +542,20 @@ hipError_t fwd_geom(const Plan& p, int B, int C, const void* X, void* coef, hipS
   return hipGetLastError();
 }
 
+template <int WM, int WN, int ST>
+hipError_t fwd_geom_f32(const Plan& p, int B, int C, const void* X, void* coef, hipStream_t st) {
+  using G = FwdGeomF<WM, WN, ST>;
+  const int Np = 2 * B * C;
+  const int nrt = (p.L + G::RA - 1) / G::RA, nnt = (Np + G::RB - 1) / G::RB;
+  const long long blocks = (long long)p.n_in * p.M * nrt * nnt;
+  auto kern = lat_fwd_dma_f32_kernel<WM, WN, ST>;
+  const hipError_t e = ensure_dynamic_lds((const void*)kern, G::SMEM);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(G::NT), G::SMEM, st, (const float*)X,
+                     (const float*)p.tab_fwd, (float*)coef, p.L, p.H, B, C, p.n_in, nrt, nnt);
+  return hipGetLastError();
+}
+
 template <int RA, int RB, int ST>
 hipError_t inv_geom(const Plan& p, int B, int C, const void* coef, void* Y, hipStream_t st) {
   const int Np = 2 * B * C;
@@ -411,6 +582,10 @@ constexpr int inv_ra(int) { return RA; }
 bool lat_fwd_dma_supported(const Plan& p, int B, int C) {
   constexpr int BK = fwd_bk<SWSFT_LAT_FWD_DMA>(0);
   static_assert(fwd_bk<SWSFT_LAT_FWD_DMA_WIDE>(0) == BK, "wide tile");
+  // float: columns 2BC >= 1024 (narrower ones leave too few workgroups; the
+  // register-staged kernel takes them)
+  if (p.dtype == SWSFT_F32)
+    return p.H % kJT == 0 && p.Hp == p.H && p.JT == kJT && C % 2 == 0 && 2 * B * C >= 1024;
   return p.dtype == SWSFT_BF16 && p.H >= BK && p.H % BK == 0 && p.Hp == p.H && p.JT == kJT &&
          (2 * C) % 8 == 0;
 }
@@ -424,6 +599,14 @@ bool lat_inv_dma_supported(const Plan& p, int B, int C) {
 
 hipError_t launch_lat_fwd_dma(const Plan& p, int B, int C, const void* X, void* coef,
                               hipStream_t st) {
+  // float: 32 rows l x 256 columns while L <= 32, else 64 x 128; a single
+  // K step (H = 32) needs a single stage, which leaves room for 4 workgroups
+  // per CU
+  if (p.dtype == SWSFT_F32) {
+    if (p.H == kJT) return fwd_geom_f32<1, 4, 1>(p, B, C, X, coef, st);
+    if (p.L <= 32) return fwd_geom_f32<1, 4, 2>(p, B, C, X, coef, st);
+    return fwd_geom_f32<2, 2, 3>(p, B, C, X, coef, st);
+  }
   if ((2 * B * C) % fwd_rb<SWSFT_LAT_FWD_DMA_WIDE>(0) == 0)
     return fwd_geom<SWSFT_LAT_FWD_DMA_WIDE>(p, B, C, X, coef, st);
   return fwd_geom<SWSFT_LAT_FWD_DMA>(p, B, C, X, coef, st);
