@@ -1,5 +1,5 @@
-// Latitude stages of the transform (bfloat16 storage; the forward also for
-// float storage), as GEMMs whose operands are copied global -> LDS directly
+// Latitude stages of the transform (bfloat16 and float storage), as GEMMs
+// whose operands are copied global -> LDS directly
 // (global_load_lds_dwordx4; see lds_dma.h) into a ring of K steps.
 //
 //   forward  coef[l][m][b][s][c] = sum_j Tf[s][m][l][j] X[s][m][j][b c]      (eq. (4))
@@ -516,6 +516,193 @@ __global__ void __launch_bounds__((InvGeom<RA, RB, ST>::NT))
   }
 }
 
+// Float inverse: K steps of 32 degrees.  The coefficient tile enters LDS
+// K-major ([l][n'], 4 RA bytes per degree row, 16-byte chunks of odd rows
+// moved by 128 bytes so that the two K halves of a read hit different banks)
+// and a lane reads its n' at degree 2 step + K half as one float; the table
+// rows j (K = l contiguous) give both K values of two steps in one 16-byte
+// chunk.  Each wave owns TM x TN (TM TN = 2) MFMA 32x32x2 blocks of
+// (n', j); the n' tile may span several batch items (a lane keeps its own
+// column offset, only the degree row moves per K step).
+template <int TM, int WM, int WN, int ST>
+struct InvGeomF {
+  static constexpr int BK = 32;  // degrees per K step
+  static constexpr int TN = 2 / TM;
+  static constexpr int NW = WM * WN, NT = 64 * NW;
+  static constexpr int RA = 32 * TM * WM, RB = 32 * TN * WN;  // n' rows, j columns
+  static constexpr int PITCH_A = 4 * RA, CPR_A = PITCH_A / 16;
+  static constexpr int RPI_A = 1024 / PITCH_A, LPR_A = 64 / RPI_A;
+  static constexpr int PITCH_B = 4 * BK, CPR_B = PITCH_B / 16;
+  static constexpr int RPI_B = 1024 / PITCH_B, LPR_B = 64 / RPI_B;
+  static constexpr int A_BYTES = BK * PITCH_A, B_BYTES = RB * PITCH_B;
+  static constexpr int NI_A = A_BYTES / 1024, NI = NI_A + B_BYTES / 1024;
+  static constexpr int PER_WAVE = NI / NW;
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int LDC = RB + 4;  // floats per row of the output tile
+  static constexpr int RING = ST * STAGE, CTILE = RA * LDC * 4;
+  static constexpr int SMEM = RING > CTILE ? RING : CTILE;
+  static_assert(TM * TN == 2 && PITCH_A >= 256 && PITCH_A <= 1024 && B_BYTES % 1024 == 0 &&
+                    NI % NW == 0 && ST >= 1 && (ST - 2) * PER_WAVE < 64,
+                "tile shape");
+};
+
+// chunk slot of a degree row of the float coefficient tile
+__device__ __forceinline__ int swa(int k, int c) { return c ^ ((k & 1) << 3); }
+
+template <int TM, int WM, int WN, int ST>
+__global__ void __launch_bounds__((InvGeomF<TM, WM, WN, ST>::NT))
+    lat_inv_dma_f32_kernel(const float* __restrict__ coef, const float* __restrict__ tab,
+                           float* __restrict__ Y, int L, int H, int Lp, int B, int Bc, int C,
+                           int S, SpinList sout_, int n_tiles_n) {
+  using G = InvGeomF<TM, WM, WN, ST>;
+  constexpr int BK = G::BK, TN = G::TN, RA = G::RA, RB = G::RB;
+  extern __shared__ __align__(16) unsigned char smem[];  // G::SMEM bytes
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int M = 2 * L - 1;
+  // logical block = ((s, order, j tile), n' tile), as for bf16
+  const int n_tiles_j = (H + RB - 1) / RB;
+  int lbk = xcd_logical_block();
+  if (lbk >= S * M * n_tiles_j * n_tiles_n) return;
+  const int nt = lbk % n_tiles_n;
+  lbk /= n_tiles_n;
+  const int jt = lbk % n_tiles_j;
+  lbk /= n_tiles_j;
+  const int mi = mixed_order(lbk % M, L), si = lbk / M;
+  const int m = mi - (L - 1);
+  const int spin = sout_.s[si];
+  const int lo = iabs_(m) > iabs_(spin) ? iabs_(m) : iabs_(spin);
+  const int Np = 2 * B * C, twoC = 2 * C;
+  const int n0 = nt * RA, j0 = jt * RB;
+  const int kb = (lo / BK) * BK;
+  const int nk = (Lp - kb) / BK;  // Lp is a multiple of BK; table columns >= L are zero
+  const float* Tb = tab + (size_t)(si * M + mi) * H * Lp;
+  const size_t row_elems = (size_t)Bc * S * twoC;  // elements per coefficient row (l, m)
+
+  // copies g < NI_A: coefficient degree rows k of the step, this lane's chunk
+  // of n' (its batch item and offset fixed); copies g >= NI_A: table rows j
+  int ka[G::PER_WAVE];
+  size_t coff[G::PER_WAVE];
+  const float* bsrc[G::PER_WAVE];
+#pragma unroll
+  for (int u = 0; u < G::PER_WAVE; ++u) {
+    const int g = wave * G::PER_WAVE + u;
+    if (g < G::NI_A) {
+      const int k = g * G::RPI_A + lane / G::LPR_A;
+      const int np = imin_(n0 + 4 * swa(k, lane % G::LPR_A), Np - 4);
+      const int b = np / twoC, rem = np - b * twoC;
+      ka[u] = k;
+      coff[u] = (size_t)b * S * twoC + (size_t)si * twoC + rem;
+      bsrc[u] = nullptr;
+    } else {
+      const int gb = g - G::NI_A;
+      const int tr = gb * G::RPI_B + lane / G::LPR_B, slot = lane % G::LPR_B;
+      const int j = imin_(j0 + tr, H - 1);
+      ka[u] = 0;
+      coff[u] = 0;
+      bsrc[u] = Tb + (size_t)j * Lp + kb + swz<G::CPR_B>(tr, slot) * 4;
+    }
+  }
+  const unsigned ring = lds_addr(smem);
+  auto issue = [&](int i, int stage) {
+    const unsigned base = ring + stage * G::STAGE + wave * G::PER_WAVE * 1024;
+#pragma unroll
+    for (int u = 0; u < G::PER_WAVE; ++u) {
+      const float* p;
+      if (wave * G::PER_WAVE + u < G::NI_A) {
+        int l = kb + i * BK + ka[u];
+        l = l < lo ? lo : l;
+        l = l > L - 1 ? L - 1 : l;  // last, so that a row of the array is read even if lo >= L
+        p = coef + (size_t)(l * l + l + m) * row_elems + coff[u];
+      } else {
+        p = bsrc[u] + i * BK;
+      }
+      dma16(p, base + u * 1024);
+    }
+  };
+
+  v16f acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+#pragma unroll
+  for (int s = 0; s < ST - 1; ++s)
+    if (s < nk) issue(s, s);
+  if constexpr (ST == 1) issue(0, 0);  // one stage: a single K step (checked by the launcher)
+  const int r32 = lane & 31, kh = lane >> 5;
+  for (int i = 0; i < nk; ++i) {
+    if constexpr (ST == 1) {
+      wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+    } else {
+      const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
+      wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
+      __builtin_amdgcn_s_barrier();
+      if (i + ST - 1 < nk) issue(i + ST - 1, (i + ST - 1) % ST);
+    }
+    const unsigned char* As = smem + (i % ST) * G::STAGE;
+    const unsigned char* Bs = As + G::A_BYTES;
+    auto lda = [&](int ii, int k) {  // A[n'][degree k] of this lane's row block ii
+      const int n = wm * 32 * TM + ii * 32 + r32;
+      return *reinterpret_cast<const float*>(As + k * G::PITCH_A + swa(k, n >> 2) * 16 + (n & 3) * 4);
+    };
+    auto ldb = [&](int jj, int cc) {
+      const int r = wn * 32 * TN + jj * 32 + r32;
+      return *reinterpret_cast<const float4*>(Bs + r * G::PITCH_B + swz<G::CPR_B>(r, cc) * 16);
+    };
+#pragma unroll
+    for (int cc = 0; cc < G::CPR_B; ++cc) {  // four degrees = two MFMA steps
+      float4 bv[TN];
+#pragma unroll
+      for (int jj = 0; jj < TN; ++jj) bv[jj] = ldb(jj, cc);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        float a[TM];
+#pragma unroll
+        for (int ii = 0; ii < TM; ++ii) a[ii] = lda(ii, 4 * cc + 2 * e + kh);
+#pragma unroll
+        for (int jj = 0; jj < TN; ++jj) {
+          const float b = kh ? (e ? bv[jj].w : bv[jj].y) : (e ? bv[jj].z : bv[jj].x);
+#pragma unroll
+          for (int ii = 0; ii < TM; ++ii)
+            acc[ii][jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[ii], b, acc[ii][jj], 0, 0, 0);
+        }
+      }
+    }
+  }
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  // epilogue: rows n', columns j through LDS; Y K-tiled [H/32][Np][32]: 4
+  // consecutive j of one n' are one 16-byte vector inside a latitude tile
+  float* cs = reinterpret_cast<float*>(smem);
+  {
+    const int col_l = lane & 31, row_l = 4 * (lane >> 5);
+#pragma unroll
+    for (int ii = 0; ii < TM; ++ii)
+#pragma unroll
+      for (int jj = 0; jj < TN; ++jj)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          cs[(wm * 32 * TM + ii * 32 + 8 * (r >> 2) + row_l + (r & 3)) * G::LDC + wn * 32 * TN +
+             jj * 32 + col_l] = acc[ii][jj][r];
+  }
+  __syncthreads();
+  float* Y0 = Y + (size_t)(si * M + mi) * Np * H;
+  const size_t tstride = (size_t)Np * kJT;
+  constexpr int VPR = RB / 4;
+  for (int idx = tid; idx < RA * VPR; idx += G::NT) {
+    const int row = idx / VPR, col = (idx % VPR) * 4;
+    const int np = n0 + row, j = j0 + col;
+    if (np >= Np || j >= H) continue;
+    *reinterpret_cast<float4*>(Y0 + (j / kJT) * tstride + (size_t)np * kJT + j % kJT) =
+        *reinterpret_cast<const float4*>(&cs[row * G::LDC + col]);
+  }
+}
+
 // forward: BK, rows l, columns n', stages; the wide tile when 2BC allows it
 #ifndef SWSFT_LAT_FWD_DMA_WIDE
 #define SWSFT_LAT_FWD_DMA_WIDE 32, 128, 256, 3
@@ -570,6 +757,23 @@ hipError_t inv_geom(const Plan& p, int B, int C, const void* coef, void* Y, hipS
   return hipGetLastError();
 }
 
+template <int TM, int WM, int WN, int ST>
+hipError_t inv_geom_f32(const Plan& p, int B, int C, const void* coef, void* Y, hipStream_t st) {
+  using G = InvGeomF<TM, WM, WN, ST>;
+  const int Np = 2 * B * C;
+  const int nnt = (Np + G::RA - 1) / G::RA, njt = (p.H + G::RB - 1) / G::RB;
+  const long long blocks = (long long)p.n_out * p.M * njt * nnt;
+  SpinList so{};
+  for (int i = 0; i < p.n_out; ++i) so.s[i] = p.spins_out[i];
+  auto kern = lat_inv_dma_f32_kernel<TM, WM, WN, ST>;
+  const hipError_t e = ensure_dynamic_lds((const void*)kern, G::SMEM);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(G::NT), G::SMEM, st, (const float*)coef,
+                     (const float*)p.tab_inv, (float*)Y, p.L, p.H, p.Lp, B,
+                     p.coef_ldb > 0 ? p.coef_ldb : B, C, p.n_out, so, nnt);
+  return hipGetLastError();
+}
+
 template <int BK, int RA, int RB, int ST>
 constexpr int fwd_bk(int) { return BK; }
 template <int BK, int RA, int RB, int ST>
@@ -593,6 +797,10 @@ bool lat_fwd_dma_supported(const Plan& p, int B, int C) {
 bool lat_inv_dma_supported(const Plan& p, int B, int C) {
   constexpr int RA = inv_ra<SWSFT_LAT_INV_DMA>(0);
   static_assert(inv_ra<SWSFT_LAT_INV_DMA_WIDE>(0) % RA == 0, "wide tile");
+  // float: columns 2BC >= 1024, as for the forward
+  if (p.dtype == SWSFT_F32)
+    return p.H % kJT == 0 && p.JT == kJT && p.Hp == p.H && p.Lp % 32 == 0 && C % 2 == 0 &&
+           2 * B * C >= 1024;
   return p.dtype == SWSFT_BF16 && p.H % kJT == 0 && p.JT == kJT && (2 * C) % RA == 0 &&
          p.Lp % InvGeom<SWSFT_LAT_INV_DMA>::BK == 0 && p.Hp == p.H;
 }
@@ -614,6 +822,12 @@ hipError_t launch_lat_fwd_dma(const Plan& p, int B, int C, const void* X, void* 
 
 hipError_t launch_lat_inv_dma(const Plan& p, int B, int C, const void* coef, void* Y,
                               hipStream_t st) {
+  // float: 256 n' x 32 j in one stage when H = 32 (then L <= 16 < 32: one K
+  // step); else 64 n' x 128 j with two stages
+  if (p.dtype == SWSFT_F32) {
+    if (p.H == kJT) return inv_geom_f32<2, 4, 1, 1>(p, B, C, coef, Y, st);
+    return inv_geom_f32<1, 2, 2, 2>(p, B, C, coef, Y, st);
+  }
   if ((2 * C) % inv_ra<SWSFT_LAT_INV_DMA_WIDE>(0) == 0)
     return inv_geom<SWSFT_LAT_INV_DMA_WIDE>(p, B, C, coef, Y, st);
   return inv_geom<SWSFT_LAT_INV_DMA>(p, B, C, coef, Y, st);
