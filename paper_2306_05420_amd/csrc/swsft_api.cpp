@@ -399,25 +399,22 @@ swsft_status forward_stages(Plan& p, int B, int C, const void* x, void* X, void*
 // longitude DFT that reads them.
 constexpr size_t kCacheResidentBytes = size_t(128) << 20;
 
-// The inverse transform coef -> y (see forward_stages).  When the spectrum Y
-// of the whole batch exceeds kCacheResidentBytes, synthesis and inverse DFT
-// alternate over batch ranges whose Y fits, so the DFT reads Y from the
-// cache instead of HBM.
-swsft_status inverse_stages(Plan& p, int B, int C, const void* coef, void* Y, void* D, void* y,
-                            hipStream_t st) {
-  if (swsft::small_path(p, 1))
-    return run_stage(p, swsft::kStageSmallInv, st, "small_inv", [&] {
-      return swsft::launch_small_inv(p, B, 1, C, coef, nullptr, y, st);
-    });
-  if (!swsft::is_delta(p)) {
+// Latitude synthesis and inverse DFT, coef -> y, on the output spins of p
+// (direct latitude route; stage times are recorded on tp, the caller's
+// plan).  When the spectrum Y of the whole batch exceeds kCacheResidentBytes,
+// the two alternate over batch ranges whose Y fits, so the DFT reads Y from
+// the cache instead of HBM.
+swsft_status synthesis_stages(Plan& tp, const Plan& p, int B, int C, const void* coef, void* Y,
+                              void* y, hipStream_t st) {
+  {
     const size_t per_item = swsft::xy_elems(p, p.n_out, 1, C) * p.elem;
     int bc = per_item == 0 ? B : (int)(kCacheResidentBytes / per_item);
     bc = bc < 1 ? 1 : (bc > B ? B : bc);
     if (((size_t)p.n_out * 2 * C * p.elem) % 16 != 0) bc = B;  // batch offsets keep 16-byte rows
     if (bc >= B) {
-      SWSFT_TRY(run_stage(p, swsft::kStageLatInv, st, "lat_inv",
+      SWSFT_TRY(run_stage(tp, swsft::kStageLatInv, st, "lat_inv",
                           [&] { return swsft::launch_lat_inv(p, B, C, coef, Y, st); }));
-      return run_stage(p, swsft::kStageDftInv, st, "dft_inv",
+      return run_stage(tp, swsft::kStageDftInv, st, "dft_inv",
                        [&] { return swsft::launch_dft_inv(p, p.n_out, B, C, Y, y, st); });
     }
     Plan v = p;
@@ -428,12 +425,24 @@ swsft_status inverse_stages(Plan& p, int B, int C, const void* coef, void* Y, vo
       const int n = B - b0 < bc ? B - b0 : bc;
       const void* cb = static_cast<const char*>(coef) + b0 * coef_step;
       void* yb = static_cast<char*>(y) + b0 * y_step;
-      SWSFT_TRY(run_stage(p, swsft::kStageLatInv, st, "lat_inv",
+      SWSFT_TRY(run_stage(tp, swsft::kStageLatInv, st, "lat_inv",
                           [&] { return swsft::launch_lat_inv(v, n, C, cb, Y, st); }));
-      SWSFT_TRY(run_stage(p, swsft::kStageDftInv, st, "dft_inv",
+      SWSFT_TRY(run_stage(tp, swsft::kStageDftInv, st, "dft_inv",
                           [&] { return swsft::launch_dft_inv(p, p.n_out, n, C, Y, yb, st); }));
     }
     return SWSFT_OK;
+  }
+}
+
+// The inverse transform coef -> y (see forward_stages).
+swsft_status inverse_stages(Plan& p, int B, int C, const void* coef, void* Y, void* D, void* y,
+                            hipStream_t st) {
+  if (swsft::small_path(p, 1))
+    return run_stage(p, swsft::kStageSmallInv, st, "small_inv", [&] {
+      return swsft::launch_small_inv(p, B, 1, C, coef, nullptr, y, st);
+    });
+  if (!swsft::is_delta(p)) {
+    return synthesis_stages(p, p, B, C, coef, Y, y, st);
   } else {
     Plan v = p;
     v.H = v.Hp = swsft::delta_rows(p);
@@ -664,11 +673,9 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
     SWSFT_TRY(run_stage(*p, swsft::kStageMix, st, "mix", [&] {
       return swsft::launch_mix(adj, B, C_out, C_in, g_out, KH, g_in, st);
     }));
-    SWSFT_TRY(run_stage(*p, swsft::kStageLatInv, st, "lat_inv",
-                        [&] { return swsft::launch_lat_inv(syn, B, C_in, g_in, XY, st); }));
-    SWSFT_TRY(run_stage(*p, swsft::kStageDftInv, st, "dft_inv", [&] {
-      return swsft::launch_dft_inv(*p, p->n_in, B, C_in, XY, grad_x, st);
-    }));
+    // F^H: the synthesis with the weighted table on the input spins, over
+    // cache-sized batch ranges like the layer's inverse
+    SWSFT_TRY(synthesis_stages(*p, syn, B, C_in, g_in, XY, grad_x, st));
   }
   return SWSFT_OK;
 }
