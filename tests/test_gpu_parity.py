@@ -194,6 +194,12 @@ EDGE = [
     (64, 32, (1, -2), (2, 0), 2, 64, 64, "bf16"),     # |s| = 2: degree ranges start at max(|m|, |s|)
     (64, 32, (1,), (0, -1), 1, 33, 17, "f32"),     # ragged tiles everywhere
     (64, 20, (0,), (0,), 3, 8, 8, "f32"),          # spectral truncation L << H/2
+    # f32 through the direct-to-LDS kernels (2 B C >= 1024, S_out C_out >= 128):
+    (64, 32, (0, 1), (0, 1, 2), 4, 128, 132, "f32"),  # mixing: ragged outputs, dead output spin
+                                                       # below l = 2; inverse: ragged n' tiles that
+                                                       # span batch items
+    (32, 16, (1, 0), (0, -1), 4, 130, 128, "f32"),    # one-stage latitude GEMMs (H = 32), ragged
+                                                       # forward columns
 ]
 
 
