@@ -229,7 +229,10 @@ swsft_status spin_sph_conv_forward_train(swsft_plan p, int B, int C_in, int C_ou
  *  bias  [C] complex float.
  *  y     [B][S_out][C][H][W] complex, written; y == x (in place) is allowed,
  *        any other overlap is not.
- * Returns SWSFT_E_INVALID if spin 0 is not in spins_out.
+ *  W1, W2 and bias must be 8-byte aligned, x and y 16-byte aligned.
+ * Returns SWSFT_E_INVALID if spin 0 is not in spins_out, SWSFT_E_UNSUPPORTED
+ * if C exceeds the channel count whose staging fits one CU's LDS for S_out
+ * spins (160 for two spins).
  */
 swsft_status spin_sph_phase_collapse(swsft_plan p, int B, int C, const void* x,
                                      const void* W1, const void* W2, const void* bias,
