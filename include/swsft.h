@@ -358,7 +358,7 @@ const char* swsft_stage_name(int stage);
  *           up to a multiple of 8 (padding columns are 0).
  *  which 1: inverse table, [2L-1][H][Lp] per spins_out entry:
  *           (-1)^s sqrt((2l+1)/(4 pi)) d^l_{m,-s}(theta_j), Lp = L rounded
- *           up to a multiple of 8.
+ *           up to a multiple of 32 (padding columns are 0).
  *  which 2: backward synthesis table, [2L-1][H][Lp] per spins_in entry: the
  *           values of table 0 in the layout of table 1.
  *  which 3: backward analysis table, [2L-1][L][Hp] per spins_out entry: the

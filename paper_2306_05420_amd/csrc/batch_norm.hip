@@ -127,6 +127,55 @@ __global__ void __launch_bounds__(kNT) bn_finalize_kernel(const float* __restric
   if (var_out != nullptr) var_out[col] = var;
 }
 
+// 4 whole complex values as one 16-byte (bf16) or two 16-byte (float)
+// accesses; n < 4 values fall back to element accesses
+template <typename T>
+__device__ __forceinline__ void ld4(const T* p, long long i0, int n, float2 (&v)[4]) {
+  if (n == 4) {
+    if constexpr (sizeof(T) == 4) {
+      const float4 u = *reinterpret_cast<const float4*>(p + 2 * i0);
+      const float4 w = *reinterpret_cast<const float4*>(p + 2 * i0 + 4);
+      v[0] = make_float2(u.x, u.y); v[1] = make_float2(u.z, u.w);
+      v[2] = make_float2(w.x, w.y); v[3] = make_float2(w.z, w.w);
+    } else {
+      typedef __bf16 v8b __attribute__((ext_vector_type(8)));
+      const v8b u = *reinterpret_cast<const v8b*>(p + 2 * i0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = make_float2((float)u[2 * e], (float)u[2 * e + 1]);
+    }
+  } else {
+    // constant indices only (a runtime bound would put the array in memory)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = e < n ? ld_c(p, i0 + e) : make_float2(0.f, 0.f);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void st4(T* p, long long i0, int n, const float2 (&v)[4]) {
+  if (n == 4) {
+    if constexpr (sizeof(T) == 4) {
+      *reinterpret_cast<float4*>(p + 2 * i0) = make_float4(v[0].x, v[0].y, v[1].x, v[1].y);
+      *reinterpret_cast<float4*>(p + 2 * i0 + 4) = make_float4(v[2].x, v[2].y, v[3].x, v[3].y);
+    } else {
+      typedef __bf16 v8b __attribute__((ext_vector_type(8)));
+      v8b u;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        u[2 * e] = (__bf16)v[e].x;
+        u[2 * e + 1] = (__bf16)v[e].y;
+      }
+      *reinterpret_cast<v8b*>(p + 2 * i0) = u;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (e < n) {
+        p[2 * (i0 + e)] = (T)v[e].x;
+        p[2 * (i0 + e) + 1] = (T)v[e].y;
+      }
+  }
+}
+
 // rows [0, B) are degree 0; columns are (spin, channel), s0 the spin-0 slot or -1
 template <typename T>
 __global__ void __launch_bounds__(kNT) bn_apply_kernel(const T* a,  // may be out (in place)
@@ -137,34 +186,19 @@ __global__ void __launch_bounds__(kNT) bn_apply_kernel(const T* a,  // may be ou
                                                        int s0) {
   const long long i0 = ((long long)blockIdx.x * kNT + threadIdx.x) * 4;
   if (i0 >= n_cplx) return;
-  float2 v[4];
   const int n = n_cplx - i0 < 4 ? (int)(n_cplx - i0) : 4;
-  if (n == 4) {  // 4 whole complex values: a 16-byte (bf16) or 2 x 16-byte (f32) load
-    if constexpr (sizeof(T) == 4) {
-      const float4 u = *reinterpret_cast<const float4*>(a + 2 * i0);
-      const float4 w = *reinterpret_cast<const float4*>(a + 2 * i0 + 4);
-      v[0] = make_float2(u.x, u.y); v[1] = make_float2(u.z, u.w);
-      v[2] = make_float2(w.x, w.y); v[3] = make_float2(w.z, w.w);
-    } else {
-      typedef __bf16 v8b __attribute__((ext_vector_type(8)));
-      const v8b u = *reinterpret_cast<const v8b*>(a + 2 * i0);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = make_float2((float)u[2 * e], (float)u[2 * e + 1]);
-    }
-  } else {
-    for (int e = 0; e < n; ++e) v[e] = ld_c(a, i0 + e);
-  }
+  float2 v[4], k[4];
+  ld4(a, i0, n, v);
+  if (skip != nullptr) ld4(skip, i0, n, k);
   float2 o[4];
   long long row = i0 / ncol;
   int col = (int)(i0 - row * ncol);
 #pragma unroll
   for (int e = 0; e < 4; ++e, ++col) {
-    if (e >= n) break;
     if (col == ncol) {
       col = 0;
       ++row;
     }
-    const long long i = i0 + e;
     if (row < B) {  // degree 0: the bias for spin 0, else 0
       o[e] = (col / C == s0 && beta != nullptr) ? beta[col % C] : make_float2(0.f, 0.f);
     } else {
@@ -172,15 +206,11 @@ __global__ void __launch_bounds__(kNT) bn_apply_kernel(const T* a,  // may be ou
       o[e] = make_float2(v[e].x * sc, v[e].y * sc);
     }
     if (skip != nullptr) {
-      const float2 k = ld_c(skip, i);
-      o[e].x += k.x;
-      o[e].y += k.y;
+      o[e].x += k[e].x;
+      o[e].y += k[e].y;
     }
   }
-  for (int e = 0; e < n; ++e) {
-    out[2 * (i0 + e)] = (T)o[e].x;
-    out[2 * (i0 + e) + 1] = (T)o[e].y;
-  }
+  st4(out, i0, n, o);
 }
 
 }  // namespace

@@ -384,7 +384,7 @@ __global__ void __launch_bounds__(NT) lat_inv_kernel(const T* __restrict__ coef,
   la.lo = lo;
   la.L = L;
   la.k_base = kb;
-  RowLoader<T, BN, BK, true> lb;  // table rows: Lp is a multiple of 8
+  RowLoader<T, BN, BK, true> lb;  // table rows: Lp is a multiple of 32
   lb.init([&](int r) -> const T* { const int j = j0 + r; return j < H ? Tb + (size_t)j * Lp : nullptr; },
           Tb + (size_t)j0 * Lp, kb, Lp, tid);
   Tile tile;

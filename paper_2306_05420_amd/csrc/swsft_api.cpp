@@ -270,7 +270,7 @@ swsft_status swsft_plan_create_ex(int H, int W, int L, const int* spins_in, int 
   p->L = L;
   p->Hp = swsft::round_up(H, 8);
   p->JT = H < 32 ? H : 32;
-  p->Lp = swsft::round_up(L, 8);
+  p->Lp = swsft::round_up(L, 32);
   p->M = 2 * L - 1;
   p->n_in = n_spins_in;
   p->n_out = n_spins_out;

@@ -38,7 +38,7 @@ struct Plan {
   int H = 0, W = 0, L = 0;
   int Hp = 0;  // H rounded up to a multiple of 8 (row pitch of the forward tables)
   int JT = 0;  // latitude tile of the X / Y spectra: min(H, 32), the latitude GEMMs' K step
-  int Lp = 0;  // L rounded up to a multiple of 8 (row pitch of inverse tables)
+  int Lp = 0;  // L rounded up to a multiple of 32 (row pitch of inverse tables: whole K steps)
   int M = 0;   // number of orders, 2L - 1
   int n_in = 0, n_out = 0;
   int spins_in[kMaxSpins] = {0};

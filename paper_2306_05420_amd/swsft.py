@@ -405,7 +405,7 @@ class Plan:
         which 2: [2L-1, Hp, Lp] backward synthesis (input spins);
         which 3: [2L-1, L, Hp] backward analysis (output spins)."""
         Hp = (self.H + 7) // 8 * 8
-        Lp = (self.L + 7) // 8 * 8
+        Lp = (self.L + 31) // 32 * 32
         M = 2 * self.L - 1
         shape = (M, self.L, Hp) if which in (0, 3) else (M, Hp, Lp)
         dt = torch.float32 if self.dtype == "f32" else torch.bfloat16

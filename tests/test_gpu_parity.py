@@ -37,7 +37,7 @@ def _ref_table(plan, which, spin):
     H, W, L = plan.H, plan.W, plan.L
     theta, _ = O.grid(H, W)
     w = O.dh_weights(H)
-    Hp, Lp = (H + 7) // 8 * 8, (L + 7) // 8 * 8
+    Hp, Lp = (H + 7) // 8 * 8, (L + 31) // 32 * 32
     M = 2 * L - 1
     N = np.sqrt((2 * np.arange(L) + 1) / (4 * np.pi))
     if which == 0:
