@@ -223,14 +223,14 @@ hipError_t launch_geom(const Plan& p, int B, int Cin, int Cout, const void* coef
 }
 
 // Float form.  K steps of 32 floats (16 complex entries: one 128-byte line
-// per row and copy).  Each of the 4 waves owns one block of 32 expanded rows
-// (16 coefficient rows) x two blocks of 32 outputs, MFMA 32x32x2 f32; the
+// per row and copy).  Each wave owns one block of 32 expanded rows (16
+// coefficient rows) x TN blocks of 32 outputs, MFMA 32x32x2 f32; the
 // workgroup covers WM x WN such wave tiles, i.e. 16 WM coefficient rows x
-// 64 WN outputs.  A lane's A value for row 2i (re, -im) / 2i+1 (im, re) is
+// 32 TN WN outputs.  A lane's A value for row 2i (re, -im) / 2i+1 (im, re) is
 // picked from the 16-byte chunk of coefficient row i (two complex entries,
 // two MFMA steps) by the parity of its row and its K half; the filter rows
 // enter as stored (re, im).
-template <int WM, int WN, int ST>
+template <int WM, int WN, int ST, int TN>
 struct MixGeomF {
   static constexpr int BK = 32;                 // floats per row per K step
   static constexpr int PITCH = 4 * BK;          // bytes per tile row
@@ -238,7 +238,7 @@ struct MixGeomF {
   static constexpr int RPI = 1024 / PITCH;      // rows per 1 KiB copy
   static constexpr int LPR = 64 / RPI;          // lanes per row
   static constexpr int NW = WM * WN, NT = 64 * NW;
-  static constexpr int RA = 16 * WM, RB = 64 * WN;
+  static constexpr int RA = 16 * WM, RB = 32 * TN * WN;
   static constexpr int NI = (RA + RB) / RPI;    // copies per stage
   static constexpr int PER_WAVE = NI / NW;
   static constexpr int STAGE = (RA + RB) * PITCH;
@@ -248,12 +248,12 @@ struct MixGeomF {
   static_assert(ST >= 2 && (ST - 2) * PER_WAVE < 64, "stages");
 };
 
-template <int WM, int WN, int ST>
-__global__ void __launch_bounds__((MixGeomF<WM, WN, ST>::NT))
+template <int WM, int WN, int ST, int TN>
+__global__ void __launch_bounds__((MixGeomF<WM, WN, ST, TN>::NT))
     mix_dma_f32_kernel(const float* __restrict__ coef, const float* __restrict__ K,
                        float* __restrict__ out, int L, int B, int Cin, int Cout, int Sin,
                        int Sout, Spins sin_, Spins sout_) {
-  using G = MixGeomF<WM, WN, ST>;
+  using G = MixGeomF<WM, WN, ST, TN>;
   constexpr int RA = G::RA, RB = G::RB, BK = G::BK;
   extern __shared__ __align__(16) unsigned char smem[];  // G::SMEM bytes: the ring
   __shared__ int live[G::MAX_KT];
@@ -320,9 +320,9 @@ __global__ void __launch_bounds__((MixGeomF<WM, WN, ST>::NT))
     for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + koff, base + u * 1024);
   };
 
-  v16f acc[2];
+  v16f acc[TN];
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
+  for (int j = 0; j < TN; ++j)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
 
@@ -345,32 +345,37 @@ __global__ void __launch_bounds__((MixGeomF<WM, WN, ST>::NT))
       return *reinterpret_cast<const float4*>(As + cr * G::PITCH + swz<G::CPR>(cr, cc) * 16);
     };
     auto ldb = [&](int jj, int cc) {
-      const int q = wn * 64 + jj * 32 + r32;
+      const int q = wn * 32 * TN + jj * 32 + r32;
       return *reinterpret_cast<const float4*>(Bs + q * G::PITCH + swz<G::CPR>(q, cc) * 16);
     };
     // chunk cc + 1 is read while the MFMAs of chunk cc run
-    float4 av = lda(0), bv0 = ldb(0, 0), bv1 = ldb(1, 0);
+    float4 av = lda(0), bv[TN];
+#pragma unroll
+    for (int jj = 0; jj < TN; ++jj) bv[jj] = ldb(jj, 0);
 #pragma unroll
     for (int cc = 0; cc < G::CPR; ++cc) {  // two complex entries = two MFMA steps
-      float4 nav = av, nb0 = bv0, nb1 = bv1;
+      float4 nav = av, nb[TN];
+#pragma unroll
+      for (int jj = 0; jj < TN; ++jj) nb[jj] = bv[jj];
       if (cc + 1 < G::CPR) {
         nav = lda(cc + 1);
-        nb0 = ldb(0, cc + 1);
-        nb1 = ldb(1, cc + 1);
+#pragma unroll
+        for (int jj = 0; jj < TN; ++jj) nb[jj] = ldb(jj, cc + 1);
       }
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         const float a = sgn * (sel_im ? (e ? av.w : av.y) : (e ? av.z : av.x));
-        const float b0 = kh ? (e ? bv0.w : bv0.y) : (e ? bv0.z : bv0.x);
-        const float b1 = kh ? (e ? bv1.w : bv1.y) : (e ? bv1.z : bv1.x);
-        acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b0, acc[0], 0, 0, 0);
-        acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b1, acc[1], 0, 0, 0);
+#pragma unroll
+        for (int jj = 0; jj < TN; ++jj) {
+          const float b = kh ? (e ? bv[jj].w : bv[jj].y) : (e ? bv[jj].z : bv[jj].x);
+          acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc[jj], 0, 0, 0);
+        }
       }
       av = nav;
-      bv0 = nb0;
-      bv1 = nb1;
-      if (cc + 1 < G::CPR) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);  // LDS reads
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                       // MFMA
+#pragma unroll
+      for (int jj = 0; jj < TN; ++jj) bv[jj] = nb[jj];
+      if (cc + 1 < G::CPR) __builtin_amdgcn_sched_group_barrier(0x100, 1 + TN, 0);  // LDS reads
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * TN, 0);                      // MFMA
       __builtin_amdgcn_sched_barrier(0);
     }
   }
@@ -380,8 +385,8 @@ __global__ void __launch_bounds__((MixGeomF<WM, WN, ST>::NT))
   // of its column q: the real and imaginary part of output (row0 + i, q0 + q)
   const int col_l = lane & 31, row_l = 4 * (lane >> 5);
 #pragma unroll
-  for (int jj = 0; jj < 2; ++jj) {
-    const int q = q0 + wn * 64 + jj * 32 + col_l;
+  for (int jj = 0; jj < TN; ++jj) {
+    const int q = q0 + wn * 32 * TN + jj * 32 + col_l;
     const bool qok = q < Nc;
     const bool tok = qok && iabs_(sout_.s[(qok ? q : 0) / Cout]) <= l;
 #pragma unroll
@@ -395,10 +400,10 @@ __global__ void __launch_bounds__((MixGeomF<WM, WN, ST>::NT))
   }
 }
 
-template <int WM, int WN, int ST>
+template <int WM, int WN, int ST, int TN>
 hipError_t launch_geom_f32(const Plan& p, int B, int Cin, int Cout, const void* coef,
                            const void* K, void* out, hipStream_t st) {
-  using G = MixGeomF<WM, WN, ST>;
+  using G = MixGeomF<WM, WN, ST, TN>;
   Spins si{}, so{};
   for (int i = 0; i < p.n_in; ++i) si.s[i] = p.spins_in[i];
   for (int i = 0; i < p.n_out; ++i) so.s[i] = p.spins_out[i];
@@ -406,9 +411,9 @@ hipError_t launch_geom_f32(const Plan& p, int B, int Cin, int Cout, const void* 
   for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + G::RA - 1) / G::RA;
   const int Nc = p.n_out * Cout;
   const long long blocks = tiles * ((Nc + G::RB - 1) / G::RB);
-  const hipError_t e = ensure_dynamic_lds((const void*)mix_dma_f32_kernel<WM, WN, ST>, G::SMEM);
+  const hipError_t e = ensure_dynamic_lds((const void*)mix_dma_f32_kernel<WM, WN, ST, TN>, G::SMEM);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((mix_dma_f32_kernel<WM, WN, ST>), dim3(xcd_grid(blocks)), dim3(G::NT), G::SMEM, st,
+  hipLaunchKernelGGL((mix_dma_f32_kernel<WM, WN, ST, TN>), dim3(xcd_grid(blocks)), dim3(G::NT), G::SMEM, st,
                      (const float*)coef, (const float*)K, (float*)out, p.L, B, Cin, Cout, p.n_in,
                      p.n_out, si, so);
   return hipGetLastError();
@@ -443,7 +448,8 @@ bool mix_dma_supported(const Plan& p, int Cin, int Cout) {
 hipError_t launch_mix_dma(const Plan& p, int B, int Cin, int Cout, const void* coef,
                           const void* K, void* out, hipStream_t st) {
   // float: 32 coefficient rows x 128 outputs, 3 K steps resident
-  if (p.dtype == SWSFT_F32) return launch_geom_f32<2, 2, 3>(p, B, Cin, Cout, coef, K, out, st);
+  // (one output block per wave at 8 waves, 64 x 64, measured slower at the molecule workload)
+  if (p.dtype == SWSFT_F32) return launch_geom_f32<2, 2, 3, 2>(p, B, Cin, Cout, coef, K, out, st);
   if ((2 * Cin) % SWSFT_MIX_DMA_BK == 0)
     return launch_geom<SWSFT_MIX_DMA_BK, SWSFT_MIX_DMA_RA, SWSFT_MIX_DMA_RB, SWSFT_MIX_DMA_STAGES>(
         p, B, Cin, Cout, coef, K, out, st);
