@@ -175,12 +175,44 @@ __device__ __forceinline__ v8bf cat8(v4s lo, v4s hi, unsigned flip) {
 // of the grid) pairs long contractions with short ones.
 __device__ __forceinline__ int paired_degree(int q, int L) { return (q & 1) ? (q >> 1) : L - 1 - (q >> 1); }
 
+// Number of kc-row chunks of degree l's contraction (kc > 0).
+__device__ __host__ __forceinline__ int grad_chunks(int l, int B, int kc) {
+  return ((2 * l + 1) * B + kc - 1) / kc;
+}
+
+// Walks n = grad_chunks(l, B, kc) for l = 0, 1, ... with two divisions in
+// all: the numerator (2l + 1) B + kc - 1 grows by 2B per degree, so its
+// quotient and remainder by kc advance by those of 2B, plus a carry.
+struct ChunkWalk {
+  int n, rem, dn, dr, kc;
+  __device__ ChunkWalk(int B, int kc_) : kc(kc_) {
+    const int t = B + kc - 1;
+    n = t / kc;
+    rem = t - n * kc;
+    dn = 2 * B / kc;
+    dr = 2 * B - dn * kc;
+  }
+  __device__ void next() {
+    n += dn;
+    rem += dr;
+    if (rem >= kc) {
+      rem -= kc;
+      ++n;
+    }
+  }
+};
+
+// kc == 0: one workgroup per (degree, tile), the whole contraction, gK
+// written.  kc > 0: one workgroup per (degree, chunk of kc contraction rows,
+// tile), chunks numbered by increasing degree; the raw float sums go to
+// part[chunk][t'][s'] (complex) and filter_grad_reduce_kernel adds them up.
 template <typename T, bool VEC>
 __global__ void __launch_bounds__(GNT) filter_grad_kernel(const T* __restrict__ a,
                                                           const T* __restrict__ g, T* __restrict__ gK,
                                                           int L, int B, int Cin, int Cout, int n_in,
                                                           int n_out, Spins sin_, Spins sout_,
-                                                          int tiles_r, int tiles_c) {
+                                                          int tiles_r, int tiles_c, int kc,
+                                                          float* __restrict__ part) {
   using G = GradGeom<T>;
   extern __shared__ __align__(16) unsigned char smem_raw[];
   T* Gr = reinterpret_cast<T*>(smem_raw);
@@ -190,13 +222,29 @@ __global__ void __launch_bounds__(GNT) filter_grad_kernel(const T* __restrict__ 
 
   const int per_l = tiles_r * tiles_c;
   const int lb = xcd_logical_block();
-  if (lb >= L * per_l) return;
-  const int l = paired_degree(lb / per_l, L);
+  int l, k_begin = 0, chunk = 0;
+  if (kc == 0) {
+    if (lb >= L * per_l) return;
+    l = paired_degree(lb / per_l, L);
+  } else {
+    int q = lb / per_l;  // global chunk index
+    ChunkWalk cw(B, kc);
+    for (l = 0; l < L; ++l, cw.next()) {
+      if (q < cw.n) break;
+      q -= cw.n;
+      chunk += cw.n;
+    }
+    if (l >= L) return;
+    chunk += q;
+    k_begin = q * kc;
+  }
   const int tile = lb % per_l;
   const int r0 = (tile / tiles_c) * GBM, c0 = (tile % tiles_c) * GBN;
   const int Nc = n_out * Cout, Kc = n_in * Cin;
-  const int Kl = (2 * l + 1) * B;               // contraction length
-  const size_t row0 = (size_t)l * l * B;        // first (m,b) row of degree l
+  const int Kdeg = (2 * l + 1) * B;                            // degree l's contraction length
+  const int k_end = kc == 0 ? Kdeg : min(k_begin + kc, Kdeg);  // this workgroup's rows
+  const int Kl = k_end - k_begin;
+  const size_t row0 = (size_t)l * l * B + k_begin;             // first (m,b) row
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave >> 1, wc = wave & 1;
 
@@ -318,7 +366,26 @@ __global__ void __launch_bounds__(GNT) filter_grad_kernel(const T* __restrict__ 
   }
 
   // epilogue: registers (r, r + 8) of a lane are the real and imaginary parts
-  // of one output; zeros where a spin does not exist at degree l
+  // of one output; zeros where a spin does not exist at degree l (a split
+  // contraction writes its raw float sums, the reduction applies them)
+  if (kc != 0) {
+    float* pout = part + (size_t)chunk * Nc * Kc * 2;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int sc = c0 + wc * 64 + j * 32 + (lane & 31);
+        if (sc >= Kc) continue;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          const int tc = r0 + wr * 32 + i * 16 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (tc >= Nc) continue;
+          *reinterpret_cast<float2*>(pout + ((size_t)tc * Kc + sc) * 2) =
+              make_float2(acc[i][j][r], acc[i][j][r + 8]);
+        }
+      }
+    return;
+  }
   T* out = gK + (size_t)l * Nc * Kc * 2;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -349,6 +416,50 @@ Spins to_spins(const int* s, int n) {
   Spins r{};
   for (int i = 0; i < n && i < kMaxSpins; ++i) r.s[i] = s[i];
   return r;
+}
+
+// gK[l] = sum over the chunks of degree l of part[chunk], in chunk order
+// (deterministic), zero where a spin does not exist at degree l.  Grid: L x
+// ceil(Nc Kc / 256) workgroups, one complex output per thread.
+template <typename T>
+__global__ void __launch_bounds__(256) filter_grad_reduce_kernel(const float* __restrict__ part,
+                                                                 T* __restrict__ gK, int L, int B,
+                                                                 int Cin, int Cout, int n_in,
+                                                                 int n_out, Spins sin_, Spins sout_,
+                                                                 int kc, int blocks_per_l) {
+  const int l = blockIdx.x / blocks_per_l;
+  const int Nc = n_out * Cout, Kc = n_in * Cin;
+  const int e = (blockIdx.x % blocks_per_l) * 256 + threadIdx.x;  // output (t', s')
+  if (l >= L || e >= Nc * Kc) return;
+  int base = 0;
+  ChunkWalk cw(B, kc);
+  for (int d = 0; d < l; ++d, cw.next()) base += cw.n;
+  const int n = cw.n;
+  const size_t stride = (size_t)Nc * Kc;
+  const float2* p = reinterpret_cast<const float2*>(part) + (size_t)base * stride + e;
+  // four loads in flight; the sum order stays chunk order
+  float re = 0.f, im = 0.f;
+  int c = 0;
+  for (; c + 4 <= n; c += 4) {
+    float2 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = p[(size_t)(c + u) * stride];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      re += v[u].x;
+      im += v[u].y;
+    }
+  }
+  for (; c < n; ++c) {
+    const float2 v = p[(size_t)c * stride];
+    re += v.x;
+    im += v.y;
+  }
+  const int tc = e / Kc, sc = e - tc * Kc;
+  const bool live = iabs_(sout_.s[tc / Cout]) <= l && iabs_(sin_.s[sc / Cin]) <= l;
+  T* o = gK + ((size_t)l * Nc * Kc + e) * 2;
+  o[0] = (T)(live ? re : 0.f);
+  o[1] = (T)(live ? im : 0.f);
 }
 
 // ---------------------------------------------------------------- bf16 filter gradient, DMA
@@ -556,25 +667,42 @@ hipError_t filter_grad_dma_t(const Plan& p, int B, int Cin, int Cout, const void
   return hipGetLastError();
 }
 
+bool grad_uses_dma(const Plan& p, int Cin, int Cout) {
+  // bf16 rows as 16-byte chunks: channel counts with 2 S C % 8 == 0
+  return p.dtype == SWSFT_BF16 && (2 * p.n_out * Cout) % 8 == 0 && (2 * p.n_in * Cin) % 8 == 0;
+}
+
 template <typename T>
 hipError_t filter_grad_t(const Plan& p, int B, int Cin, int Cout, const void* a, const void* g,
-                         void* gK, hipStream_t st) {
+                         void* gK, void* part, hipStream_t st) {
   if constexpr (std::is_same<T, __bf16>::value) {
-    // interleaved rows as 16-byte chunks: channel counts with 2 S C % 8 == 0
-    if ((2 * p.n_out * Cout) % 8 == 0 && (2 * p.n_in * Cin) % 8 == 0)
+    if (grad_uses_dma(p, Cin, Cout))
       return filter_grad_dma_t<SWSFT_GRAD_DMA>(p, B, Cin, Cout, a, g, gK, st);
   }
   using G = GradGeom<T>;
   const int Nc = p.n_out * Cout, Kc = p.n_in * Cin;
   const int tiles_r = (Nc + GBM - 1) / GBM, tiles_c = (Kc + GBN - 1) / GBN;
-  const long long blocks = (long long)p.L * tiles_r * tiles_c;
+  const int kc = filter_grad_split_rows(p, B, Cin, Cout);
+  long long units = p.L;  // degrees, or chunks of split contractions
+  if (kc > 0) {
+    units = 0;
+    for (int l = 0; l < p.L; ++l) units += grad_chunks(l, B, kc);
+  }
+  const long long blocks = units * tiles_r * tiles_c;
   const bool vec = Nc % 4 == 0 && Kc % 4 == 0;
   auto kern = vec ? filter_grad_kernel<T, true> : filter_grad_kernel<T, false>;
   const hipError_t e = ensure_dynamic_lds((const void*)kern, G::SMEM);
   if (e != hipSuccess) return e;
+  const Spins si = to_spins(p.spins_in, p.n_in), so = to_spins(p.spins_out, p.n_out);
   hipLaunchKernelGGL(kern, dim3(xcd_grid(blocks)), dim3(GNT), G::SMEM, st, (const T*)a,
-                     (const T*)g, (T*)gK, p.L, B, Cin, Cout, p.n_in, p.n_out,
-                     to_spins(p.spins_in, p.n_in), to_spins(p.spins_out, p.n_out), tiles_r, tiles_c);
+                     (const T*)g, (T*)gK, p.L, B, Cin, Cout, p.n_in, p.n_out, si, so, tiles_r,
+                     tiles_c, kc, (float*)part);
+  if (kc > 0) {
+    const int per_l = (Nc * Kc + 255) / 256;
+    hipLaunchKernelGGL(filter_grad_reduce_kernel<T>, dim3((unsigned)((long long)p.L * per_l)),
+                       dim3(256), 0, st, (const float*)part, (T*)gK, p.L, B, Cin, Cout, p.n_in,
+                       p.n_out, si, so, kc, per_l);
+  }
   return hipGetLastError();
 }
 
@@ -597,10 +725,38 @@ hipError_t launch_filter_adjoint(const Plan& p, int C_in, int C_out, const void*
   return filter_adjoint_t<float>(p, C_in, C_out, K, KH, st);
 }
 
+#ifndef SWSFT_GRAD_SPLIT_WG
+#define SWSFT_GRAD_SPLIT_WG 384
+#endif
+
+// Contraction rows per chunk of the register-staged kernel: a multiple of
+// the K stage, sized for about SWSFT_GRAD_SPLIT_WG workgroups, when one workgroup per
+// (degree, tile) would leave CUs idle (few degrees, long contractions, as at
+// small bandlimits with large batches); 0 when the contraction is not split.
+int filter_grad_split_rows(const Plan& p, int B, int C_in, int C_out) {
+  if (grad_uses_dma(p, C_in, C_out)) return 0;
+  const int Nc = p.n_out * C_out, Kc = p.n_in * C_in;
+  const long long tiles = (long long)((Nc + GBM - 1) / GBM) * ((Kc + GBN - 1) / GBN);
+  if ((long long)p.L * tiles >= 256) return 0;
+  const long long rows = (long long)p.L * p.L * B;  // all degrees' contraction rows
+  long long kc = (rows * tiles + SWSFT_GRAD_SPLIT_WG - 1) / SWSFT_GRAD_SPLIT_WG;
+  kc = (kc + GBK - 1) / GBK * GBK;
+  if (kc >= (long long)(2 * p.L - 1) * B) return 0;  // no degree would be split
+  return (int)kc;
+}
+
+size_t filter_grad_split_bytes(const Plan& p, int B, int C_in, int C_out) {
+  const int kc = filter_grad_split_rows(p, B, C_in, C_out);
+  if (kc == 0) return 0;
+  size_t chunks = 0;
+  for (int l = 0; l < p.L; ++l) chunks += grad_chunks(l, B, kc);
+  return chunks * p.n_out * C_out * p.n_in * C_in * 2 * sizeof(float);
+}
+
 hipError_t launch_filter_grad(const Plan& p, int B, int C_in, int C_out, const void* a,
-                              const void* g, void* gK, hipStream_t st) {
-  if (p.dtype == SWSFT_BF16) return filter_grad_t<__bf16>(p, B, C_in, C_out, a, g, gK, st);
-  return filter_grad_t<float>(p, B, C_in, C_out, a, g, gK, st);
+                              const void* g, void* gK, void* part, hipStream_t st) {
+  if (p.dtype == SWSFT_BF16) return filter_grad_t<__bf16>(p, B, C_in, C_out, a, g, gK, part, st);
+  return filter_grad_t<float>(p, B, C_in, C_out, a, g, gK, part, st);
 }
 
 }  // namespace swsft

@@ -93,7 +93,8 @@ size_t ws_need(const Plan& p, int op, int B, int Cin, int Cout) {
       return align_up((xin > xout ? xin : xout) * e) +
              2 * align_up(swsft::coef_elems(p, p.n_in, B, Cin) * e) +
              align_up(swsft::coef_elems(p, p.n_out, B, Cout) * e) +
-             align_up(filter_elems(p, Cin, Cout) * e);
+             align_up(filter_elems(p, Cin, Cout) * e) +
+             align_up(swsft::filter_grad_split_bytes(p, B, Cin, Cout));
     }
     case SWSFT_OP_BATCH_NORM:
       return align_up(swsft::bn_workspace_bytes(p, B, Cout));
@@ -628,6 +629,8 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
   void* g_out = w;  // G^H grad_y
   w += align_up(swsft::coef_elems(*p, p->n_out, B, C_out) * p->elem);
   void* KH = w;
+  w += align_up(filter_elems(*p, C_in, C_out) * p->elem);
+  void* part = w;  // partial sums of a split filter-gradient contraction
 
   // Views of the plan for the adjoint stages (shallow copies, nothing owned):
   // G^H grad_y is the forward latitude GEMM with the unweighted l-major table
@@ -663,7 +666,7 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
       a = a_in;
     }
     SWSFT_TRY(run_stage(*p, swsft::kStageFilterGrad, st, "filter_grad", [&] {
-      return swsft::launch_filter_grad(*p, B, C_in, C_out, a, g_out, grad_filters, st);
+      return swsft::launch_filter_grad(*p, B, C_in, C_out, a, g_out, grad_filters, part, st);
     }));
   }
   if (grad_x != nullptr) {

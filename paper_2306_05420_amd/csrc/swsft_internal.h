@@ -144,9 +144,13 @@ hipError_t launch_mix(const Plan& p, int B, int C_in, int C_out, const void* coe
 hipError_t launch_filter_adjoint(const Plan& p, int C_in, int C_out, const void* K, void* KH,
                                  hipStream_t st);
 // gK[l][(t,c')][(s,c)] = sum_{(m,b)} g[l][(m,b)][(t,c')] conj(a[l][(m,b)][(s,c)]), zero
-// where |s| > l or |t| > l; a [L^2][B][S_in][C_in], g [L^2][B][S_out][C_out]
+// where |s| > l or |t| > l; a [L^2][B][S_in][C_in], g [L^2][B][S_out][C_out].
+// part: filter_grad_split_bytes(p, B, C_in, C_out) bytes of workspace (the
+// partial sums of a split contraction; unused when that is 0).
+size_t filter_grad_split_bytes(const Plan& p, int B, int C_in, int C_out);
+int filter_grad_split_rows(const Plan& p, int B, int C_in, int C_out);
 hipError_t launch_filter_grad(const Plan& p, int B, int C_in, int C_out, const void* a,
-                              const void* g, void* gK, hipStream_t st);
+                              const void* g, void* gK, void* part, hipStream_t st);
 // Spectral batch norm on coefficients [L^2][B][S_out][C] of plan p's output
 // spins (batch_norm.hip); ws holds bn_workspace_bytes(p, B, C) bytes.
 size_t bn_workspace_bytes(const Plan& p, int B, int C);
