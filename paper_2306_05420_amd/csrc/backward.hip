@@ -420,46 +420,49 @@ Spins to_spins(const int* s, int n) {
 
 // gK[l] = sum over the chunks of degree l of part[chunk], in chunk order
 // (deterministic), zero where a spin does not exist at degree l.  Grid: L x
-// ceil(Nc Kc / 256) workgroups, one complex output per thread.
-template <typename T>
+// ceil(Nc Kc / (256 V)) workgroups, V consecutive complex outputs per thread
+// (V = 2 takes 16-byte loads and needs Nc Kc even).
+template <typename T, int V>
 __global__ void __launch_bounds__(256) filter_grad_reduce_kernel(const float* __restrict__ part,
                                                                  T* __restrict__ gK, int L, int B,
                                                                  int Cin, int Cout, int n_in,
                                                                  int n_out, Spins sin_, Spins sout_,
                                                                  int kc, int blocks_per_l) {
+  using VF = typename std::conditional<V == 2, float4, float2>::type;
   const int l = blockIdx.x / blocks_per_l;
-  const int Nc = n_out * Cout, Kc = n_in * Cin;
-  const int e = (blockIdx.x % blocks_per_l) * 256 + threadIdx.x;  // output (t', s')
-  if (l >= L || e >= Nc * Kc) return;
+  const int Nc = n_out * Cout, Kc = n_in * Cin, NK = Nc * Kc;
+  const int e = ((blockIdx.x % blocks_per_l) * 256 + threadIdx.x) * V;  // first output (t', s')
+  if (l >= L || e >= NK) return;
   int base = 0;
   ChunkWalk cw(B, kc);
   for (int d = 0; d < l; ++d, cw.next()) base += cw.n;
   const int n = cw.n;
-  const size_t stride = (size_t)Nc * Kc;
-  const float2* p = reinterpret_cast<const float2*>(part) + (size_t)base * stride + e;
+  const size_t stride = (size_t)NK / V;  // one chunk, in VF units
+  const VF* p = reinterpret_cast<const VF*>(part) + ((size_t)base * NK + e) / V;
+  float acc[2 * V] = {};
+  auto add = [&](const VF& v) {
+    const float* f = reinterpret_cast<const float*>(&v);
+#pragma unroll
+    for (int u = 0; u < 2 * V; ++u) acc[u] += f[u];
+  };
   // four loads in flight; the sum order stays chunk order
-  float re = 0.f, im = 0.f;
   int c = 0;
   for (; c + 4 <= n; c += 4) {
-    float2 v[4];
+    VF v[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) v[u] = p[(size_t)(c + u) * stride];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      re += v[u].x;
-      im += v[u].y;
-    }
+    for (int u = 0; u < 4; ++u) add(v[u]);
   }
-  for (; c < n; ++c) {
-    const float2 v = p[(size_t)c * stride];
-    re += v.x;
-    im += v.y;
+  for (; c < n; ++c) add(p[(size_t)c * stride]);
+  T* o = gK + ((size_t)l * NK + e) * 2;
+#pragma unroll
+  for (int u = 0; u < V; ++u) {
+    const int tc = (e + u) / Kc, sc = e + u - tc * Kc;
+    const bool live = iabs_(sout_.s[tc / Cout]) <= l && iabs_(sin_.s[sc / Cin]) <= l;
+    o[2 * u] = (T)(live ? acc[2 * u] : 0.f);
+    o[2 * u + 1] = (T)(live ? acc[2 * u + 1] : 0.f);
   }
-  const int tc = e / Kc, sc = e - tc * Kc;
-  const bool live = iabs_(sout_.s[tc / Cout]) <= l && iabs_(sin_.s[sc / Cin]) <= l;
-  T* o = gK + ((size_t)l * Nc * Kc + e) * 2;
-  o[0] = (T)(live ? re : 0.f);
-  o[1] = (T)(live ? im : 0.f);
 }
 
 // ---------------------------------------------------------------- bf16 filter gradient, DMA
@@ -698,10 +701,12 @@ hipError_t filter_grad_t(const Plan& p, int B, int Cin, int Cout, const void* a,
                      (const T*)g, (T*)gK, p.L, B, Cin, Cout, p.n_in, p.n_out, si, so, tiles_r,
                      tiles_c, kc, (float*)part);
   if (kc > 0) {
-    const int per_l = (Nc * Kc + 255) / 256;
-    hipLaunchKernelGGL(filter_grad_reduce_kernel<T>, dim3((unsigned)((long long)p.L * per_l)),
-                       dim3(256), 0, st, (const float*)part, (T*)gK, p.L, B, Cin, Cout, p.n_in,
-                       p.n_out, si, so, kc, per_l);
+    const bool two = (Nc * Kc) % 2 == 0;
+    const int per_l = (Nc * Kc + (two ? 511 : 255)) / (two ? 512 : 256);
+    auto rk = two ? filter_grad_reduce_kernel<T, 2> : filter_grad_reduce_kernel<T, 1>;
+    hipLaunchKernelGGL(rk, dim3((unsigned)((long long)p.L * per_l)), dim3(256), 0, st,
+                       (const float*)part, (T*)gK, p.L, B, Cin, Cout, p.n_in, p.n_out, si, so, kc,
+                       per_l);
   }
   return hipGetLastError();
 }
