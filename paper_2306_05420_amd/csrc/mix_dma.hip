@@ -19,6 +19,18 @@
 //
 // Preconditions (checked by the launcher): K' = 2 S_in C_in with each input
 // spin's channel block a whole number of K steps; bf16 also C_out % 4 == 0.
+//
+// The bf16 kernel also computes the adjoint mixing of the backward pass
+// straight from the filters as stored (ADJ):
+//   coef'[l][(m,b)][(s,c)] = sum_(t,c') g[l][(m,b)][(t,c')] conj(K[l][(t,c')][(s,c)]),
+// the contraction now running over the filter rows.  With g = a + ib and
+// K = c + id, Re = ac + bd and Im = bc - ad, so the expanded rows become
+// (a, b) and (b, -a) against the filter values as stored (c, d); the filter
+// tile is copied k-major ([32 contraction rows][RB outputs], 16-byte chunks
+// moved by 128 bytes on alternate groups of 4 rows so that the two K halves
+// of a wave read different banks) and a lane gathers its 4 consecutive
+// contraction rows of one output as 4 dword reads.  No conjugate-transposed
+// copy of the filters is made.
 #include "lds_dma.h"
 #include "mfma_tile.h"
 #include "swsft_internal.h"
@@ -44,6 +56,11 @@ struct MixGeom {
   static constexpr int RPI = 1024 / PITCH;           // rows per 1 KiB copy
   static constexpr int LPR = 64 / RPI;               // lanes per row
   static constexpr int NI = (RA + RB) / RPI;         // copies per stage
+  static constexpr int NI_A = RA / RPI;              // of which coefficient rows
+  // k-major filter tile of the adjoint: BK / 2 contraction rows of RB outputs
+  static constexpr int PITCH_T = 4 * RB;
+  static constexpr int RPI_T = PITCH_T <= 1024 ? 1024 / PITCH_T : 1;
+  static constexpr int LPR_T = 64 / RPI_T;
   static constexpr int PER_WAVE = NI / NW;
   static constexpr int STAGE = (RA + RB) * PITCH;
   static constexpr int SMEM = ST * STAGE;  // the ring (the epilogue needs no LDS)
@@ -52,12 +69,20 @@ struct MixGeom {
   static_assert(ST >= 2 && (ST - 2) * PER_WAVE < 64, "stages");
 };
 
-template <int BK, int RA, int RB, int ST>
+// chunk position of the adjoint's filter tile (self-inverse)
+__device__ __forceinline__ int swz_adj(int k, int c) { return c ^ (((k >> 2) & 1) << 3); }
+
+// ADJ: the adjoint (Cin, Sin, sin_ describe the contraction side, i.e. the
+// forward's outputs; Cout, Sout, sout_ the results, the forward's inputs).
+template <int BK, int RA, int RB, int ST, bool ADJ>
 __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
     mix_dma_kernel(const __bf16* __restrict__ coef, const __bf16* __restrict__ K,
                    __bf16* __restrict__ out, int L, int B, int Cin, int Cout, int Sin, int Sout,
                    Spins sin_, Spins sout_) {
   using G = MixGeom<BK, RA, RB, ST>;
+  static_assert(!ADJ || (G::PITCH_T <= 1024 && 1024 % G::PITCH_T == 0 &&
+                         (BK / 2) % G::RPI_T == 0 && (BK / 2) * G::PITCH_T == RB * G::PITCH),
+                "adjoint filter tile");
   __shared__ __align__(16) unsigned char smem[G::SMEM];
   __shared__ int live[G::MAX_KT];
   __shared__ int n_live_s;
@@ -102,25 +127,33 @@ __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
   // stage [A rows; B rows]; rows past the end of the matrix are clamped to
   // its last row (their products are discarded)
   const __bf16* gsrc[G::PER_WAVE];
+  bool is_a[G::PER_WAVE];  // wave-uniform
 #pragma unroll
   for (int u = 0; u < G::PER_WAVE; ++u) {
     const int g = wave * G::PER_WAVE + u;
-    const int tr = g * G::RPI + lane / G::LPR;  // row of the stage
-    const int slot = lane % G::LPR;
-    if (tr < RA) {
+    is_a[u] = g < G::NI_A;
+    if (is_a[u]) {
+      const int tr = g * G::RPI + lane / G::LPR;  // row of the stage
       const int row = row0 + tr < Mrows ? row0 + tr : Mrows - 1;
-      gsrc[u] = A0 + (size_t)row * Kp + swz<G::CPR>(tr, slot) * 8;
-    } else {
-      const int rb = tr - RA;
+      gsrc[u] = A0 + (size_t)row * Kp + swz<G::CPR>(tr, lane % G::LPR) * 8;
+    } else if (!ADJ) {
+      const int rb = (g - G::NI_A) * G::RPI + lane / G::LPR;
       const int q = q0 + rb < Nc ? q0 + rb : Nc - 1;
-      gsrc[u] = K0 + (size_t)q * Kp + swz<G::CPR>(rb, slot) * 8;
+      gsrc[u] = K0 + (size_t)q * Kp + swz<G::CPR>(rb, lane % G::LPR) * 8;
+    } else {
+      // contraction row kb of the step, 4 outputs per chunk; chunks past the
+      // last output are clamped to it (their products are discarded)
+      const int kb = (g - G::NI_A) * G::RPI_T + lane / G::LPR_T;
+      const int q = min(q0 + 4 * swz_adj(kb, lane % G::LPR_T), Nc - 4);
+      gsrc[u] = K0 + (size_t)kb * (2 * Nc) + 2 * q;
     }
   }
   auto issue = [&](int i, int stage) {
-    const int koff = live[i] * BK;
+    const int koff = live[i] * BK;                                   // along coefficient rows
+    const size_t koff_b = ADJ ? (size_t)live[i] * (BK / 2) * (2 * Nc) : (size_t)koff;
     const unsigned base = ring_base + stage * G::STAGE + wave * G::PER_WAVE * 1024;
 #pragma unroll
-    for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + koff, base + u * 1024);
+    for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + (is_a[u] ? koff : koff_b), base + u * 1024);
   };
 
   typedef unsigned v4u __attribute__((ext_vector_type(4)));
@@ -139,9 +172,10 @@ __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
 
   const int r32 = lane & 31, kh = lane >> 5;
   // odd expanded rows (im, re): rotate by 16 bits; even rows (re, -im): flip
-  // the high half's sign (the row parity is the lane parity)
+  // the high half's sign (the row parity is the lane parity).  Adjoint: even
+  // rows (re, im) as stored, odd rows (im, -re): rotate, then flip.
   const unsigned rot = (lane & 1) ? 16u : 0u;
-  const unsigned sgn = (lane & 1) ? 0u : 0x80000000u;
+  const unsigned sgn = ((lane & 1) != 0) == ADJ ? 0x80000000u : 0u;
   for (int i = 0; i < nk; ++i) {
     // K step i has landed once at most (issued - i - 1) steps are outstanding
     const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
@@ -166,7 +200,19 @@ __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
 #pragma unroll
       for (int jj = 0; jj < 2; ++jj) {
         const int rb = wn * 64 + jj * 32 + r32;
-        b[jj] = *reinterpret_cast<const v8bf*>(Bs + rb * G::PITCH + swz<G::CPR>(rb, c) * 16);
+        if constexpr (!ADJ) {
+          b[jj] = *reinterpret_cast<const v8bf*>(Bs + rb * G::PITCH + swz<G::CPR>(rb, c) * 16);
+        } else {
+          // contraction rows 4c .. 4c + 3 of output rb: (re, im) each
+          v4u y;
+#pragma unroll
+          for (int d = 0; d < 4; ++d) {
+            const int kr = 4 * c + d;
+            y[d] = *reinterpret_cast<const unsigned*>(Bs + kr * G::PITCH_T +
+                                                      swz_adj(kr, rb >> 2) * 16 + (rb & 3) * 4);
+          }
+          b[jj] = __builtin_bit_cast(v8bf, y);
+        }
       }
 #pragma unroll
       for (int ii = 0; ii < 2; ++ii)
@@ -205,7 +251,7 @@ __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
   }
 }
 
-template <int BK, int RA, int RB, int ST>
+template <int BK, int RA, int RB, int ST, bool ADJ = false>
 hipError_t launch_geom(const Plan& p, int B, int Cin, int Cout, const void* coef, const void* K,
                        void* out, hipStream_t st) {
   using G = MixGeom<BK, RA, RB, ST>;
@@ -216,7 +262,7 @@ hipError_t launch_geom(const Plan& p, int B, int Cin, int Cout, const void* coef
   for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + RA - 1) / RA;
   const int Nc = p.n_out * Cout;
   const long long blocks = (long long)tiles * ((Nc + RB - 1) / RB);
-  hipLaunchKernelGGL((mix_dma_kernel<BK, RA, RB, ST>), dim3(xcd_grid(blocks)), dim3(G::NT), 0,
+  hipLaunchKernelGGL((mix_dma_kernel<BK, RA, RB, ST, ADJ>), dim3(xcd_grid(blocks)), dim3(G::NT), 0,
                      st, (const __bf16*)coef, (const __bf16*)K, (__bf16*)out, p.L, B, Cin, Cout,
                      p.n_in, p.n_out, si, so);
   return hipGetLastError();
@@ -443,6 +489,16 @@ bool mix_dma_supported(const Plan& p, int Cin, int Cout) {
     return (2 * Cin) % 32 == 0 && 2 * p.n_in * Cin <= kMaxKp && p.n_out * Cout >= 128;
   return p.dtype == SWSFT_BF16 && (2 * Cin) % 32 == 0 && 2 * p.n_in * Cin <= kMaxKp &&
          Cout % 4 == 0;
+}
+
+bool mix_adj_dma_supported(const Plan& p, int Cin, int Cout) {
+  return p.dtype == SWSFT_BF16 && (2 * Cin) % 64 == 0 && 2 * p.n_in * Cin <= kMaxKp &&
+         Cout % 4 == 0;
+}
+
+hipError_t launch_mix_adj_dma(const Plan& p, int B, int Cin, int Cout, const void* coef,
+                              const void* K, void* out, hipStream_t st) {
+  return launch_geom<64, 128, 128, 2, true>(p, B, Cin, Cout, coef, K, out, st);
 }
 
 hipError_t launch_mix_dma(const Plan& p, int B, int Cin, int Cout, const void* coef,

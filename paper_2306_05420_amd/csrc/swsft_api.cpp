@@ -670,12 +670,19 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
     }));
   }
   if (grad_x != nullptr) {
-    SWSFT_TRY(run_stage(*p, swsft::kStageFilterAdjoint, st, "filter_adjoint", [&] {
-      return swsft::launch_filter_adjoint(*p, C_in, C_out, filters, KH, st);
-    }));
-    SWSFT_TRY(run_stage(*p, swsft::kStageMix, st, "mix", [&] {
-      return swsft::launch_mix(adj, B, C_out, C_in, g_out, KH, g_in, st);
-    }));
+    if (swsft::mix_adj_dma_supported(adj, C_out, C_in)) {
+      // K^H applied from the filters as stored
+      SWSFT_TRY(run_stage(*p, swsft::kStageMix, st, "mix", [&] {
+        return swsft::launch_mix_adj_dma(adj, B, C_out, C_in, g_out, filters, g_in, st);
+      }));
+    } else {
+      SWSFT_TRY(run_stage(*p, swsft::kStageFilterAdjoint, st, "filter_adjoint", [&] {
+        return swsft::launch_filter_adjoint(*p, C_in, C_out, filters, KH, st);
+      }));
+      SWSFT_TRY(run_stage(*p, swsft::kStageMix, st, "mix", [&] {
+        return swsft::launch_mix(adj, B, C_out, C_in, g_out, KH, g_in, st);
+      }));
+    }
     // F^H: the synthesis with the weighted table on the input spins, over
     // cache-sized batch ranges like the layer's inverse
     SWSFT_TRY(synthesis_stages(*p, syn, B, C_in, g_in, XY, grad_x, st));

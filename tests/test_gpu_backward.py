@@ -113,6 +113,7 @@ BACKWARD_EDGE = [
     (16, 8, (-2, 0), (0, 1), 3, 64, 8, "bf16"),         # |s| = 2: gradient zero below l = 2
     (64, 32, (1, -2), (2, 0), 2, 64, 64, "bf16"),       # latitude GEMMs on the direct-to-LDS path
     (64, 32, (0,), (0, 1), 2, 20, 64, "bf16"),
+    (32, 16, (0, -1, 1), (1, 0), 3, 12, 32, "bf16"),   # adjoint from K as stored, ragged outputs
 ]
 
 
