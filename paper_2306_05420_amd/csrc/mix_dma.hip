@@ -290,16 +290,28 @@ struct MixGeomF {
   static constexpr int STAGE = (RA + RB) * PITCH;
   static constexpr int SMEM = ST * STAGE;
   static constexpr int MAX_KT = kMaxKp / BK;
-  static_assert((RA + RB) % RPI == 0 && NI % NW == 0, "tile shape");
+  static constexpr int NI_A = RA / RPI;  // copies of coefficient rows
+  // k-major filter tile of the adjoint: BK / 2 contraction rows of RB outputs
+  static constexpr int PITCH_T = 8 * RB;
+  static constexpr int RPI_T = PITCH_T <= 1024 ? 1024 / PITCH_T : 1;
+  static constexpr int LPR_T = 64 / RPI_T;
+  static_assert((RA + RB) % RPI == 0 && NI % NW == 0 && RA % RPI == 0, "tile shape");
   static_assert(ST >= 2 && (ST - 2) * PER_WAVE < 64, "stages");
 };
 
-template <int WM, int WN, int ST, int TN>
+// ADJ: the adjoint from the filters as stored, as for bfloat16 above; the
+// expanded rows are (re, im) / (im, -re) and a lane reads the one filter
+// value of its MFMA step (contraction row, output column, its K half) from
+// the k-major tile (64 lanes: 64 consecutive dwords).
+template <int WM, int WN, int ST, int TN, bool ADJ>
 __global__ void __launch_bounds__((MixGeomF<WM, WN, ST, TN>::NT))
     mix_dma_f32_kernel(const float* __restrict__ coef, const float* __restrict__ K,
                        float* __restrict__ out, int L, int B, int Cin, int Cout, int Sin,
                        int Sout, Spins sin_, Spins sout_) {
   using G = MixGeomF<WM, WN, ST, TN>;
+  static_assert(!ADJ || (G::PITCH_T <= 1024 && 1024 % G::PITCH_T == 0 &&
+                         (G::BK / 2) % G::RPI_T == 0 && (G::BK / 2) * G::PITCH_T == G::RB * G::PITCH),
+                "adjoint filter tile");
   constexpr int RA = G::RA, RB = G::RB, BK = G::BK;
   extern __shared__ __align__(16) unsigned char smem[];  // G::SMEM bytes: the ring
   __shared__ int live[G::MAX_KT];
@@ -345,25 +357,33 @@ __global__ void __launch_bounds__((MixGeomF<WM, WN, ST, TN>::NT))
   // stage [A rows; B rows]; rows past the end of a matrix are clamped to its
   // last row (their products are discarded)
   const float* gsrc[G::PER_WAVE];
+  bool is_a[G::PER_WAVE];  // wave-uniform
 #pragma unroll
   for (int u = 0; u < G::PER_WAVE; ++u) {
     const int g = wave * G::PER_WAVE + u;
-    const int tr = g * G::RPI + lane / G::LPR;
-    const int slot = lane % G::LPR;
-    if (tr < RA) {
+    is_a[u] = g < G::NI_A;
+    if (is_a[u]) {
+      const int tr = g * G::RPI + lane / G::LPR;
       const int row = row0 + tr < Mrows ? row0 + tr : Mrows - 1;
-      gsrc[u] = A0 + (size_t)row * Kp + swz<G::CPR>(tr, slot) * 4;
-    } else {
-      const int rb = tr - RA;
+      gsrc[u] = A0 + (size_t)row * Kp + swz<G::CPR>(tr, lane % G::LPR) * 4;
+    } else if (!ADJ) {
+      const int rb = (g - G::NI_A) * G::RPI + lane / G::LPR;
       const int q = q0 + rb < Nc ? q0 + rb : Nc - 1;
-      gsrc[u] = K0 + (size_t)q * Kp + swz<G::CPR>(rb, slot) * 4;
+      gsrc[u] = K0 + (size_t)q * Kp + swz<G::CPR>(rb, lane % G::LPR) * 4;
+    } else {
+      // contraction row kb of the step, 2 outputs per chunk; chunks past the
+      // last output are clamped to it (their products are discarded)
+      const int kb = (g - G::NI_A) * G::RPI_T + lane / G::LPR_T;
+      const int q = min(q0 + 2 * (lane % G::LPR_T), Nc - 2);
+      gsrc[u] = K0 + (size_t)kb * (2 * Nc) + 2 * q;
     }
   }
   auto issue = [&](int i, int stage) {
-    const int koff = live[i] * BK;
+    const int koff = live[i] * BK;  // along coefficient rows
+    const size_t koff_b = ADJ ? (size_t)live[i] * (BK / 2) * (2 * Nc) : (size_t)koff;
     const unsigned base = ring_base + stage * G::STAGE + wave * G::PER_WAVE * 1024;
 #pragma unroll
-    for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + koff, base + u * 1024);
+    for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + (is_a[u] ? koff : koff_b), base + u * 1024);
   };
 
   v16f acc[TN];
@@ -379,7 +399,9 @@ __global__ void __launch_bounds__((MixGeomF<WM, WN, ST, TN>::NT))
   const int r32 = lane & 31, kh = lane >> 5;
   const int cr = wm * 16 + (r32 >> 1);      // coefficient row of this lane's A row
   const bool sel_im = ((r32 & 1) ^ kh) != 0;  // (re, -im) / (im, re): which part
-  const float sgn = ((r32 & 1) == 0 && kh == 1) ? -1.f : 1.f;
+  // negated: the imaginary part of even rows; adjoint ((re, im) / (im, -re)):
+  // the real part of odd rows
+  const float sgn = (((r32 & 1) != 0) == ADJ && kh == 1) ? -1.f : 1.f;
   for (int i = 0; i < nk; ++i) {
     const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
     wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
@@ -392,7 +414,13 @@ __global__ void __launch_bounds__((MixGeomF<WM, WN, ST, TN>::NT))
     };
     auto ldb = [&](int jj, int cc) {
       const int q = wn * 32 * TN + jj * 32 + r32;
-      return *reinterpret_cast<const float4*>(Bs + q * G::PITCH + swz<G::CPR>(q, cc) * 16);
+      if constexpr (!ADJ) {
+        return *reinterpret_cast<const float4*>(Bs + q * G::PITCH + swz<G::CPR>(q, cc) * 16);
+      } else {
+        // contraction rows 2cc and 2cc + 1 of output q, this lane's K half
+        const float* p0 = reinterpret_cast<const float*>(Bs + 2 * cc * G::PITCH_T + q * 8 + kh * 4);
+        return make_float4(p0[0], p0[G::PITCH_T / 4], 0.f, 0.f);
+      }
     };
     // chunk cc + 1 is read while the MFMAs of chunk cc run
     float4 av = lda(0), bv[TN];
@@ -413,14 +441,16 @@ __global__ void __launch_bounds__((MixGeomF<WM, WN, ST, TN>::NT))
         const float a = sgn * (sel_im ? (e ? av.w : av.y) : (e ? av.z : av.x));
 #pragma unroll
         for (int jj = 0; jj < TN; ++jj) {
-          const float b = kh ? (e ? bv[jj].w : bv[jj].y) : (e ? bv[jj].z : bv[jj].x);
+          const float b = ADJ ? (e ? bv[jj].y : bv[jj].x)
+                              : kh ? (e ? bv[jj].w : bv[jj].y) : (e ? bv[jj].z : bv[jj].x);
           acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc[jj], 0, 0, 0);
         }
       }
       av = nav;
 #pragma unroll
       for (int jj = 0; jj < TN; ++jj) bv[jj] = nb[jj];
-      if (cc + 1 < G::CPR) __builtin_amdgcn_sched_group_barrier(0x100, 1 + TN, 0);  // LDS reads
+      if (cc + 1 < G::CPR)
+        __builtin_amdgcn_sched_group_barrier(0x100, ADJ ? 1 + 2 * TN : 1 + TN, 0);  // LDS reads
       __builtin_amdgcn_sched_group_barrier(0x008, 2 * TN, 0);                      // MFMA
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -446,7 +476,7 @@ __global__ void __launch_bounds__((MixGeomF<WM, WN, ST, TN>::NT))
   }
 }
 
-template <int WM, int WN, int ST, int TN>
+template <int WM, int WN, int ST, int TN, bool ADJ = false>
 hipError_t launch_geom_f32(const Plan& p, int B, int Cin, int Cout, const void* coef,
                            const void* K, void* out, hipStream_t st) {
   using G = MixGeomF<WM, WN, ST, TN>;
@@ -457,9 +487,10 @@ hipError_t launch_geom_f32(const Plan& p, int B, int Cin, int Cout, const void* 
   for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + G::RA - 1) / G::RA;
   const int Nc = p.n_out * Cout;
   const long long blocks = tiles * ((Nc + G::RB - 1) / G::RB);
-  const hipError_t e = ensure_dynamic_lds((const void*)mix_dma_f32_kernel<WM, WN, ST, TN>, G::SMEM);
+  const hipError_t e =
+      ensure_dynamic_lds((const void*)mix_dma_f32_kernel<WM, WN, ST, TN, ADJ>, G::SMEM);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((mix_dma_f32_kernel<WM, WN, ST, TN>), dim3(xcd_grid(blocks)), dim3(G::NT), G::SMEM, st,
+  hipLaunchKernelGGL((mix_dma_f32_kernel<WM, WN, ST, TN, ADJ>), dim3(xcd_grid(blocks)), dim3(G::NT), G::SMEM, st,
                      (const float*)coef, (const float*)K, (float*)out, p.L, B, Cin, Cout, p.n_in,
                      p.n_out, si, so);
   return hipGetLastError();
@@ -492,12 +523,17 @@ bool mix_dma_supported(const Plan& p, int Cin, int Cout) {
 }
 
 bool mix_adj_dma_supported(const Plan& p, int Cin, int Cout) {
+  if (p.dtype == SWSFT_F32)  // as the forward float kernel; outputs in 16-byte pairs
+    return (2 * Cin) % 32 == 0 && 2 * p.n_in * Cin <= kMaxKp && p.n_out * Cout >= 128 &&
+           (p.n_out * Cout) % 2 == 0;
   return p.dtype == SWSFT_BF16 && (2 * Cin) % 64 == 0 && 2 * p.n_in * Cin <= kMaxKp &&
          Cout % 4 == 0;
 }
 
 hipError_t launch_mix_adj_dma(const Plan& p, int B, int Cin, int Cout, const void* coef,
                               const void* K, void* out, hipStream_t st) {
+  if (p.dtype == SWSFT_F32)
+    return launch_geom_f32<2, 2, 3, 2, true>(p, B, Cin, Cout, coef, K, out, st);
   return launch_geom<64, 128, 128, 2, true>(p, B, Cin, Cout, coef, K, out, st);
 }
 

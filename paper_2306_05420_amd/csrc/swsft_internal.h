@@ -169,7 +169,7 @@ hipError_t launch_lat_inv_dma(const Plan& p, int B, int C, const void* coef, voi
 bool mix_dma_supported(const Plan& p, int C_in, int C_out);
 hipError_t launch_mix_dma(const Plan& p, int B, int C_in, int C_out, const void* coef,
                           const void* K, void* coef_out, hipStream_t st);
-// The adjoint mixing from the filters as stored (bf16): with plan p whose
+// The adjoint mixing from the filters as stored (DMA kernels): with plan p whose
 // input spins are the layer's output spins, coef_out[l][(m,b)][(s,c)] =
 // sum_(t,c') coef[l][(m,b)][(t,c')] conj(K[l][(t,c')][(s,c)]), K the layer's
 // filters [L][S_p_in][C_in][S_p_out][C_out] (C_in, C_out of this call).
