@@ -622,9 +622,15 @@ __global__ void __launch_bounds__((GradDmaGeom<RA, RB, TN, ST>::NT))
   // epilogue: rows 2q, 2q+1 of a column are registers r, r+1 of one lane;
   // columns 2p, 2p+1 are lanes 2p', 2p'+1: the even lane combines
   //   re = P[2q][2p] + P[2q+1][2p+1],  im = P[2q+1][2p] - P[2q][2p+1]
+  // into one bf16 pair, staged in LDS as the tile's [t'][s'] block (row pitch
+  // padded by 16 bytes: the two row groups of a store hit different banks),
+  // then written by all threads as 16-byte chunks (4 outputs) along s'.
   typedef float f32x2 __attribute__((ext_vector_type(2)));
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  __bf16* out = gK + (size_t)l * Nc * Kc * 2;
+  constexpr int OP = RB / 2 * 4 + 16;  // bytes per staged row
+  constexpr int CPRO = RB / 8;         // 16-byte chunks per staged row
+  static_assert(RA / 2 * OP <= G::SMEM, "staged output tile");
+  __syncthreads();  // every wave is done with the ring
 #pragma unroll
   for (int ii = 0; ii < TM; ++ii)
 #pragma unroll
@@ -632,22 +638,30 @@ __global__ void __launch_bounds__((GradDmaGeom<RA, RB, TN, ST>::NT))
       float x[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) x[r] = __shfl_xor(acc[ii][jj][r], 1);
-      const int col = c0 + wn * 32 * TN + jj * 32 + (lane & 31);
-      if ((lane & 1) || col >= Q2) continue;
-      const int sc = col >> 1;
-      const bool col_live = iabs_(sin_.s[sc / Cin]) <= l;
+      if (lane & 1) continue;
+      const int cl = wn * 32 * TN + jj * 32 + (lane & 31);  // even local column
+      const int sc = (c0 + cl) >> 1;
+      const bool col_live = sc < Kc && iabs_(sin_.s[sc / Cin]) <= l;
 #pragma unroll
       for (int r = 0; r < 16; r += 2) {
-        const int row = r0 + wm * 32 * TM + ii * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row >= R2) continue;
-        const int tc = row >> 1;
-        const bool live = col_live && iabs_(sout_.s[tc / Cout]) <= l;
+        const int rl = wm * 32 * TM + ii * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int tc = (r0 + rl) >> 1;
+        const bool live = col_live && tc < Nc && iabs_(sout_.s[tc / Cout]) <= l;
         const float re = live ? acc[ii][jj][r] + x[r + 1] : 0.f;
         const float im = live ? acc[ii][jj][r + 1] - x[r] : 0.f;
-        *reinterpret_cast<bf16x2*>(out + ((size_t)tc * Kc + sc) * 2) =
+        *reinterpret_cast<bf16x2*>(smem + (rl >> 1) * OP + (cl >> 1) * 4) =
             __builtin_convertvector((f32x2){re, im}, bf16x2);
       }
     }
+  __syncthreads();
+  __bf16* out = gK + (size_t)l * Nc * Kc * 2;
+  for (int idx = tid; idx < RA / 2 * CPRO; idx += G::NT) {
+    const int rl = idx / CPRO, ch = idx % CPRO;
+    const int tc = r0 / 2 + rl, sc = c0 / 2 + 4 * ch;  // Kc % 4 == 0: whole chunks
+    if (tc < Nc && sc < Kc)
+      *reinterpret_cast<uint4*>(out + ((size_t)tc * Kc + sc) * 2) =
+          *reinterpret_cast<const uint4*>(smem + rl * OP + ch * 16);
+  }
 }
 
 // rows (from g) x columns (from a) per workgroup, 32-column MFMA tiles per

@@ -511,21 +511,28 @@ hipError_t launch_geom_f32(const Plan& p, int B, int Cin, int Cout, const void* 
 #ifndef SWSFT_MIX_DMA_STAGES
 #define SWSFT_MIX_DMA_STAGES 2
 #endif
+// float: WM, WN, ST, TN of MixGeomF
+#ifndef SWSFT_MIX_DMA_F32
+#define SWSFT_MIX_DMA_F32 2, 2, 4, 1
+#endif
+#ifndef SWSFT_MIX_F32_MIN_OUT
+#define SWSFT_MIX_F32_MIN_OUT 64
+#endif
 
 }  // namespace
 
 bool mix_dma_supported(const Plan& p, int Cin, int Cout) {
-  // float: outputs of at least 128 (narrower ones run as fast register-staged)
+  // float: outputs of at least 64 (narrower ones run as fast register-staged)
   if (p.dtype == SWSFT_F32)
-    return (2 * Cin) % 32 == 0 && 2 * p.n_in * Cin <= kMaxKp && p.n_out * Cout >= 128;
+    return (2 * Cin) % 32 == 0 && 2 * p.n_in * Cin <= kMaxKp && p.n_out * Cout >= SWSFT_MIX_F32_MIN_OUT;
   return p.dtype == SWSFT_BF16 && (2 * Cin) % 32 == 0 && 2 * p.n_in * Cin <= kMaxKp &&
          Cout % 4 == 0;
 }
 
 bool mix_adj_dma_supported(const Plan& p, int Cin, int Cout) {
   if (p.dtype == SWSFT_F32)  // as the forward float kernel; outputs in 16-byte pairs
-    return (2 * Cin) % 32 == 0 && 2 * p.n_in * Cin <= kMaxKp && p.n_out * Cout >= 128 &&
-           (p.n_out * Cout) % 2 == 0;
+    return (2 * Cin) % 32 == 0 && 2 * p.n_in * Cin <= kMaxKp &&
+           p.n_out * Cout >= SWSFT_MIX_F32_MIN_OUT && (p.n_out * Cout) % 2 == 0;
   return p.dtype == SWSFT_BF16 && (2 * Cin) % 64 == 0 && 2 * p.n_in * Cin <= kMaxKp &&
          Cout % 4 == 0;
 }
@@ -533,15 +540,16 @@ bool mix_adj_dma_supported(const Plan& p, int Cin, int Cout) {
 hipError_t launch_mix_adj_dma(const Plan& p, int B, int Cin, int Cout, const void* coef,
                               const void* K, void* out, hipStream_t st) {
   if (p.dtype == SWSFT_F32)
-    return launch_geom_f32<2, 2, 3, 2, true>(p, B, Cin, Cout, coef, K, out, st);
+    return launch_geom_f32<SWSFT_MIX_DMA_F32, true>(p, B, Cin, Cout, coef, K, out, st);
   return launch_geom<64, 128, 128, 2, true>(p, B, Cin, Cout, coef, K, out, st);
 }
 
 hipError_t launch_mix_dma(const Plan& p, int B, int Cin, int Cout, const void* coef,
                           const void* K, void* out, hipStream_t st) {
-  // float: 32 coefficient rows x 128 outputs, 3 K steps resident
-  // (one output block per wave at 8 waves, 64 x 64, measured slower at the molecule workload)
-  if (p.dtype == SWSFT_F32) return launch_geom_f32<2, 2, 3, 2>(p, B, Cin, Cout, coef, K, out, st);
+  // float: 32 coefficient rows x 64 outputs, one 32 x 32 block per wave, 4 K
+  // steps resident (measured against 32 x 128 with 3 steps, 16 x 128, 32 x 64
+  // with 2 waves and 64 x 64 with 8 waves: mol 19.4 -> 18.3 us, wx128 42.3 -> 36.4 us)
+  if (p.dtype == SWSFT_F32) return launch_geom_f32<SWSFT_MIX_DMA_F32>(p, B, Cin, Cout, coef, K, out, st);
   if ((2 * Cin) % SWSFT_MIX_DMA_BK == 0)
     return launch_geom<SWSFT_MIX_DMA_BK, SWSFT_MIX_DMA_RA, SWSFT_MIX_DMA_RB, SWSFT_MIX_DMA_STAGES>(
         p, B, Cin, Cout, coef, K, out, st);
