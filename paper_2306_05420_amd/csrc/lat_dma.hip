@@ -805,13 +805,21 @@ bool lat_inv_dma_supported(const Plan& p, int B, int C) {
          p.Lp % InvGeom<SWSFT_LAT_INV_DMA>::BK == 0 && p.Hp == p.H;
 }
 
+// float geometries at H = 32 (WM, WN, ST of FwdGeomF; TM, WM, WN, ST of InvGeomF)
+#ifndef SWSFT_LAT_FWD_F32_H32
+#define SWSFT_LAT_FWD_F32_H32 1, 4, 1
+#endif
+#ifndef SWSFT_LAT_INV_F32_H32
+#define SWSFT_LAT_INV_F32_H32 2, 4, 1, 1
+#endif
+
 hipError_t launch_lat_fwd_dma(const Plan& p, int B, int C, const void* X, void* coef,
                               hipStream_t st) {
   // float: 32 rows l x 256 columns while L <= 32, else 64 x 128; a single
   // K step (H = 32) needs a single stage, which leaves room for 4 workgroups
   // per CU
   if (p.dtype == SWSFT_F32) {
-    if (p.H == kJT) return fwd_geom_f32<1, 4, 1>(p, B, C, X, coef, st);
+    if (p.H == kJT) return fwd_geom_f32<SWSFT_LAT_FWD_F32_H32>(p, B, C, X, coef, st);
     if (p.L <= 32) return fwd_geom_f32<1, 4, 2>(p, B, C, X, coef, st);
     return fwd_geom_f32<2, 2, 3>(p, B, C, X, coef, st);
   }
@@ -825,7 +833,7 @@ hipError_t launch_lat_inv_dma(const Plan& p, int B, int C, const void* coef, voi
   // float: 256 n' x 32 j in one stage when H = 32 (then L <= 16 < 32: one K
   // step); else 64 n' x 128 j with two stages
   if (p.dtype == SWSFT_F32) {
-    if (p.H == kJT) return inv_geom_f32<2, 4, 1, 1>(p, B, C, coef, Y, st);
+    if (p.H == kJT) return inv_geom_f32<SWSFT_LAT_INV_F32_H32>(p, B, C, coef, Y, st);
     return inv_geom_f32<1, 2, 2, 2>(p, B, C, coef, Y, st);
   }
   if ((2 * C) % inv_ra<SWSFT_LAT_INV_DMA_WIDE>(0) == 0)
