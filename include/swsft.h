@@ -198,7 +198,10 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
  *  other or an input that is read; an input that no requested output needs
  *  (x for grad_x alone, filters for grad_filters alone) may be NULL.
  *  Returns SWSFT_E_INVALID / SWSFT_E_WORKSPACE on bad arguments before any
- *  launch, SWSFT_E_HIP if a launch fails.
+ *  launch, SWSFT_E_HIP if a launch fails.  Results are deterministic: no
+ *  atomics; where the filter-gradient contraction over (m, b) is split across
+ *  workgroups, the partial sums (kept in the workspace) are added in a fixed
+ *  order, so repeated calls are bit-identical.
  *  ws  workspace of ws_bytes >= swsft_workspace_bytes(p, SWSFT_OP_CONV_BACKWARD, B, C_in, C_out).
  */
 swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, const void* x,
