@@ -64,10 +64,17 @@ size_t dft_lds_bytes(int M) {
 // Raw register image of one complex input sample (loaded before any compute).
 template <typename T>
 struct Raw;
+// NT: the non-temporal hint (streams much larger than the caches).
 template <>
 struct Raw<float> {
   using type = float2;
+  template <bool NT>
   static __device__ __forceinline__ type load(const float* p, size_t i) {
+    typedef float f2v __attribute__((ext_vector_type(2)));
+    if constexpr (NT) {
+      const f2v v = __builtin_nontemporal_load(reinterpret_cast<const f2v*>(p) + i);
+      return make_float2(v.x, v.y);
+    }
     return reinterpret_cast<const float2*>(p)[i];
   }
   static __device__ __forceinline__ float2 unpack(type v) { return v; }
@@ -75,7 +82,9 @@ struct Raw<float> {
 template <>
 struct Raw<__bf16> {
   using type = uint32_t;
+  template <bool NT>
   static __device__ __forceinline__ type load(const __bf16* p, size_t i) {
+    if constexpr (NT) return __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p) + i);
     return reinterpret_cast<const uint32_t*>(p)[i];
   }
   static __device__ __forceinline__ float2 unpack(type u) {
@@ -92,14 +101,21 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
 }
 
-template <typename T>
-__device__ __forceinline__ void store_cplx(T* p, size_t i, float2 v);
-template <>
-__device__ __forceinline__ void store_cplx<float>(float* p, size_t i, float2 v) {
+// One complex output sample; NT: the non-temporal hint.
+template <bool NT>
+__device__ __forceinline__ void store_cplx(float* p, size_t i, float2 v) {
+  if constexpr (NT) {
+    __builtin_nontemporal_store((f32x2_t){v.x, v.y}, reinterpret_cast<f32x2_t*>(p) + i);
+    return;
+  }
   reinterpret_cast<float2*>(p)[i] = v;
 }
-template <>
-__device__ __forceinline__ void store_cplx<__bf16>(__bf16* p, size_t i, float2 v) {
+template <bool NT>
+__device__ __forceinline__ void store_cplx(__bf16* p, size_t i, float2 v) {
+  if constexpr (NT) {
+    __builtin_nontemporal_store(pack_bf16x2(v.x, v.y), reinterpret_cast<uint32_t*>(p) + i);
+    return;
+  }
   reinterpret_cast<uint32_t*>(p)[i] = pack_bf16x2(v.x, v.y);
 }
 
@@ -212,7 +228,8 @@ __device__ __forceinline__ bool map_block(int S, int C, int NB, MapBlock& mb) {
   return true;
 }
 
-template <typename Tin, typename Tout, int W1, int W2>
+// STREAM: the input rows are read with the non-temporal hint (see launch_dft_fwd).
+template <typename Tin, typename Tout, int W1, int W2, bool STREAM>
 __global__ void __launch_bounds__((DftGeom<W1, W2>::NT))
     dft_fwd_kernel(const Tin* __restrict__ x, Tout* __restrict__ X,
                    const float2* __restrict__ tw, int S, int C, int NB, int NBC, int L) {
@@ -236,7 +253,7 @@ __global__ void __launch_bounds__((DftGeom<W1, W2>::NT))
 #pragma unroll
   for (int p = 0; p < NP; ++p)
 #pragma unroll
-    for (int q = 0; q < W2; ++q) raw[p][q] = Raw<Tin>::load(x, row_base + (size_t)p * W + W1 * q);
+    for (int q = 0; q < W2; ++q) raw[p][q] = Raw<Tin>::template load<STREAM>(x, row_base + (size_t)p * W + W1 * q);
   float2 twr[W2];
 #pragma unroll
   for (int k2 = 1; k2 < W2; ++k2) twr[k2] = tw[t * k2];
@@ -293,7 +310,8 @@ __global__ void __launch_bounds__((DftGeom<W1, W2>::NT))
                                      M, (size_t)(H / JB) * tile, mb.n, tid);
 }
 
-template <typename Tin, typename Tout, int W1, int W2>
+// STREAM: the output rows are written with the non-temporal hint.
+template <typename Tin, typename Tout, int W1, int W2, bool STREAM>
 __global__ void __launch_bounds__((DftGeom<W1, W2>::NT))
     dft_inv_kernel(const Tin* __restrict__ Y, Tout* __restrict__ y,
                    const float2* __restrict__ tw, int S, int C, int NB, int NBC, int L) {
@@ -359,9 +377,23 @@ __global__ void __launch_bounds__((DftGeom<W1, W2>::NT))
       fft_reg<W1, +1>(u);
 #pragma unroll
       for (int k1 = 0; k1 < W1; ++k1)
-        store_cplx<Tout>(y, row_base + (size_t)p * W + k2 + W2 * k1, u[k1]);
+        store_cplx<STREAM>(y, row_base + (size_t)p * W + k2 + W2 * k1, u[k1]);
     }
   }
+}
+
+// Launches that move at least kStreamBytes (about half the 256 MB Infinity
+// Cache) read their input (forward) or write their output (inverse) with the
+// non-temporal hint: such a stream cannot stay cached anyway, and keeping it
+// out leaves the cache to the spectrum the next stage reads (wx256: forward
+// DFT 120 -> 106 us, layer 480 -> 462 us; at 33 MB (mol) the same hint costs
+// 1.5-2.4x, since there everything fits).  Instantiated for W >= 128 only.
+constexpr size_t kStreamBytes = size_t(128) << 20;
+template <int W>
+constexpr bool kHasStream = W >= 128;
+template <int W>
+bool streams_past_caches(size_t bytes) {
+  return kHasStream<W> && bytes >= kStreamBytes;
 }
 
 template <class Kern>
@@ -375,7 +407,9 @@ hipError_t launch_fwd_shape(const Plan& p, int S, int B, int C, const void* x, v
   using G = DftGeom<W1, W2>;
   if (p.H != G::W || p.JT != G::JB) return hipErrorInvalidValue;
   const size_t lds = dft_lds_bytes<Tout, G>(p.M);
-  auto kern = dft_fwd_kernel<Tin, Tout, W1, W2>;
+  const size_t bytes = (size_t)B * S * C * p.H * p.W * 2 * sizeof(Tin) + xy_elems(p, S, B, C) * sizeof(Tout);
+  auto kern = streams_past_caches<W1 * W2>(bytes) ? dft_fwd_kernel<Tin, Tout, W1, W2, kHasStream<W1 * W2>>
+                                                  : dft_fwd_kernel<Tin, Tout, W1, W2, false>;
   const hipError_t e = allow_lds(kern, lds);
   if (e != hipSuccess) return e;
   const long long blocks = (long long)B * S * C * (p.H / G::JB);
@@ -390,7 +424,9 @@ hipError_t launch_inv_shape(const Plan& p, int S, int B, int C, const void* Y, v
   using G = DftGeom<W1, W2>;
   if (p.H != G::W || p.JT != G::JB) return hipErrorInvalidValue;
   const size_t lds = dft_lds_bytes<Tin, G>(p.M);
-  auto kern = dft_inv_kernel<Tin, Tout, W1, W2>;
+  const size_t bytes = xy_elems(p, S, B, C) * sizeof(Tin) + (size_t)B * S * C * p.H * p.W * 2 * sizeof(Tout);
+  auto kern = streams_past_caches<W1 * W2>(bytes) ? dft_inv_kernel<Tin, Tout, W1, W2, kHasStream<W1 * W2>>
+                                                  : dft_inv_kernel<Tin, Tout, W1, W2, false>;
   const hipError_t e = allow_lds(kern, lds);
   if (e != hipSuccess) return e;
   const long long blocks = (long long)B * S * C * (p.H / G::JB);
