@@ -812,16 +812,22 @@ bool lat_inv_dma_supported(const Plan& p, int B, int C) {
 #ifndef SWSFT_LAT_INV_F32_H32
 #define SWSFT_LAT_INV_F32_H32 2, 4, 1, 1
 #endif
+// and for H > 32 (forward: 32 rows l x 256 columns with 2 stages, measured
+// against 64 x 128 with 2 or 3 stages, 32 x 128 and 64 x 64: wx128 31.5 -> 30.1 us)
+#ifndef SWSFT_LAT_FWD_F32
+#define SWSFT_LAT_FWD_F32 1, 4, 2
+#endif
+#ifndef SWSFT_LAT_INV_F32
+#define SWSFT_LAT_INV_F32 1, 2, 2, 2
+#endif
 
 hipError_t launch_lat_fwd_dma(const Plan& p, int B, int C, const void* X, void* coef,
                               hipStream_t st) {
-  // float: 32 rows l x 256 columns while L <= 32, else 64 x 128; a single
-  // K step (H = 32) needs a single stage, which leaves room for 4 workgroups
-  // per CU
+  // float: 32 rows l x 256 columns; a single K step (H = 32) needs a single
+  // stage, which leaves room for 4 workgroups per CU
   if (p.dtype == SWSFT_F32) {
     if (p.H == kJT) return fwd_geom_f32<SWSFT_LAT_FWD_F32_H32>(p, B, C, X, coef, st);
-    if (p.L <= 32) return fwd_geom_f32<1, 4, 2>(p, B, C, X, coef, st);
-    return fwd_geom_f32<2, 2, 3>(p, B, C, X, coef, st);
+    return fwd_geom_f32<SWSFT_LAT_FWD_F32>(p, B, C, X, coef, st);
   }
   if ((2 * B * C) % fwd_rb<SWSFT_LAT_FWD_DMA_WIDE>(0) == 0)
     return fwd_geom<SWSFT_LAT_FWD_DMA_WIDE>(p, B, C, X, coef, st);
@@ -834,7 +840,7 @@ hipError_t launch_lat_inv_dma(const Plan& p, int B, int C, const void* coef, voi
   // step); else 64 n' x 128 j with two stages
   if (p.dtype == SWSFT_F32) {
     if (p.H == kJT) return inv_geom_f32<SWSFT_LAT_INV_F32_H32>(p, B, C, coef, Y, st);
-    return inv_geom_f32<1, 2, 2, 2>(p, B, C, coef, Y, st);
+    return inv_geom_f32<SWSFT_LAT_INV_F32>(p, B, C, coef, Y, st);
   }
   if ((2 * C) % inv_ra<SWSFT_LAT_INV_DMA_WIDE>(0) == 0)
     return inv_geom<SWSFT_LAT_INV_DMA_WIDE>(p, B, C, coef, Y, st);
