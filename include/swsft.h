@@ -27,7 +27,11 @@
  *                  rows with l < |s| are written as 0 and ignored on input
  *    filters       K        [L][S_out][C_out][S_in][C_in]   complex;
  *                  output spin/channel first, like a dense-layer weight;
- *                  entries with l < max(|s_in|, |s_out|) are ignored
+ *                  entries with l < max(|s_in|, |s_out|) are ignored;
+ *                  S_out C_out S_in C_in <= 2^30 (one degree's block),
+ *                  else SWSFT_E_UNSUPPORTED
+ *  Sizes      1 <= B <= 65535, 1 <= C <= 2^20 and B C <= 2^26 for every
+ *             channel count C (SWSFT_E_INVALID otherwise)
  *  S is the number of spins of the side concerned; spins are the plan's
  *  spins_in (forward transform, conv input) or spins_out (inverse transform,
  *  conv output, phase collapse), in the order given to swsft_plan_create.

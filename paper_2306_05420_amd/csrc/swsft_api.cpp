@@ -62,6 +62,16 @@ swsft_status check_bc(int B, int C, const char* cname) {
   return SWSFT_OK;
 }
 
+// One degree's filter block, S_out C_out x S_in C_in complex values, is
+// indexed with 32-bit integers inside the kernels.
+swsft_status check_filter_block(const Plan& p, int C_in, int C_out) {
+  const long long n = (long long)p.n_out * C_out * p.n_in * C_in;
+  if (n > (1LL << 30))
+    return fail(SWSFT_E_UNSUPPORTED,
+                "S_out * C_out * S_in * C_in = %lld exceeds 2^30 filter entries per degree", n);
+  return SWSFT_OK;
+}
+
 bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
   const char *pa = static_cast<const char*>(a), *pb = static_cast<const char*>(b);
   return pa != nullptr && pb != nullptr && pa < pb + nb && pb < pa + na;
@@ -509,6 +519,7 @@ swsft_status conv_forward(swsft_plan p, int B, int C_in, int C_out, const void* 
   if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
   SWSFT_TRY(check_bc(B, C_in, "C_in"));
   SWSFT_TRY(check_bc(B, C_out, "C_out"));
+  SWSFT_TRY(check_filter_block(*p, C_in, C_out));
   SWSFT_TRY(check_ptr(x, "x"));
   SWSFT_TRY(check_ptr(filters, "filters"));
   SWSFT_TRY(check_ptr(y, "y"));
@@ -575,6 +586,7 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
   if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
   SWSFT_TRY(check_bc(B, C_in, "C_in"));
   SWSFT_TRY(check_bc(B, C_out, "C_out"));
+  SWSFT_TRY(check_filter_block(*p, C_in, C_out));
   if (grad_x == nullptr && grad_filters == nullptr)
     return fail(SWSFT_E_INVALID, "neither grad_x nor grad_filters requested");
   SWSFT_TRY(check_ptr(grad_y, "grad_y"));
@@ -696,6 +708,7 @@ swsft_status spin_sph_mix(swsft_plan p, int B, int C_in, int C_out, const void* 
   if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
   SWSFT_TRY(check_bc(B, C_in, "C_in"));
   SWSFT_TRY(check_bc(B, C_out, "C_out"));
+  SWSFT_TRY(check_filter_block(*p, C_in, C_out));
   SWSFT_TRY(check_ptr(coef, "coef"));
   SWSFT_TRY(check_ptr(filters, "filters"));
   SWSFT_TRY(check_ptr(coef_out, "coef_out"));

@@ -188,6 +188,14 @@ def test_backward_call_validation():
                                     ws.data_ptr(), need, None) == S.E_INVALID   # overlaps coef_x
     assert call(None, p(K), p(y), p(gx), None) == S.OK                  # x unused for grad_x only
     assert call(p(x), None, p(y), None, p(gk)) == S.OK                  # filters unused
+    # one degree's filter block above 2^30 entries (2 x 40000 x 1 x 40000) is
+    # refused before any pointer is used
+    big = 40000
+    assert L.spin_sph_conv_backward(plan._h, 1, big, big, p(x), None, p(K), p(y), p(gx), p(gk),
+                                    ws.data_ptr(), need, None) == S.E_UNSUPPORTED
+    assert L.spin_sph_conv_forward(plan._h, 1, big, big, p(x), p(K), p(y), ws.data_ptr(), need,
+                                   None) == S.E_UNSUPPORTED
+    assert L.spin_sph_mix(plan._h, 1, big, big, p(c), p(K), p(gk), None) == S.E_UNSUPPORTED
     torch.cuda.synchronize()
     plan.close()
 
