@@ -108,6 +108,7 @@ BACKWARD_EDGE = [
     (2, 1, (0,), (0,), 2, 2, 3, "f32"),                # smallest grid, l = 0 only
     (64, 32, (1,), (0, -1), 1, 33, 17, "f32"),         # ragged tiles, spin 1 absent at l = 0
     (32, 16, (0, 1, -1), (0, 1), 2, 50, 16, "f32"),    # adjoint from K as stored, 150 outputs
+    (8, 4, (0,), (0,), 32, 3, 5, "f32"),               # split contraction, every chunk full (32 rows)
     (8, 4, (0,), (0, 1), 5, 7, 9, "bf16"),
     (32, 16, (0, 1), (0, 1), 2, 40, 24, "bf16"),        # several column tiles of the gradient
     (32, 16, (0, 1), (0, 1, -1), 3, 32, 44, "bf16"),    # adjoint mixing with 2 C_out % 32 == 0
