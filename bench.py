@@ -203,6 +203,61 @@ def _cpu_model() -> str:
     return "unknown"
 
 
+def vendor_mix(steps: int, warmup: int) -> dict:
+    """The mixing stage at wx256 (L = 128, B = 2, spins {0,1}, C = 256) as real
+    bf16 GEMMs per degree l, [2 (2l+1) B expanded rows x 2 S C] x [2 S C x S C],
+    run by torch.bmm (hipBLASLt) with the rows padded to uniform batches: all
+    degrees padded to 1024 rows, and degrees grouped by row counts padded to
+    multiples of 256; next to spin_sph_mix on the same sizes (random values:
+    timings do not depend on them)."""
+    import torch
+
+    from paper_2306_05420_amd import swsft as S
+
+    dev = torch.device("cuda", 0)
+    L, B, Sn, C = 128, 2, 2, 256
+    Kp, N = 2 * Sn * C, Sn * C
+    useful = sum(8 * (2 * l + 1) * B * N * N for l in range(L))
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps * 1e3  # us
+
+    out = {"useful_gflop": round(useful / 1e9, 2)}
+    a = torch.randn(L, 1024, Kp, device=dev).to(torch.bfloat16)
+    b = torch.randn(L, Kp, N, device=dev).to(torch.bfloat16)
+    us = timed(lambda: torch.bmm(a, b))
+    out["bmm_padded_1024"] = {"us": round(us, 1), "useful_TFLOP/s": round(useful / us / 1e6, 1)}
+    del a, b
+    groups = {}
+    for l in range(L):
+        groups.setdefault((2 * (2 * l + 1) * B + 255) // 256 * 256, []).append(l)
+    mats = [(torch.randn(len(ls), g, Kp, device=dev).to(torch.bfloat16),
+             torch.randn(len(ls), Kp, N, device=dev).to(torch.bfloat16)) for g, ls in groups.items()]
+    us = timed(lambda: [torch.bmm(x, y) for x, y in mats])
+    out["bmm_grouped_256"] = {"us": round(us, 1), "useful_TFLOP/s": round(useful / us / 1e6, 1),
+                              "launches": len(mats)}
+    del mats
+    plan = S.Plan(2 * L, 2 * L, L, (0, 1), (0, 1), "bf16")
+    coef = plan.empty(L * L, B, Sn, C)
+    coef.copy_(torch.randn(coef.shape, device=dev).to(torch.bfloat16))
+    K = plan.empty(L, Sn, C, Sn, C)
+    K.copy_(torch.randn(K.shape, device=dev).to(torch.bfloat16))
+    res = plan.empty(L * L, B, Sn, C)
+    us = timed(lambda: plan.mix(coef, K, res))
+    out["spin_sph_mix"] = {"us": round(us, 1), "useful_TFLOP/s": round(useful / us / 1e6, 1)}
+    plan.close()
+    return out
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -223,6 +278,9 @@ def main(argv=None):
     ap.add_argument("--delta-routes", action="store_true",
                     help="compare the latitude stages: direct d(theta) tables vs the Wigner-Delta "
                          "route with and without its symmetries (wx128 and wx256 workloads)")
+    ap.add_argument("--vendor-mix", action="store_true",
+                    help="time torch's bf16 batched matmul (hipBLASLt) on the mixing stage's "
+                         "per-degree shapes at wx256 next to the library's mixing kernel")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic_<workload>.json from two counter runs and exit")
     args = ap.parse_args(argv)
@@ -248,6 +306,9 @@ def main(argv=None):
             for route in ("direct", "delta_sym", "delta"):
                 print(delta_route_row(name, route, min(args.steps, 50), min(args.warmup, 5)),
                       flush=True)
+        return 0
+    if args.vendor_mix:
+        print(json.dumps(vendor_mix(min(args.steps, 50), min(args.warmup, 5))))
         return 0
     if args.dft_vs_fft:
         print(DFT_HEAD)
