@@ -156,10 +156,11 @@ def summarize_counters(fetch_csv: str, write_csv: str, out_path: str) -> dict:
     return rec
 
 
-def cpu_baseline(w, runs: int = 3):
-    """The float64 oracle on the host cores, one whole layer call on the full
+def cpu_baseline(w, min_runs: int = 3, min_seconds: float = 10.0, max_runs: int = 200):
+    """The float64 oracle on the host cores, whole layer calls on the full
     workload (random complex input and filters of the workload's shapes: its
-    cost does not depend on the values), `runs` times; median seconds."""
+    cost does not depend on the values), repeated until at least `min_runs`
+    calls and `min_seconds` of work (a bounded sample); median seconds."""
     import numpy as np
     import torch
 
@@ -175,10 +176,11 @@ def cpu_baseline(w, runs: int = 3):
     x = cn(w.B, len(w.spins_in), w.C_in, w.H, w.W)
     K = cn(w.L, len(w.spins_out), w.C_out, len(w.spins_in), w.C_in)
     times = []
-    for _ in range(runs):
+    while len(times) < max_runs and (len(times) < min_runs or sum(times) < min_seconds):
         t0 = time.perf_counter()
         O.conv(x, K, w.L, w.spins_in, w.spins_out)
         times.append(time.perf_counter() - t0)
+    runs = len(times)
     t_layer = float(np.median(times))
     return {
         "value": 1.0 / t_layer,
@@ -186,8 +188,8 @@ def cpu_baseline(w, runs: int = 3):
         "cores": cores,
         "kind": "oracle",
         "sample": (f"float64 numpy oracle (forward, mixing, inverse) on the full workload, "
-                   f"{runs} layer calls, median {t_layer:.2f} s "
-                   f"(runs: {', '.join(f'{t:.2f}' for t in times)} s)"),
+                   f"{runs} layer calls ({sum(times):.1f} s of work), median {t_layer:.3f} s "
+                   f"(min {min(times):.3f}, max {max(times):.3f} s)"),
         "seconds_per_fwd": t_layer,
         "cpu": _cpu_model(),
     }
