@@ -53,3 +53,54 @@ def test_graph_replays_match_eager(name):
             assert torch.equal(got, want), (name, rep)
     del g
     plan.close()
+
+
+def test_graph_replays_match_eager_bf16_wx256():
+    """The 256 x 256, C = 256, bfloat16 layer and backward (direct-to-LDS
+    GEMMs, the adjoint mixing from the filters as stored, the streamed DFTs,
+    the inverse over batch items) captured and replayed; random inputs of the
+    workload's shapes (a replay is compared with the eager call, not with the
+    oracle)."""
+    assert torch.cuda.is_available()
+    w = syn.workload("wx256")
+    plan = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_out, w.dtype)
+    gen = torch.Generator(device="cuda").manual_seed(5)
+
+    def rnd(*shape, scale=1.0):
+        t = plan.empty(*shape)
+        t.copy_((torch.randn(t.shape, device="cuda", generator=gen) * scale).to(torch.bfloat16))
+        return t
+
+    Si, So = len(w.spins_in), len(w.spins_out)
+    xd = rnd(w.B, Si, w.C_in, w.H, w.W)
+    Kd = rnd(w.L, So, w.C_out, Si, w.C_in, scale=0.05)
+    gd = rnd(w.B, So, w.C_out, w.H, w.W)
+    y = plan.empty(w.B, So, w.C_out, w.H, w.W)
+    gx = plan.empty(w.B, Si, w.C_in, w.H, w.W)
+    gk = plan.empty(w.L, So, w.C_out, Si, w.C_in)
+
+    def step():
+        plan.conv(xd, Kd, y)
+        plan.conv_backward(xd, Kd, gd, grad_x=gx, grad_filters=gk)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [y.clone(), gx.clone(), gk.clone()]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for rep in range(3):
+        for t in (y, gx, gk):
+            t.zero_()
+        plan.forward(xd)
+        g.replay()
+        torch.cuda.synchronize()
+        for got, want in zip((y, gx, gk), ref):
+            assert torch.equal(got, want), ("wx256", rep)
+    del g
+    plan.close()
