@@ -272,10 +272,14 @@ hipError_t launch_geom(const Plan& p, int B, int Cin, int Cout, const void* coef
 // per row and copy).  Each wave owns one block of 32 expanded rows (16
 // coefficient rows) x TN blocks of 32 outputs, MFMA 32x32x2 f32; the
 // workgroup covers WM x WN such wave tiles, i.e. 16 WM coefficient rows x
-// 32 TN WN outputs.  A lane's A value for row 2i (re, -im) / 2i+1 (im, re) is
-// picked from the 16-byte chunk of coefficient row i (two complex entries,
-// two MFMA steps) by the parity of its row and its K half; the filter rows
-// enter as stored (re, im).
+// 32 TN WN outputs.  The contraction order inside a 16-byte chunk (complex
+// entries 2c, 2c + 1) is chosen so that each lane needs only one entry: the
+// chunk's first MFMA step pairs the real parts of the filter values, the
+// second the imaginary parts, and lane half kh holds entry 2c + kh; so a lane
+// reads 8 bytes of its coefficient row and 8 of its filter row, and its A
+// values are (re, -im) for even expanded rows, (im, re) for odd ones (mol
+// mixing 18.5 -> 17.5 us, wx128 36.8 -> 34.7 us against picking two of the
+// four floats of a whole 16-byte read).
 template <int WM, int WN, int ST, int TN>
 struct MixGeomF {
   static constexpr int BK = 32;                 // floats per row per K step
@@ -300,9 +304,9 @@ struct MixGeomF {
 };
 
 // ADJ: the adjoint from the filters as stored, as for bfloat16 above; the
-// expanded rows are (re, im) / (im, -re) and a lane reads the one filter
-// value of its MFMA step (contraction row, output column, its K half) from
-// the k-major tile (64 lanes: 64 consecutive dwords).
+// A values are (re, im) for even rows, (im, -re) for odd ones, and a lane
+// reads its filter entry (contraction row 2c + kh, its output column) as 8
+// bytes of the k-major tile (32 lanes: 256 contiguous bytes).
 template <int WM, int WN, int ST, int TN, bool ADJ>
 __global__ void __launch_bounds__((MixGeomF<WM, WN, ST, TN>::NT))
     mix_dma_f32_kernel(const float* __restrict__ coef, const float* __restrict__ K,
@@ -397,11 +401,7 @@ __global__ void __launch_bounds__((MixGeomF<WM, WN, ST, TN>::NT))
     if (s < nk) issue(s, s);
 
   const int r32 = lane & 31, kh = lane >> 5;
-  const int cr = wm * 16 + (r32 >> 1);      // coefficient row of this lane's A row
-  const bool sel_im = ((r32 & 1) ^ kh) != 0;  // (re, -im) / (im, re): which part
-  // negated: the imaginary part of even rows; adjoint ((re, im) / (im, -re)):
-  // the real part of odd rows
-  const float sgn = (((r32 & 1) != 0) == ADJ && kh == 1) ? -1.f : 1.f;
+  const int cr = wm * 16 + (r32 >> 1);  // coefficient row of this lane's A row
   for (int i = 0; i < nk; ++i) {
     const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
     wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
@@ -409,48 +409,49 @@ __global__ void __launch_bounds__((MixGeomF<WM, WN, ST, TN>::NT))
     if (i + ST - 1 < nk) issue(i + ST - 1, (i + ST - 1) % ST);
     const unsigned char* As = smem + (i % ST) * G::STAGE;
     const unsigned char* Bs = As + RA * G::PITCH;
-    auto lda = [&](int cc) {
-      return *reinterpret_cast<const float4*>(As + cr * G::PITCH + swz<G::CPR>(cr, cc) * 16);
+    // the two MFMA steps of a 16-byte chunk (complex entries 2cc, 2cc + 1)
+    // take the real parts (step 0) and then the imaginary parts (step 1),
+    // lane half kh holding entry 2cc + kh: each lane reads only its 8-byte
+    // half of both operands.  Row parity picks the expansion: forward
+    // (re | -im) / (im | re), adjoint (re | im) / (im | -re).
+    const bool odd = (r32 & 1) != 0;
+    auto lda2 = [&](int cc) {
+      return *reinterpret_cast<const float2*>(As + cr * G::PITCH + swz<G::CPR>(cr, cc) * 16 +
+                                              kh * 8);
     };
-    auto ldb = [&](int jj, int cc) {
+    auto ldb2 = [&](int jj, int cc) {
       const int q = wn * 32 * TN + jj * 32 + r32;
-      if constexpr (!ADJ) {
-        return *reinterpret_cast<const float4*>(Bs + q * G::PITCH + swz<G::CPR>(q, cc) * 16);
-      } else {
-        // contraction rows 2cc and 2cc + 1 of output q, this lane's K half
-        const float* p0 = reinterpret_cast<const float*>(Bs + 2 * cc * G::PITCH_T + q * 8 + kh * 4);
-        return make_float4(p0[0], p0[G::PITCH_T / 4], 0.f, 0.f);
-      }
+      if constexpr (!ADJ)
+        return *reinterpret_cast<const float2*>(Bs + q * G::PITCH + swz<G::CPR>(q, cc) * 16 +
+                                                kh * 8);
+      else
+        return *reinterpret_cast<const float2*>(Bs + (2 * cc + kh) * G::PITCH_T + q * 8);
     };
-    // chunk cc + 1 is read while the MFMAs of chunk cc run
-    float4 av = lda(0), bv[TN];
+    float2 a2 = lda2(0), b2[TN];
 #pragma unroll
-    for (int jj = 0; jj < TN; ++jj) bv[jj] = ldb(jj, 0);
+    for (int jj = 0; jj < TN; ++jj) b2[jj] = ldb2(jj, 0);
 #pragma unroll
-    for (int cc = 0; cc < G::CPR; ++cc) {  // two complex entries = two MFMA steps
-      float4 nav = av, nb[TN];
+    for (int cc = 0; cc < G::CPR; ++cc) {
+      float2 na = a2, nb[TN];
 #pragma unroll
-      for (int jj = 0; jj < TN; ++jj) nb[jj] = bv[jj];
+      for (int jj = 0; jj < TN; ++jj) nb[jj] = b2[jj];
       if (cc + 1 < G::CPR) {
-        nav = lda(cc + 1);
+        na = lda2(cc + 1);
 #pragma unroll
-        for (int jj = 0; jj < TN; ++jj) nb[jj] = ldb(jj, cc + 1);
+        for (int jj = 0; jj < TN; ++jj) nb[jj] = ldb2(jj, cc + 1);
       }
+      const float a0 = odd ? a2.y : a2.x;
+      const float a1 = ADJ ? (odd ? -a2.x : a2.y) : (odd ? a2.x : -a2.y);
 #pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const float a = sgn * (sel_im ? (e ? av.w : av.y) : (e ? av.z : av.x));
+      for (int jj = 0; jj < TN; ++jj)
+        acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b2[jj].x, acc[jj], 0, 0, 0);
 #pragma unroll
-        for (int jj = 0; jj < TN; ++jj) {
-          const float b = ADJ ? (e ? bv[jj].y : bv[jj].x)
-                              : kh ? (e ? bv[jj].w : bv[jj].y) : (e ? bv[jj].z : bv[jj].x);
-          acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc[jj], 0, 0, 0);
-        }
-      }
-      av = nav;
+      for (int jj = 0; jj < TN; ++jj)
+        acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b2[jj].y, acc[jj], 0, 0, 0);
+      a2 = na;
 #pragma unroll
-      for (int jj = 0; jj < TN; ++jj) bv[jj] = nb[jj];
-      if (cc + 1 < G::CPR)
-        __builtin_amdgcn_sched_group_barrier(0x100, ADJ ? 1 + 2 * TN : 1 + TN, 0);  // LDS reads
+      for (int jj = 0; jj < TN; ++jj) b2[jj] = nb[jj];
+      if (cc + 1 < G::CPR) __builtin_amdgcn_sched_group_barrier(0x100, 1 + TN, 0);  // LDS reads
       __builtin_amdgcn_sched_group_barrier(0x008, 2 * TN, 0);                      // MFMA
       __builtin_amdgcn_sched_barrier(0);
     }
