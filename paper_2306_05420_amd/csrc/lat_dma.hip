@@ -197,8 +197,9 @@ __global__ void __launch_bounds__((FwdGeom<BK, RA, RB, ST>::NT))
 }
 
 // Float forward: K steps of 32 latitudes (128 bytes per row and copy); each
-// of the 4 waves owns 32 rows l x 64 columns n' (two MFMA 32x32x2 chains, a
-// lane's two K values of a step taken from one 16-byte chunk); the
+// of the 4 waves owns 32 rows l x 64 columns n' (two MFMA 32x32x2 chains;
+// a 16-byte chunk's four latitudes feed two steps, lane half kh taking
+// latitudes 2 kh and 2 kh + 1 from one 8-byte read of each operand); the
 // workgroup covers 32 WM rows x 64 WN columns.
 template <int WM, int WN, int ST>
 struct FwdGeomF {
@@ -291,18 +292,21 @@ __global__ void __launch_bounds__((FwdGeomF<WM, WN, ST>::NT))
     }
     const unsigned char* As = smem + (i % ST) * G::STAGE;
     const unsigned char* Bs = As + RA * G::PITCH;
+    // a chunk's four latitudes feed two MFMA steps; lane half kh takes
+    // latitudes 2 kh and 2 kh + 1 of it (steps 0 and 1) from one 8-byte read
     auto lda = [&](int cc) {
-      return *reinterpret_cast<const float4*>(As + ra * G::PITCH + swz<G::CPR>(ra, cc) * 16);
+      return *reinterpret_cast<const float2*>(As + ra * G::PITCH + swz<G::CPR>(ra, cc) * 16 +
+                                              kh * 8);
     };
     auto ldb = [&](int jj, int cc) {
       const int r = wn * 64 + jj * 32 + r32;
-      return *reinterpret_cast<const float4*>(Bs + r * G::PITCH + swz<G::CPR>(r, cc) * 16);
+      return *reinterpret_cast<const float2*>(Bs + r * G::PITCH + swz<G::CPR>(r, cc) * 16 + kh * 8);
     };
     // chunk cc + 1 is read while the MFMAs of chunk cc run
-    float4 av = lda(0), bv0 = ldb(0, 0), bv1 = ldb(1, 0);
+    float2 av = lda(0), bv0 = ldb(0, 0), bv1 = ldb(1, 0);
 #pragma unroll
     for (int cc = 0; cc < G::CPR; ++cc) {  // four latitudes = two MFMA steps
-      float4 nav = av, nb0 = bv0, nb1 = bv1;
+      float2 nav = av, nb0 = bv0, nb1 = bv1;
       if (cc + 1 < G::CPR) {
         nav = lda(cc + 1);
         nb0 = ldb(0, cc + 1);
@@ -310,9 +314,9 @@ __global__ void __launch_bounds__((FwdGeomF<WM, WN, ST>::NT))
       }
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        const float a = kh ? (e ? av.w : av.y) : (e ? av.z : av.x);
-        const float b0 = kh ? (e ? bv0.w : bv0.y) : (e ? bv0.z : bv0.x);
-        const float b1 = kh ? (e ? bv1.w : bv1.y) : (e ? bv1.z : bv1.x);
+        const float a = e ? av.y : av.x;
+        const float b0 = e ? bv0.y : bv0.x;
+        const float b1 = e ? bv1.y : bv1.x;
         acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b0, acc[0], 0, 0, 0);
         acc[1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b1, acc[1], 0, 0, 0);
       }
@@ -517,11 +521,12 @@ __global__ void __launch_bounds__((InvGeom<RA, RB, ST>::NT))
 }
 
 // Float inverse: K steps of 32 degrees.  The coefficient tile enters LDS
-// K-major ([l][n'], 4 RA bytes per degree row, 16-byte chunks of odd rows
-// moved by 128 bytes so that the two K halves of a read hit different banks)
-// and a lane reads its n' at degree 2 step + K half as one float; the table
-// rows j (K = l contiguous) give both K values of two steps in one 16-byte
-// chunk.  Each wave owns TM x TN (TM TN = 2) MFMA 32x32x2 blocks of
+// K-major ([l][n'], 4 RA bytes per degree row, 16-byte chunks of rows with
+// degree bit 1 set moved by 128 bytes so that the two lane halves of a read
+// hit different banks); of a chunk's four degrees 4c .. 4c + 3, lane half kh
+// takes 4c + 2 kh and 4c + 2 kh + 1 (steps 0 and 1): one float of the
+// coefficient tile per step and one 8-byte read of its table row j (K = l
+// contiguous) per chunk.  Each wave owns TM x TN (TM TN = 2) MFMA 32x32x2 blocks of
 // (n', j); the n' tile may span several batch items (a lane keeps its own
 // column offset, only the degree row moves per K step).
 template <int TM, int WM, int WN, int ST>
@@ -546,8 +551,10 @@ struct InvGeomF {
                 "tile shape");
 };
 
-// chunk slot of a degree row of the float coefficient tile
-__device__ __forceinline__ int swa(int k, int c) { return c ^ ((k & 1) << 3); }
+// chunk slot of a degree row of the float coefficient tile: the 16-byte
+// chunks of degree rows with bit 1 set move by 128 bytes, so the two lane
+// halves of a read (degrees 4c + e and 4c + 2 + e) hit different banks
+__device__ __forceinline__ int swa(int k, int c) { return c ^ (((k >> 1) & 1) << 3); }
 
 template <int TM, int WM, int WN, int ST>
 __global__ void __launch_bounds__((InvGeomF<TM, WM, WN, ST>::NT))
@@ -649,23 +656,26 @@ __global__ void __launch_bounds__((InvGeomF<TM, WM, WN, ST>::NT))
       const int n = wm * 32 * TM + ii * 32 + r32;
       return *reinterpret_cast<const float*>(As + k * G::PITCH_A + swa(k, n >> 2) * 16 + (n & 3) * 4);
     };
+    // a chunk's four degrees feed two MFMA steps; lane half kh takes degrees
+    // 2 kh and 2 kh + 1 of it (steps 0 and 1), one 8-byte table read
     auto ldb = [&](int jj, int cc) {
       const int r = wn * 32 * TN + jj * 32 + r32;
-      return *reinterpret_cast<const float4*>(Bs + r * G::PITCH_B + swz<G::CPR_B>(r, cc) * 16);
+      return *reinterpret_cast<const float2*>(Bs + r * G::PITCH_B + swz<G::CPR_B>(r, cc) * 16 +
+                                              kh * 8);
     };
 #pragma unroll
     for (int cc = 0; cc < G::CPR_B; ++cc) {  // four degrees = two MFMA steps
-      float4 bv[TN];
+      float2 bv[TN];
 #pragma unroll
       for (int jj = 0; jj < TN; ++jj) bv[jj] = ldb(jj, cc);
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         float a[TM];
 #pragma unroll
-        for (int ii = 0; ii < TM; ++ii) a[ii] = lda(ii, 4 * cc + 2 * e + kh);
+        for (int ii = 0; ii < TM; ++ii) a[ii] = lda(ii, 4 * cc + 2 * kh + e);
 #pragma unroll
         for (int jj = 0; jj < TN; ++jj) {
-          const float b = kh ? (e ? bv[jj].w : bv[jj].y) : (e ? bv[jj].z : bv[jj].x);
+          const float b = e ? bv[jj].y : bv[jj].x;
 #pragma unroll
           for (int ii = 0; ii < TM; ++ii)
             acc[ii][jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[ii], b, acc[ii][jj], 0, 0, 0);
