@@ -42,9 +42,10 @@
  *  per-call buffer, including a workspace of at least swsft_workspace_bytes.
  *  Calls never allocate, never synchronize and enqueue all work on `stream`
  *  (a hipStream_t; NULL is the null stream) of the plan's device; results are
- *  ready when the stream reaches them.  A plan is immutable after creation;
- *  calls on different streams may run concurrently if their workspaces and
- *  outputs are distinct.
+ *  ready when the stream reaches them.  A plan is immutable after creation
+ *  (apart from the stage-timing record, see swsft_stage_timing); calls on
+ *  different streams may run concurrently if their workspaces and outputs
+ *  are distinct.
  *
  * Errors
  *  Every call validates its arguments on the host before enqueuing
@@ -148,6 +149,7 @@ size_t swsft_workspace_bytes(swsft_plan p, int op, int B, int C_in, int C_out);
  *  x     [B][S_in][C][H][W] complex, read only.
  *  coef  [L*L][B][S_in][C] complex, written (rows l < |s| set to 0).
  *  ws    workspace of ws_bytes >= swsft_workspace_bytes(p, SWSFT_OP_FORWARD, B, C, 0).
+ *  coef and ws must not overlap each other or x (SWSFT_E_INVALID).
  */
 swsft_status swsft_forward(swsft_plan p, int B, int C, const void* x, void* coef, void* ws,
                            size_t ws_bytes, void* stream);
@@ -158,6 +160,7 @@ swsft_status swsft_forward(swsft_plan p, int B, int C, const void* x, void* coef
  *  coef  [L*L][B][S_out][C] complex, read only (rows l < |s| ignored).
  *  y     [B][S_out][C][H][W] complex, written.
  *  ws    workspace of ws_bytes >= swsft_workspace_bytes(p, SWSFT_OP_INVERSE, B, 0, C).
+ *  y and ws must not overlap each other or coef (SWSFT_E_INVALID).
  */
 swsft_status swsft_inverse(swsft_plan p, int B, int C, const void* coef, void* y, void* ws,
                            size_t ws_bytes, void* stream);
@@ -171,8 +174,9 @@ swsft_status swsft_inverse(swsft_plan p, int B, int C, const void* coef, void* y
  *  y  = inverse(a')                                  on spins_out
  *  x        [B][S_in][C_in][H][W] complex, read only.
  *  filters  [L][S_out][C_out][S_in][C_in] complex, read only.
- *  y        [B][S_out][C_out][H][W] complex, written; must not overlap x.
+ *  y        [B][S_out][C_out][H][W] complex, written.
  *  ws       workspace of ws_bytes >= swsft_workspace_bytes(p, SWSFT_OP_CONV, B, C_in, C_out).
+ *  y and ws must not overlap each other, x or filters (SWSFT_E_INVALID).
  */
 swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, const void* x,
                                    const void* filters, void* y, void* ws, size_t ws_bytes,
@@ -198,8 +202,8 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
  *  grad_y        [B][S_out][C_out][H][W] complex, read only.
  *  grad_x        [B][S_in][C_in][H][W] complex, written; NULL: not computed.
  *  grad_filters  [L][S_out][C_out][S_in][C_in] complex, written; NULL: not computed.
- *  At least one output must be requested.  Outputs must not overlap each
- *  other or an input that is read; an input that no requested output needs
+ *  At least one output must be requested.  Outputs and the workspace must not
+ *  overlap each other or an input that is read; an input that no requested output needs
  *  (x for grad_x alone, filters for grad_filters alone) may be NULL.
  *  Returns SWSFT_E_INVALID / SWSFT_E_WORKSPACE on bad arguments before any
  *  launch, SWSFT_E_HIP if a launch fails.  Results are deterministic: no
@@ -351,7 +355,10 @@ const char* swsft_last_error(void);
  * i < n (stage i is named by swsft_stage_name(i)), clears the record and
  * returns the number of stages.  Disabled by default; enabling costs two
  * event records per launch.  At most 4096 launches are recorded between
- * reads; later ones are not timed.
+ * reads; later ones are not timed.  The record is shared by every call on
+ * the plan: while timing is enabled, each launch and each read-out takes one
+ * library-wide lock, so calls from several threads stay correct (and are
+ * serialised launch by launch); a plan without timing takes no lock.
  */
 swsft_status swsft_stage_timing(swsft_plan p, int enable);
 int swsft_stage_times(swsft_plan p, double* ms, long long* launches, int n);

@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <initializer_list>
 #include <map>
 #include <mutex>
 #include <new>
@@ -77,8 +78,31 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
   return pa != nullptr && pb != nullptr && pa < pb + nb && pb < pa + na;
 }
 
+// A buffer of a call: written by the call (outputs and the workspace) or
+// only read.  Buffers that are both read need not be disjoint; a written
+// buffer must not overlap any other buffer of the call.
+struct Region {
+  const void* ptr;
+  size_t bytes;
+  const char* name;
+  bool written;
+};
+
+swsft_status check_disjoint(std::initializer_list<Region> rs) {
+  for (auto a = rs.begin(); a != rs.end(); ++a)
+    for (auto b = a + 1; b != rs.end(); ++b)
+      if ((a->written || b->written) && overlaps(a->ptr, a->bytes, b->ptr, b->bytes))
+        return fail(SWSFT_E_INVALID, "%s and %s overlap", a->name, b->name);
+  return SWSFT_OK;
+}
+
 size_t filter_elems(const Plan& p, int Cin, int Cout) {
   return (size_t)p.L * p.n_out * Cout * p.n_in * Cin * 2;
+}
+
+// Bytes of a [B][S][C][H][W] complex field of the storage type.
+size_t spatial_bytes(const Plan& p, int S, int B, int C) {
+  return (size_t)B * S * C * p.H * p.W * 2 * p.elem;
 }
 
 size_t ws_need(const Plan& p, int op, int B, int Cin, int Cout) {
@@ -169,9 +193,17 @@ swsft_status check_device(const Plan& p) {
   return SWSFT_OK;
 }
 
+// Stage timing appends to the plan's event record; calls on a timing-enabled
+// plan from several threads take this lock for every launch (and
+// swsft_stage_times for the read-out), so the record stays consistent.  A
+// plan without timing takes no lock.
+std::mutex g_timing_mu;
+
 // Launch one stage, bracketed by timing events when enabled.
 template <class F>
 swsft_status run_stage(Plan& p, int stage, hipStream_t st, const char* name, F&& launch) {
+  std::unique_lock<std::mutex> lock(g_timing_mu, std::defer_lock);
+  if (p.timing) lock.lock();
   const bool timed = p.timing && p.ev != nullptr && p.n_timed < swsft::kMaxTimedLaunches;
   if (timed) {
     hipError_t e = hipEventRecord(p.ev[2 * p.n_timed], st);
@@ -485,6 +517,9 @@ swsft_status swsft_forward(swsft_plan p, int B, int C, const void* x, void* coef
   SWSFT_TRY(check_ptr(x, "x"));
   SWSFT_TRY(check_ptr(coef, "coef"));
   SWSFT_TRY(check_ws(*p, SWSFT_OP_FORWARD, B, C, 1, ws, ws_bytes));
+  SWSFT_TRY(check_disjoint({{x, spatial_bytes(*p, p->n_in, B, C), "x", false},
+                            {coef, swsft::coef_elems(*p, p->n_in, B, C) * p->elem, "coef", true},
+                            {ws, ws_bytes, "the workspace", true}}));
   SWSFT_TRY(check_device(*p));
   hipStream_t st = static_cast<hipStream_t>(stream);
   char* X = static_cast<char*>(ws);
@@ -501,6 +536,9 @@ swsft_status swsft_inverse(swsft_plan p, int B, int C, const void* coef, void* y
   SWSFT_TRY(check_ptr(y, "y"));
   SWSFT_TRY(check_inverse_stage(*p));
   SWSFT_TRY(check_ws(*p, SWSFT_OP_INVERSE, B, 1, C, ws, ws_bytes));
+  SWSFT_TRY(check_disjoint({{coef, swsft::coef_elems(*p, p->n_out, B, C) * p->elem, "coef", false},
+                            {y, spatial_bytes(*p, p->n_out, B, C), "y", true},
+                            {ws, ws_bytes, "the workspace", true}}));
   SWSFT_TRY(check_device(*p));
   hipStream_t st = static_cast<hipStream_t>(stream);
   char* Y = static_cast<char*>(ws);
@@ -530,10 +568,11 @@ swsft_status conv_forward(swsft_plan p, int B, int C_in, int C_out, const void* 
   const size_t ys = (size_t)B * p->n_out * C_out * p->H * p->W * 2 * p->elem;
   const size_t cs = swsft::coef_elems(*p, p->n_in, B, C_in) * p->elem;
   const size_t ks = filter_elems(*p, C_in, C_out) * p->elem;
-  if (overlaps(x, xs, y, ys)) return fail(SWSFT_E_INVALID, "x and y overlap");
-  if (overlaps(coef_x, cs, x, xs) || overlaps(coef_x, cs, y, ys) ||
-      overlaps(coef_x, cs, filters, ks) || overlaps(coef_x, cs, ws, ws_bytes))
-    return fail(SWSFT_E_INVALID, "coef_x overlaps another argument");
+  SWSFT_TRY(check_disjoint({{x, xs, "x", false},
+                            {filters, ks, "filters", false},
+                            {y, ys, "y", true},
+                            {coef_x, cs, "coef_x", true},
+                            {ws, ws_bytes, "the workspace", true}}));
   SWSFT_TRY(check_device(*p));
   hipStream_t st = static_cast<hipStream_t>(stream);
   const size_t xin = swsft::xy_elems(*p, p->n_in, B, C_in);
@@ -626,6 +665,10 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
       const char *a = static_cast<const char*>(grad_x), *b = static_cast<const char*>(grad_filters);
       if (a < b + ks && b < a + xs) return fail(SWSFT_E_INVALID, "grad_x and grad_filters overlap");
     }
+    for (const R& r : ins)
+      if (overlaps(ws, ws_bytes, r.a, r.n)) return fail(SWSFT_E_INVALID, "the workspace overlaps an input");
+    for (const R& r : outs)
+      if (overlaps(ws, ws_bytes, r.a, r.n)) return fail(SWSFT_E_INVALID, "the workspace overlaps an output");
   }
   SWSFT_TRY(check_device(*p));
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -932,6 +975,7 @@ swsft_status swsft_stage_timing(swsft_plan p, int enable) {
       if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
     }
   }
+  std::lock_guard<std::mutex> lock(g_timing_mu);
   p->timing = enable != 0;
   p->n_timed = 0;
   return SWSFT_OK;
@@ -939,6 +983,7 @@ swsft_status swsft_stage_timing(swsft_plan p, int enable) {
 
 int swsft_stage_times(swsft_plan p, double* ms, long long* launches, int n) {
   if (p == nullptr) return 0;
+  std::lock_guard<std::mutex> lock(g_timing_mu);
   for (int i = 0; i < p->n_timed; ++i) {
     const int s = p->ev_stage[i];
     if (hipEventSynchronize(p->ev[2 * i + 1]) != hipSuccess) continue;

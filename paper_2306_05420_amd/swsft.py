@@ -129,7 +129,8 @@ class Plan:
     with the J and G symmetries).
 
     Owns the device tables built by swsft_plan_create; workspaces are cached
-    per call shape (allocated through torch, i.e. by the caller of the C ABI).
+    per call shape and stream (allocated through torch, i.e. by the caller of
+    the C ABI), so calls with the same shape on two streams never share one.
     """
 
     def __init__(self, H: int, W: int, L: int, spins_in, spins_out, dtype: str = "f32",
@@ -206,8 +207,12 @@ class Plan:
     def workspace_bytes(self, op: int, B: int, C_in: int, C_out: int) -> int:
         return int(lib().swsft_workspace_bytes(self._h, op, B, C_in, C_out))
 
-    def workspace(self, op: int, B: int, C_in: int, C_out: int) -> torch.Tensor:
-        key = (op, B, C_in, C_out)
+    def workspace(self, op: int, B: int, C_in: int, C_out: int, stream: int = None) -> torch.Tensor:
+        """The cached workspace of one call shape on one stream (a stream
+        handle as passed to the library; None: the current stream)."""
+        if stream is None:
+            stream = _stream_handle(None)
+        key = (op, B, C_in, C_out, stream)
         ws = self._ws.get(key)
         if ws is None:
             n = self.workspace_bytes(op, B, C_in, C_out)
@@ -227,7 +232,8 @@ class Plan:
             coef = self.empty(self.L * self.L, B, S, C)
         cr = self.real_view(coef)
         self._shape(cr, (self.L * self.L, B, S, C), "coef")
-        ws = self.workspace(OP_FORWARD, B, C, 1)
+        sh = _stream_handle(stream)
+        ws = self.workspace(OP_FORWARD, B, C, 1, sh)
         _check(lib().swsft_forward(self._h, B, C, xr.data_ptr(), cr.data_ptr(), ws.data_ptr(),
                                    ws.numel(), _stream_handle(stream)), "swsft_forward")
         return coef
@@ -241,7 +247,8 @@ class Plan:
             y = self.empty(B, S, C, self.H, self.W)
         yr = self.real_view(y)
         self._shape(yr, (B, S, C, self.H, self.W), "y")
-        ws = self.workspace(OP_INVERSE, B, 1, C)
+        sh = _stream_handle(stream)
+        ws = self.workspace(OP_INVERSE, B, 1, C, sh)
         _check(lib().swsft_inverse(self._h, B, C, cr.data_ptr(), yr.data_ptr(), ws.data_ptr(),
                                    ws.numel(), _stream_handle(stream)), "swsft_inverse")
         return y
@@ -262,7 +269,8 @@ class Plan:
             y = self.empty(B, len(self.spins_out), Cout, self.H, self.W)
         yr = self.real_view(y)
         self._shape(yr, (B, len(self.spins_out), Cout, self.H, self.W), "y")
-        ws = self.workspace(OP_CONV, B, Cin, Cout)
+        sh = _stream_handle(stream)
+        ws = self.workspace(OP_CONV, B, Cin, Cout, sh)
         if coef_x is None or coef_x is False:
             _check(lib().spin_sph_conv_forward(self._h, B, Cin, Cout, xr.data_ptr(),
                                                kr.data_ptr(), yr.data_ptr(), ws.data_ptr(),
@@ -321,7 +329,8 @@ class Plan:
             cr = self.real_view(coef_x)
             self._shape(cr, (self.L * self.L, B, S, Cin), "coef_x")
             cx_ptr = cr.data_ptr()
-        ws = self.workspace(OP_CONV_BACKWARD, B, Cin, Cout)
+        sh = _stream_handle(stream)
+        ws = self.workspace(OP_CONV_BACKWARD, B, Cin, Cout, sh)
         _check(lib().spin_sph_conv_backward(self._h, B, Cin, Cout, xr.data_ptr(), cx_ptr,
                                             kr.data_ptr(), gr.data_ptr(), gx_ptr, gk_ptr,
                                             ws.data_ptr(), ws.numel(), _stream_handle(stream)),
@@ -389,7 +398,8 @@ class Plan:
         orr = self.real_view(out)
         self._shape(orr, tuple(cr.shape[:-1]), "out")
         var_out = torch.empty((S, C), dtype=torch.float32, device=self.device)
-        ws = self.workspace(OP_BATCH_NORM, B, 1, C)
+        sh = _stream_handle(stream)
+        ws = self.workspace(OP_BATCH_NORM, B, 1, C, sh)
         _check(lib().spin_sph_spectral_batch_norm(
             self._h, B, C, cr.data_ptr(), gamma.data_ptr(),
             None if beta is None else beta.data_ptr(), float(eps),
@@ -449,14 +459,18 @@ class ResidualBlock:
         self.p_out.close()
         self._ws = {}
 
-    def workspace(self, B: int) -> torch.Tensor:
-        ws = self._ws.get(B)
+    def workspace(self, B: int, stream: int = None) -> torch.Tensor:
+        """The cached workspace of batch B on one stream (None: the current one)."""
+        if stream is None:
+            stream = _stream_handle(None)
+        key = (B, stream)
+        ws = self._ws.get(key)
         if ws is None:
             n = int(lib().swsft_block_workspace_bytes(self.p_in._h, self.p_out._h, B, self.C))
             if n == 0:
                 raise ValueError("invalid workspace request")
             ws = torch.empty(n, dtype=torch.uint8, device=self.p_out.device)
-            self._ws[B] = ws
+            self._ws[key] = ws
         return ws
 
     def forward(self, x, K1, K2, gamma1, beta1, gamma2, beta2, pc1, pc2, eps: float = 1e-5,
@@ -492,7 +506,8 @@ class ResidualBlock:
                           gamma2.data_ptr(), ptr(beta2), pc1[0].data_ptr(), pc1[1].data_ptr(),
                           pc1[2].data_ptr(), pc2[0].data_ptr(), pc2[1].data_ptr(),
                           pc2[2].data_ptr(), float(eps), v1.data_ptr(), v2.data_ptr())
-        ws = self.workspace(B)
+        sh = _stream_handle(stream)
+        ws = self.workspace(B, sh)
         _check(lib().spin_sph_residual_block_forward(self.p_in._h, po._h, B, C, xr.data_ptr(),
                                                      ctypes.byref(prm), yr.data_ptr(),
                                                      ws.data_ptr(), ws.numel(),

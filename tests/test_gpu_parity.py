@@ -267,9 +267,23 @@ def test_call_validation_with_plan():
 
 # ---------------------------------------------------------------------------
 # The 256 x 256, C = 256, bfloat16 workload at its full size, in the launch
-# configuration the benchmark times.  The oracle computes batch item 0 (all
-# 512 input maps) and a sample of output channels one by one.
+# configuration the benchmark times.  Every output element is compared with
+# the oracle: the whole forward transform, the whole layer output (both batch
+# items, both spins, all 256 output channels) and the whole inverse.
 # ---------------------------------------------------------------------------
+
+def report(tag, got, ref, spin_axis, spins):
+    """Relative L2 over the whole tensor, printed with the per-spin relative
+    L2 and the largest absolute error."""
+    err = rel_l2(got, ref)
+    parts = []
+    for si, s in enumerate(spins):
+        g = np.take(got, si, axis=spin_axis)
+        r = np.take(ref, si, axis=spin_axis)
+        parts.append(f"spin {s}: {rel_l2(g, r):.3e} (max-abs {np.abs(g - r).max():.3e})")
+    print(f"{tag} rel-L2 {err:.3e}, max-abs {np.abs(got - ref).max():.3e}; " + "; ".join(parts))
+    return err
+
 
 @pytest.fixture(scope="module")
 def wx256():
@@ -277,37 +291,43 @@ def wx256():
     x, K, d = workload_inputs(w)
     plan = _plan(w)
     xd, Kd = to_device(x, "bf16"), to_device(K, "bf16")
-    yield w, x, K, d, plan, xd, Kd
+    a = O.forward(x, w.L, w.spins_in)          # oracle coefficients of every input map
+    yield w, x, K, a, plan, xd, Kd
     plan.close()
 
 
-def test_wx256_forward_and_conv_sampled(wx256):
-    w, x, K, d, plan, xd, Kd = wx256
-    y = from_device(plan.conv(xd, Kd)[:1])
-    coef = from_device(plan.forward(xd)[:, :1])
-    a0 = O.forward(x[:1], w.L, w.spins_in)
-    err_f = rel_l2(coef, a0)
-    cs = [0, 1, 37, 128, 255]
-    yr = O.inverse(O.mix(a0, K[:, :, cs], w.spins_in, w.spins_out), w.H, w.W, w.spins_out)
-    err_c = rel_l2(y[:, :, cs], yr)
-    print(f"wx256 forward rel-L2 {err_f:.3e}, conv (sampled channels) rel-L2 {err_c:.3e}")
-    assert err_f <= TOL["bf16"] and err_c <= TOL["bf16"]
+def test_wx256_forward_full(wx256):
+    w, x, K, a, plan, xd, Kd = wx256
+    coef = from_device(plan.forward(xd))
+    assert coef.shape == a.shape
+    err = report("wx256 forward (whole)", coef, a, 2, w.spins_in)
+    assert err <= TOL["bf16"]
+    for si, s in enumerate(w.spins_in):
+        assert np.all(coef[: abs(s) ** 2, :, si] == 0)
 
 
-def test_wx256_inverse_sampled(wx256):
-    w, x, K, d, plan, xd, Kd = wx256
+def test_wx256_conv_full(wx256):
+    w, x, K, a, plan, xd, Kd = wx256
+    y = from_device(plan.conv(xd, Kd))
+    ref = O.inverse(O.mix(a, K, w.spins_in, w.spins_out), w.H, w.W, w.spins_out)
+    assert y.shape == ref.shape == (w.B, len(w.spins_out), w.C_out, w.H, w.W)
+    err = report("wx256 conv (whole)", y, ref, 1, w.spins_out)
+    assert err <= TOL["bf16"]
+
+
+def test_wx256_inverse_full(wx256):
+    w, x, K, a, plan, xd, Kd = wx256
     rng = np.random.default_rng(4242)
-    a = round_to(syn.random_coefficients(rng, w.L, w.B, w.spins_out, w.C_out, 1.0), "bf16")
-    y = from_device(plan.inverse(to_device(a, "bf16"))[1:2, :, 100:104])
-    ref = O.inverse(np.ascontiguousarray(a[:, 1:2, :, 100:104]), w.H, w.W, w.spins_out)
-    err = rel_l2(y, ref)
-    print(f"wx256 inverse (sampled maps) rel-L2 {err:.3e}")
+    c = round_to(syn.random_coefficients(rng, w.L, w.B, w.spins_out, w.C_out, 1.0), "bf16")
+    y = from_device(plan.inverse(to_device(c, "bf16")))
+    ref = O.inverse(c, w.H, w.W, w.spins_out)
+    err = report("wx256 inverse (whole)", y, ref, 1, w.spins_out)
     assert err <= TOL["bf16"]
 
 
 def test_wx256_properties_at_full_size(wx256):
     """Round trip and exact longitude-shift equivariance on every map."""
-    w, x, K, d, plan, xd, Kd = wx256
+    w, x, K, a, plan, xd, Kd = wx256
     coef = plan.forward(xd)
     back = plan.inverse(coef)
     xr = torch.view_as_complex(xd.float())
