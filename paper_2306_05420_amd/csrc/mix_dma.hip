@@ -31,6 +31,8 @@
 // of a wave read different banks) and a lane gathers its 4 consecutive
 // contraction rows of one output as 4 dword reads.  No conjugate-transposed
 // copy of the filters is made.
+#include <type_traits>
+
 #include "lds_dma.h"
 #include "mfma_tile.h"
 #include "swsft_internal.h"
@@ -263,6 +265,239 @@ hipError_t launch_geom(const Plan& p, int B, int Cin, int Cout, const void* coef
   const int Nc = p.n_out * Cout;
   const long long blocks = (long long)tiles * ((Nc + RB - 1) / RB);
   hipLaunchKernelGGL((mix_dma_kernel<BK, RA, RB, ST, ADJ>), dim3(xcd_grid(blocks)), dim3(G::NT), 0,
+                     st, (const __bf16*)coef, (const __bf16*)K, (__bf16*)out, p.L, B, Cin, Cout,
+                     p.n_in, p.n_out, si, so);
+  return hipGetLastError();
+}
+
+// Forward mixing, bfloat16, with separate real and imaginary accumulators.
+//
+// A lane reads 16 bytes of its coefficient row (four complex values) once per
+// 16-wide K step and forms both operands in registers: (re, -im) for the
+// real part of the product and (im, re) for the imaginary part, against the
+// filter values as stored (re, im).  So the 32 rows of an MFMA operand are
+// 32 distinct coefficient rows and each LDS read feeds two MFMAs; the
+// expanded-row kernel above reads every coefficient row twice (once per
+// expanded row) and feeds one.  Each wave owns TM x TN blocks of 32
+// coefficient rows x 32 outputs (2 TM TN accumulators); the workgroup covers
+// WM x WN waves.  Row blocks past the last row of the degree issue no MFMA
+// and no operand read (wave-uniform branch), so short degrees cost about
+// their own rows rather than a whole tile.  Both operands enter a ring of ST
+// LDS stages by direct copies of whole 128-byte lines per row (64-wide K
+// steps), swizzled as in the kernel above.
+typedef unsigned v4u_t __attribute__((ext_vector_type(4)));
+
+template <int WM, int WN, int ST>
+struct MixGeomS {
+  static constexpr int BK = 64;                  // reals per row per K step
+  static constexpr int TM = 2, TN = 2;           // 32 x 32 blocks per wave
+  static constexpr int RA = 32 * TM * WM;        // coefficient rows per workgroup
+  static constexpr int RB = 32 * TN * WN;        // outputs per workgroup
+  static constexpr int NW = WM * WN, NT = 64 * NW;
+  static constexpr int PITCH = 2 * BK, CPR = PITCH / 16;
+  static constexpr int RPI = 1024 / PITCH, LPR = 64 / RPI;
+  static constexpr int NI = (RA + RB) / RPI, NI_A = RA / RPI;
+  static constexpr int PER_WAVE = NI / NW;
+  static constexpr int STAGE = (RA + RB) * PITCH;
+  static constexpr int SMEM = ST * STAGE;
+  static constexpr int MAX_KT = kMaxKp / BK;
+  static_assert(RA % RPI == 0 && NI % NW == 0, "tile shape");
+  static_assert(ST >= 2 && (ST - 2) * PER_WAVE < 64, "stages");
+};
+
+template <int WM, int WN, int ST>
+__global__ void __launch_bounds__((MixGeomS<WM, WN, ST>::NT))
+    mix_split_kernel(const __bf16* __restrict__ coef, const __bf16* __restrict__ K,
+                     __bf16* __restrict__ out, int L, int B, int Cin, int Cout, int Sin, int Sout,
+                     Spins sin_, Spins sout_) {
+  using G = MixGeomS<WM, WN, ST>;
+  constexpr int TM = G::TM, TN = G::TN, RA = G::RA, RB = G::RB, BK = G::BK;
+  extern __shared__ __align__(16) unsigned char smem[];  // G::SMEM bytes: the ring
+  __shared__ int live[G::MAX_KT];
+  __shared__ int n_live_s;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+  const int Kc = Sin * Cin, Nc = Sout * Cout;
+  const int Kp = 2 * Kc;
+  const int n_tiles_n = (Nc + RB - 1) / RB;
+
+  // logical block = ((l, row tile), column tile), largest degrees first
+  const int lbk = xcd_logical_block();
+  const int ntile = lbk % n_tiles_n;
+  int t = lbk / n_tiles_n;
+  int l = L - 1;
+  for (; l >= 0; --l) {
+    const int ntl = ((2 * l + 1) * B + RA - 1) / RA;
+    if (t < ntl) break;
+    t -= ntl;
+  }
+  if (l < 0) return;
+  const int Mrows = (2 * l + 1) * B;
+  const int row0 = t * RA;
+  const int q0 = ntile * RB;
+
+  if (tid == 0) {
+    const int per_spin = 2 * Cin / BK;
+    int n = 0;
+    for (int si = 0; si < Sin; ++si)
+      if (iabs_(sin_.s[si]) <= l)
+        for (int k = 0; k < per_spin; ++k) live[n++] = si * per_spin + k;
+    n_live_s = n;
+  }
+  __syncthreads();
+  const int nk = n_live_s;
+
+  const __bf16* A0 = coef + (size_t)l * l * B * Kp;
+  const __bf16* K0 = K + (size_t)l * Nc * Kp;
+  const unsigned ring_base = lds_addr(smem);
+
+  const __bf16* gsrc[G::PER_WAVE];
+  bool is_a[G::PER_WAVE];
+#pragma unroll
+  for (int u = 0; u < G::PER_WAVE; ++u) {
+    const int g = wave * G::PER_WAVE + u;
+    is_a[u] = g < G::NI_A;
+    if (is_a[u]) {
+      const int tr = g * G::RPI + lane / G::LPR;
+      const int row = row0 + tr < Mrows ? row0 + tr : Mrows - 1;
+      gsrc[u] = A0 + (size_t)row * Kp + swz<G::CPR>(tr, lane % G::LPR) * 8;
+    } else {
+      const int rb = (g - G::NI_A) * G::RPI + lane / G::LPR;
+      const int q = q0 + rb < Nc ? q0 + rb : Nc - 1;
+      gsrc[u] = K0 + (size_t)q * Kp + swz<G::CPR>(rb, lane % G::LPR) * 8;
+    }
+  }
+  auto issue = [&](int i, int stage) {
+    const int koff = live[i] * BK;
+    const unsigned base = ring_base + stage * G::STAGE + wave * G::PER_WAVE * 1024;
+#pragma unroll
+    for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + koff, base + u * 1024);
+  };
+
+  v16f acc_re[TM][TN], acc_im[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc_re[i][j][r] = acc_im[i][j][r] = 0.f;
+
+  // row blocks of this wave that hold rows of the degree (wave-uniform)
+  bool blk_live[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) blk_live[i] = row0 + (wm * TM + i) * 32 < Mrows;
+
+#pragma unroll
+  for (int s = 0; s < ST - 1; ++s)
+    if (s < nk) issue(s, s);
+
+  const int r32 = lane & 31, kh = lane >> 5;
+  // The K loop for NL live row blocks (0: the wave only copies and waits at
+  // the barriers); the operands of the next 16-wide step are read from LDS
+  // while the MFMAs of the current one run.
+  auto k_loop = [&](auto nl) {
+    constexpr int NL = decltype(nl)::value;
+    for (int i = 0; i < nk; ++i) {
+      const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
+      wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
+      __builtin_amdgcn_s_barrier();  // every wave's copies of step i landed; step i-1 is consumed
+      if (i + ST - 1 < nk) issue(i + ST - 1, (i + ST - 1) % ST);
+      if constexpr (NL > 0) {
+        const unsigned char* As = smem + (i % ST) * G::STAGE;
+        const unsigned char* Bs = As + RA * G::PITCH;
+        auto read = [&](int kk, v4u_t (&xa)[TM], v8bf (&xb)[TN]) {
+          const int c = 2 * kk + kh;
+#pragma unroll
+          for (int jj = 0; jj < TN; ++jj) {
+            const int rb = (wn * TN + jj) * 32 + r32;
+            xb[jj] = *reinterpret_cast<const v8bf*>(Bs + rb * G::PITCH + swz<G::CPR>(rb, c) * 16);
+          }
+#pragma unroll
+          for (int ii = 0; ii < NL; ++ii) {
+            const int cr = (wm * TM + ii) * 32 + r32;
+            xa[ii] = *reinterpret_cast<const v4u_t*>(As + cr * G::PITCH + swz<G::CPR>(cr, c) * 16);
+          }
+        };
+        v4u_t xa[TM], na[TM];
+        v8bf xb[TN], nb[TN];
+        read(0, xa, xb);
+#pragma unroll
+        for (int kk = 0; kk < BK / 16; ++kk) {
+          if (kk + 1 < BK / 16) read(kk + 1, na, nb);
+#pragma unroll
+          for (int ii = 0; ii < NL; ++ii) {
+            v4u_t xr, xi;
+#pragma unroll
+            for (int d = 0; d < 4; ++d) {
+              xr[d] = xa[ii][d] ^ 0x80000000u;                          // (re, -im)
+              xi[d] = __builtin_amdgcn_alignbit(xa[ii][d], xa[ii][d], 16u);  // (im, re)
+            }
+            const v8bf ar = __builtin_bit_cast(v8bf, xr), ai = __builtin_bit_cast(v8bf, xi);
+#pragma unroll
+            for (int jj = 0; jj < TN; ++jj) {
+              acc_re[ii][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ar, xb[jj], acc_re[ii][jj], 0, 0, 0);
+              acc_im[ii][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ai, xb[jj], acc_im[ii][jj], 0, 0, 0);
+            }
+          }
+          if (kk + 1 < BK / 16) {
+#pragma unroll
+            for (int ii = 0; ii < NL; ++ii) xa[ii] = na[ii];
+#pragma unroll
+            for (int jj = 0; jj < TN; ++jj) xb[jj] = nb[jj];
+          }
+        }
+      }
+    }
+  };
+  static_assert(TM == 2, "live-block dispatch");
+  if (blk_live[1]) k_loop(std::integral_constant<int, 2>{});
+  else if (blk_live[0]) k_loop(std::integral_constant<int, 1>{});
+  else k_loop(std::integral_constant<int, 0>{});
+  wait_vmcnt<0>();
+
+  // register r of a lane holds row 8 (r / 4) + 4 kh + r % 4 of its block,
+  // column lane % 32: one complex output, stored as one bf16 pair (the 32
+  // lanes of a row write 128 contiguous bytes).  Output spins that do not
+  // exist at this degree are written as zero.
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  const int Np = 2 * Nc;
+  const int col_l = lane & 31, row_l = 4 * (lane >> 5);
+#pragma unroll
+  for (int jj = 0; jj < TN; ++jj) {
+    const int q = q0 + (wn * TN + jj) * 32 + col_l;
+    const bool qok = q < Nc;
+    const bool tok = qok && iabs_(sout_.s[(qok ? q : 0) / Cout]) <= l;
+#pragma unroll
+    for (int ii = 0; ii < TM; ++ii) {
+      if (!blk_live[ii]) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = row0 + (wm * TM + ii) * 32 + 8 * (r >> 2) + row_l + (r & 3);
+        if (!qok || row >= Mrows) continue;
+        const f32x2_t v = tok ? (f32x2_t){acc_re[ii][jj][r], acc_im[ii][jj][r]} : (f32x2_t){0.f, 0.f};
+        *reinterpret_cast<bf16x2_t*>(out + ((size_t)l * l * B + row) * Np + 2 * q) =
+            __builtin_convertvector(v, bf16x2_t);
+      }
+    }
+  }
+}
+
+template <int WM, int WN, int ST>
+hipError_t launch_split(const Plan& p, int B, int Cin, int Cout, const void* coef, const void* K,
+                        void* out, hipStream_t st) {
+  using G = MixGeomS<WM, WN, ST>;
+  Spins si{}, so{};
+  for (int i = 0; i < p.n_in; ++i) si.s[i] = p.spins_in[i];
+  for (int i = 0; i < p.n_out; ++i) so.s[i] = p.spins_out[i];
+  long long tiles = 0;
+  for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + G::RA - 1) / G::RA;
+  const int Nc = p.n_out * Cout;
+  const long long blocks = tiles * ((Nc + G::RB - 1) / G::RB);
+  const hipError_t e = ensure_dynamic_lds((const void*)mix_split_kernel<WM, WN, ST>, G::SMEM);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((mix_split_kernel<WM, WN, ST>), dim3(xcd_grid(blocks)), dim3(G::NT), G::SMEM,
                      st, (const __bf16*)coef, (const __bf16*)K, (__bf16*)out, p.L, B, Cin, Cout,
                      p.n_in, p.n_out, si, so);
   return hipGetLastError();
@@ -512,6 +747,13 @@ hipError_t launch_geom_f32(const Plan& p, int B, int Cin, int Cout, const void* 
 #ifndef SWSFT_MIX_DMA_STAGES
 #define SWSFT_MIX_DMA_STAGES 2
 #endif
+// bf16 forward with split real / imaginary accumulators: WM, WN, ST of MixGeomS
+#ifndef SWSFT_MIX_SPLIT
+#define SWSFT_MIX_SPLIT 1
+#endif
+#ifndef SWSFT_MIX_SPLIT_GEOM
+#define SWSFT_MIX_SPLIT_GEOM 2, 2, 2
+#endif
 // float: WM, WN, ST, TN of MixGeomF
 #ifndef SWSFT_MIX_DMA_F32
 #define SWSFT_MIX_DMA_F32 2, 2, 4, 1
@@ -551,6 +793,10 @@ hipError_t launch_mix_dma(const Plan& p, int B, int Cin, int Cout, const void* c
   // steps resident (measured against 32 x 128 with 3 steps, 16 x 128, 32 x 64
   // with 2 waves and 64 x 64 with 8 waves: mol 19.4 -> 18.3 us, wx128 42.3 -> 36.4 us)
   if (p.dtype == SWSFT_F32) return launch_geom_f32<SWSFT_MIX_DMA_F32>(p, B, Cin, Cout, coef, K, out, st);
+#if SWSFT_MIX_SPLIT
+  if ((2 * Cin) % 64 == 0)
+    return launch_split<SWSFT_MIX_SPLIT_GEOM>(p, B, Cin, Cout, coef, K, out, st);
+#endif
   if ((2 * Cin) % SWSFT_MIX_DMA_BK == 0)
     return launch_geom<SWSFT_MIX_DMA_BK, SWSFT_MIX_DMA_RA, SWSFT_MIX_DMA_RB, SWSFT_MIX_DMA_STAGES>(
         p, B, Cin, Cout, coef, K, out, st);
