@@ -218,6 +218,26 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
                                     void* stream);
 
 /*
+ * spin_sph_conv_forward without a caller workspace, for callers that cannot
+ * allocate device memory (code under graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The workspace is a static array of
+ * 128 MiB that the library holds on every device it runs on until the
+ * process ends; its device address is looked up when a plan is created on
+ * that device, and this call allocates, frees and synchronizes nothing.
+ *  x, filters, y   as for spin_sph_conv_forward (y must not overlap x).
+ * Returns SWSFT_E_UNSUPPORTED, with nothing enqueued, when the layer needs
+ * more than 128 MiB of workspace (swsft_workspace_bytes(p, SWSFT_OP_CONV, B,
+ * C_in, C_out) > 134217728; e.g. the 256 x 256, C = 256, B = 2 layer).
+ * Every call on a device shares that device's array: calls that may overlap
+ * in time on one device (other streams, other threads) race and must be
+ * serialized by the caller.  The array keeps the last call's contents; the
+ * layer reads nothing of it that the same call has not written.
+ */
+swsft_status spin_sph_conv_forward_noalloc(swsft_plan p, int B, int C_in, int C_out,
+                                           const void* x, const void* filters, void* y,
+                                           void* stream);
+
+/*
  * spin_sph_conv_forward that also writes the input's coefficients F x
  * (eq. (2); [L*L][B][S_in][C_in] complex, the layout of swsft_forward) to
  * coef_x, for the backward pass to reuse: training saves them instead of

@@ -22,7 +22,8 @@ LIB = os.path.join(PKG, "libswsft.so")
 INCLUDE = os.path.join(os.path.dirname(PKG), "include")
 
 SOURCES = ["tables.hip", "delta.hip", "dft.hip", "dft_mm.hip", "gemm.hip", "mix_dma.hip", "lat_dma.hip",
-           "phase_collapse.hip", "batch_norm.hip", "backward.hip", "small.hip", "swsft_api.cpp"]
+           "phase_collapse.hip", "batch_norm.hip", "backward.hip", "small.hip", "noalloc.hip",
+           "swsft_api.cpp"]
 ARCH = "gfx950"
 
 

@@ -330,6 +330,12 @@ swsft_status swsft_plan_create_ex(int H, int W, int L, const int* spins_in, int 
     delete static_cast<swsft_plan_s*>(p);
     return hip_fail(e, "hipGetDevice");
   }
+  // the device address of the static workspace of spin_sph_conv_forward_noalloc
+  if ((e = swsft::register_scratch(p->device)) != hipSuccess) {
+    free_plan(p);
+    delete static_cast<swsft_plan_s*>(p);
+    return hip_fail(e, "hipGetSymbolAddress of the static workspace");
+  }
   const size_t fb = (size_t)p->n_in * p->fwd_table_elems() * p->elem;
   const size_t ib = (size_t)p->n_out * p->inv_table_elems() * p->elem;
   const size_t sb = (size_t)p->n_in * p->inv_table_elems() * p->elem;   // backward synthesis
@@ -605,6 +611,27 @@ swsft_status spin_sph_conv_forward(swsft_plan p, int B, int C_in, int C_out, con
                                    const void* filters, void* y, void* ws, size_t ws_bytes,
                                    void* stream) {
   return conv_forward(p, B, C_in, C_out, x, filters, y, nullptr, ws, ws_bytes, stream);
+}
+
+swsft_status spin_sph_conv_forward_noalloc(swsft_plan p, int B, int C_in, int C_out,
+                                           const void* x, const void* filters, void* y,
+                                           void* stream) {
+  g_last_error[0] = 0;
+  if (p == nullptr) return fail(SWSFT_E_INVALID, "plan is NULL");
+  SWSFT_TRY(check_bc(B, C_in, "C_in"));
+  SWSFT_TRY(check_bc(B, C_out, "C_out"));
+  SWSFT_TRY(check_filter_block(*p, C_in, C_out));
+  const size_t need = ws_need(*p, SWSFT_OP_CONV, B, C_in, C_out);
+  if (need > swsft::kNoAllocScratchBytes)
+    return fail(SWSFT_E_UNSUPPORTED,
+                "the layer needs %zu bytes of workspace; the library's static workspace holds "
+                "%zu (use spin_sph_conv_forward with a caller workspace)",
+                need, swsft::kNoAllocScratchBytes);
+  void* ws = swsft::scratch_of(p->device);
+  if (ws == nullptr)
+    return fail(SWSFT_E_INVALID, "no static workspace registered for device %d", p->device);
+  return conv_forward(p, B, C_in, C_out, x, filters, y, nullptr, ws, swsft::kNoAllocScratchBytes,
+                      stream);
 }
 
 swsft_status spin_sph_conv_forward_train(swsft_plan p, int B, int C_in, int C_out, const void* x,

@@ -87,6 +87,14 @@ inline size_t coef_elems(const Plan& p, int S, int B, int C) {
   return (size_t)p.L * p.L * (size_t)B * S * C * 2;
 }
 
+// The library-owned workspace of spin_sph_conv_forward_noalloc (noalloc.hip):
+// a file-scope device array of this many bytes on every device.
+constexpr size_t kNoAllocScratchBytes = size_t(128) << 20;
+// Look up (once per device, with that device current) and remember the
+// device address of the array; scratch_of returns it (NULL if never looked up).
+hipError_t register_scratch(int device);
+void* scratch_of(int device);
+
 // Raise a kernel's dynamic LDS limit to `bytes` (no-op up to 64 KiB).  The
 // attribute is set once per (device, kernel) and size: later launches make no
 // runtime call, so a launch sequence can be captured in a graph once it has

@@ -73,6 +73,7 @@ def lib() -> ctypes.CDLL:
         "spin_sph_conv_forward": (i, [vp, i, i, i, vp, vp, vp, vp, sz, vp]),
         "spin_sph_conv_backward": (i, [vp, i, i, i, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "spin_sph_conv_forward_train": (i, [vp, i, i, i, vp, vp, vp, vp, vp, sz, vp]),
+        "spin_sph_conv_forward_noalloc": (i, [vp, i, i, i, vp, vp, vp, vp]),
         "spin_sph_phase_collapse": (i, [vp, i, i, vp, vp, vp, vp, vp, vp]),
         "spin_sph_mix": (i, [vp, i, i, i, vp, vp, vp, vp]),
         "spin_sph_spectral_batch_norm": (i, [vp, i, i, vp, vp, vp, ctypes.c_float, vp, vp, vp,

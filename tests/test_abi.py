@@ -16,7 +16,7 @@ def L():
 
 def test_exports_every_declared_function(L):
     names = S.header_functions()
-    assert len(names) == 20
+    assert len(names) == 21
     for n in names:
         assert hasattr(L, n), n
 
@@ -75,6 +75,7 @@ def test_calls_reject_null_plan(L):
     assert L.spin_sph_conv_forward(None, 1, 1, 1, x, x, x, x, 1 << 30, None) == S.E_INVALID
     assert L.spin_sph_conv_backward(None, 1, 1, 1, x, x, x, x, x, x, x, 1 << 30, None) == S.E_INVALID
     assert L.spin_sph_conv_forward_train(None, 1, 1, 1, x, x, x, x, x, 1 << 30, None) == S.E_INVALID
+    assert L.spin_sph_conv_forward_noalloc(None, 1, 1, 1, x, x, x, None) == S.E_INVALID
     assert L.spin_sph_phase_collapse(None, 1, 1, x, x, x, x, x, None) == S.E_INVALID
     assert L.spin_sph_mix(None, 1, 1, 1, x, x, x, None) == S.E_INVALID
     assert L.spin_sph_spectral_batch_norm(None, 1, 1, x, x, None, 0.0, None, None, None, x, x,
