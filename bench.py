@@ -318,6 +318,12 @@ def main(argv=None):
             for method in ("fft", "matmul"):
                 print(dft_vs_fft_row(H, method, min(args.steps, 50), min(args.warmup, 5)),
                       flush=True)
+        print()
+        print(DFT_LAYER_HEAD)
+        for H in (256, 512, 768):
+            for method in ("fft", "matmul"):
+                print(dft_vs_fft_layer_row(H, method, min(args.steps, 20), min(args.warmup, 3)),
+                      flush=True)
         return 0
     if args.table:
         from paper_2306_05420_amd import synthetic as syn
@@ -697,6 +703,50 @@ def dft_vs_fft_row(H: int, method: str, steps: int, warmup: int) -> str:
     pk = f"{100 * fl / lon / 1e12 / PEAK_TFLOPS['bf16']:.1f}" if method == "matmul" else "—"
     return (f"| {H}² | {name} | {lon * 1e6:.1f} | {byt / lon / 1e9:.0f} | {tf} | {pk} | "
             f"{t * 1e6:.1f} | {lib} |")
+
+
+DFT_LAYER_HEAD = ("| grid | longitude stages | layer µs | forward longitude µs | "
+                  "inverse longitude µs (per call) | layer vs FFT route |\n"
+                  "|---|---|---|---|---|---|")
+_DFT_LAYER_BASE = {}
+
+
+def dft_vs_fft_layer_row(H: int, method: str, steps: int, warmup: int) -> str:
+    """The whole layer (B = 1, spins {0,1} -> {0,1}, C = 256 -> 256, bf16,
+    bandlimit H/2) with the register-FFT or the DFT-matrix longitude stages in
+    both directions: layer time and the two longitude stages (HIP events)."""
+    import torch
+
+    from paper_2306_05420_amd import swsft as S
+    from paper_2306_05420_amd import synthetic as syn
+
+    B, spins, C, L = 1, (0, 1), 256, H // 2
+    pow2 = H & (H - 1) == 0 and H <= 512
+    if method == "fft" and not pow2:
+        return f"| {H}² | register FFT | — (no FFT of this width) | — | — | — |"
+    plan = S.Plan(H, H, L, spins, spins, "bf16", longitude=method)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(H + 1)
+    x = torch.view_as_real(syn.torch_complex_normal(gen, (B, 2, C, H, H))).to(
+        torch.bfloat16).contiguous()
+    K = torch.view_as_real(syn.torch_random_filters(gen, L, spins, C, spins, C, 1.0 / (2 * C))).to(
+        torch.bfloat16).contiguous()
+    y = plan.conv(x, K)
+    t = _time_calls(lambda: plan.conv(x, K, y), steps, warmup)
+    plan.stage_timing(True)
+    for _ in range(steps):
+        plan.conv(x, K, y)
+    torch.cuda.synchronize()
+    st = plan.stage_times()
+    plan.stage_timing(False)
+    plan.close()
+    fwd = st["dft_fwd"][0] / steps * 1e3
+    inv = st["dft_inv"][0] / steps * 1e3
+    if method == "fft":
+        _DFT_LAYER_BASE[H] = t
+    rel = f"{t / _DFT_LAYER_BASE[H]:.2f}×" if H in _DFT_LAYER_BASE else "—"
+    name = "register FFT (VALU)" if method == "fft" else "DFT matrices (MFMA bf16)"
+    return f"| {H}² | {name} | {t * 1e6:.1f} | {fwd:.1f} | {inv:.1f} | {rel} |"
 
 
 def block_flops(w, H_in: int, H_out: int) -> int:

@@ -80,11 +80,12 @@ typedef enum {
 
 /* Plan creation flags (swsft_plan_create_ex). */
 typedef enum {
-  /* Forward longitude stage as a dense DFT matrix product on MFMA (the route
-   * the paper takes on TPUs: Method, "Efficient TPU implementation"; appendix
-   * "FFT vs DFT", Table 8) instead of the register FFT.  Also admits any even
-   * W for swsft_forward; calls that need the inverse longitude stage then
-   * return SWSFT_E_UNSUPPORTED unless W is a power of two <= 512. */
+  /* Forward and inverse longitude stages as dense DFT matrix products on
+   * MFMA (the route the paper takes on TPUs: Method, "Efficient TPU
+   * implementation"; appendix "FFT vs DFT", Table 8) instead of the register
+   * FFT.  Also admits widths the FFT does not take: any even W (H <= 32 or a
+   * multiple of 32), e.g. 96 or 768.  The plan then also holds the two
+   * expanded DFT matrices. */
   SWSFT_PLAN_DFT_MATMUL = 1,
   /* Latitude stages by the paper's Wigner-Delta route (Background, eqs.
    * (4)-(6)): a Fourier sum in theta on the grid (quadrature weights folded
@@ -110,8 +111,8 @@ typedef enum {
  *  H, W        grid size; H == W (the transform needs equal sample counts on
  *              both axes, appendix "WeatherBench"), H even.  Implemented:
  *              W a power of two in [2, 512] (with SWSFT_PLAN_DFT_MATMUL
- *              any even W up to 32 or multiple of 32 for the forward
- *              transform); other sizes return SWSFT_E_UNSUPPORTED.
+ *              any even W up to 32 or multiple of 32); other sizes return
+ *              SWSFT_E_UNSUPPORTED.
  *  L           bandlimit, 1 <= L <= H/2 (L < H/2 is spectral pooling:
  *              Method, "Spectral pooling").
  *  spins_in    host array of n_spins_in distinct spins, |s| < L, 1..8 of them.
@@ -128,7 +129,8 @@ swsft_status swsft_plan_create(int H, int W, int L, const int* spins_in, int n_s
 
 /* swsft_plan_create with creation flags (swsft_plan_flags; 0 is
  * swsft_plan_create).  With SWSFT_PLAN_DFT_MATMUL the plan also holds the
- * expanded DFT matrix, [2(2L-1)][2W] reals of the storage type. */
+ * expanded forward and inverse DFT matrices, [2(2L-1)][2W] and
+ * [2W][2(2L-1)] reals of the storage type. */
 swsft_status swsft_plan_create_ex(int H, int W, int L, const int* spins_in, int n_spins_in,
                                   const int* spins_out, int n_spins_out, int dtype,
                                   unsigned flags, swsft_plan* out);

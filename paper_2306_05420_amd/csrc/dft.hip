@@ -478,6 +478,7 @@ hipError_t launch_dft_fwd(const Plan& p, int S, int B, int C, const void* x, voi
 
 hipError_t launch_dft_inv(const Plan& p, int S, int B, int C, const void* Y, void* y,
                           hipStream_t st) {
+  if (p.flags & SWSFT_PLAN_DFT_MATMUL) return launch_dft_inv_matmul(p, S, B, C, Y, y, st);
   if (p.dtype == SWSFT_BF16) return dispatch_inv<__bf16>(p, S, B, C, Y, y, st);
   return dispatch_inv<float>(p, S, B, C, Y, y, st);
 }

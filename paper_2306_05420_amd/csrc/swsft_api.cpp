@@ -178,7 +178,7 @@ hipError_t ensure_dynamic_lds(const void* kern, size_t bytes) {
 namespace {
 
 swsft_status check_inverse_stage(const Plan& p) {
-  if (!p.fft_ok)
+  if (!p.fft_ok && !(p.flags & SWSFT_PLAN_DFT_MATMUL))
     return fail(SWSFT_E_UNSUPPORTED, "W = %d: the inverse longitude stage needs a power of two <= 512",
                 p.W);
   return SWSFT_OK;
@@ -233,6 +233,7 @@ void free_plan(Plan* p) {
   if (p->tab_bwd_syn) (void)hipFree(p->tab_bwd_syn);
   if (p->tab_bwd_ana) (void)hipFree(p->tab_bwd_ana);
   if (p->dft_mat) (void)hipFree(p->dft_mat);
+  if (p->dft_mat_inv) (void)hipFree(p->dft_mat_inv);
   if (p->delta_theta_fwd) (void)hipFree(p->delta_theta_fwd);
   if (p->delta_theta_inv) (void)hipFree(p->delta_theta_inv);
   if (p->delta_fwd) (void)hipFree(p->delta_fwd);
@@ -304,7 +305,7 @@ swsft_status swsft_plan_create_ex(int H, int W, int L, const int* spins_in, int 
   if (!fft_ok && !(flags & SWSFT_PLAN_DFT_MATMUL))
     return fail(SWSFT_E_UNSUPPORTED,
                 "W = %d: the FFT longitude stage takes powers of two up to 512 "
-                "(SWSFT_PLAN_DFT_MATMUL takes any even W for the forward transform)", W);
+                "(SWSFT_PLAN_DFT_MATMUL takes any even W)", W);
 
   Plan* p = new (std::nothrow) swsft_plan_s();
   if (p == nullptr) return fail(SWSFT_E_ALLOC, "host allocation of the plan failed");
@@ -392,7 +393,16 @@ swsft_status swsft_plan_create_ex(int H, int W, int L, const int* spins_in, int 
       delete static_cast<swsft_plan_s*>(p);
       return fail(SWSFT_E_ALLOC, "hipMalloc of the %zu-byte DFT matrix failed", db);
     }
+    const size_t gb = (size_t)2 * W * swsft::dft_inv_pitch(p->M) * p->elem;
+    if (hipMalloc(&p->dft_mat_inv, gb) != hipSuccess) {
+      (void)hipGetLastError();
+      p->dft_mat_inv = nullptr;
+      free_plan(p);
+      delete static_cast<swsft_plan_s*>(p);
+      return fail(SWSFT_E_ALLOC, "hipMalloc of the %zu-byte inverse DFT matrix failed", gb);
+    }
     if ((e = swsft::launch_dft_matrix(*p, nullptr)) != hipSuccess ||
+        (e = swsft::launch_dft_matrix_inv(*p, nullptr)) != hipSuccess ||
         (e = hipDeviceSynchronize()) != hipSuccess) {
       free_plan(p);
       delete static_cast<swsft_plan_s*>(p);

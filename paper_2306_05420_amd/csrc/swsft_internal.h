@@ -60,6 +60,7 @@ struct Plan {
   int coef_ldb = 0;
   unsigned flags = 0;
   void* dft_mat = nullptr;
+  void* dft_mat_inv = nullptr;  // [2W][2M]: the inverse longitude stage of SWSFT_PLAN_DFT_MATMUL
   // Wigner-Delta route (SWSFT_PLAN_DELTA / SWSFT_PLAN_DELTA_SYM): theta tables
   // and Delta tables, layouts in delta.hip
   void* delta_theta_fwd = nullptr;
@@ -111,6 +112,12 @@ hipError_t launch_dft_fwd(const Plan& p, int S, int B, int C, const void* x, voi
 hipError_t launch_dft_fwd_matmul(const Plan& p, int S, int B, int C, const void* x, void* X,
                                  hipStream_t st);
 hipError_t launch_dft_matrix(const Plan& p, hipStream_t st);
+// the dense-DFT inverse longitude stage (dft_mm.hip) and its plan-time matrix
+// [2W][dft_inv_pitch(M)] (rows padded with zeros to a multiple of 8 values)
+__host__ __device__ inline int dft_inv_pitch(int M) { return (2 * M + 7) / 8 * 8; }
+hipError_t launch_dft_inv_matmul(const Plan& p, int S, int B, int C, const void* Y, void* y,
+                                 hipStream_t st);
+hipError_t launch_dft_matrix_inv(const Plan& p, hipStream_t st);
 // the Wigner-Delta route (delta.hip): R = L rows (with the symmetries) or 2L
 int delta_rows(const Plan& p);
 size_t delta_fwd_theta_elems(const Plan& p);

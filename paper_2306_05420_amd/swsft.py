@@ -123,8 +123,8 @@ def _stream_handle(stream) -> int:
 
 class Plan:
     """A transform plan: grid H x W, bandlimit L, input/output spins, dtype,
-    the forward longitude stage ("fft": register FFT; "matmul": dense DFT
-    matrix product on MFMA, which also takes widths that are not powers of two)
+    the longitude stages ("fft": register FFT; "matmul": dense DFT matrix
+    products on MFMA, which also take widths that are not powers of two)
     and the latitude stages ("direct": precomputed d^l(theta_j) tables;
     "delta" / "delta_sym": the Wigner-Delta route of eqs. (4)-(6), without /
     with the J and G symmetries).

@@ -1,8 +1,9 @@
-"""The forward longitude stage as a dense DFT matrix product on MFMA (plans
-created with longitude="matmul"): parity of swsft_forward, and of the layer,
-against the float64 oracle, including grid widths that are not powers of two
-(which only this route takes).  Tolerances as everywhere: relative L2
-<= 1e-5 (float32 storage), <= 2e-2 (bfloat16 storage)."""
+"""The longitude stages as dense DFT matrix products on MFMA (plans created
+with longitude="matmul"): parity of swsft_forward, swsft_inverse, the layer
+and its backward pass against the float64 oracle, including grid widths that
+are not powers of two (which only this route takes: 96, 768).  Tolerances as
+everywhere: relative L2 <= 1e-5 (float32 storage), <= 2e-2 (bfloat16
+storage)."""
 
 import numpy as np
 import pytest
@@ -68,16 +69,64 @@ def test_layer_with_matmul_longitude(name):
     plan.close()
 
 
-def test_width_without_fft_rejects_the_inverse_stage():
-    plan = S.Plan(96, 96, 48, (0,), (0,), "f32", longitude="matmul")
-    c = plan.empty(48 * 48, 1, 1, 2)
-    x = plan.empty(1, 1, 2, 96, 96)
-    K = plan.empty(48, 1, 2, 1, 2)
-    for call in (lambda: plan.inverse(c), lambda: plan.conv(x, K),
-                 lambda: plan.conv_backward(x, K, x)):
-        with pytest.raises(S.SwsftError) as e:
-            call()
-        assert e.value.status == S.E_UNSUPPORTED
+@pytest.mark.parametrize("case", CASES, ids=[f"H{c[0]}L{c[1]}S{len(c[2])}C{c[4]}{c[5]}" for c in CASES])
+def test_inverse_matmul_parity(case):
+    H, L, spins, B, C, dt, _ = case
+    rng = np.random.default_rng(H * 17 + C)
+    a = round_to(syn.random_coefficients(rng, L, B, spins, C, 1.0), dt)
+    plan = S.Plan(H, H, L, spins, spins, dt, longitude="matmul")
+    got = from_device(plan.inverse(to_device(a, dt)))
+    err = rel_l2(got, O.inverse(a, H, H, spins))
+    print(f"matmul inverse {case}: rel-L2 {err:.2e}")
+    assert err <= TOL[dt]
+    plan.close()
+
+
+LAYERS = [  # H, L, spins_in, spins_out, B, C_in, C_out, dtype
+    (96, 48, (0,), (0, 1), 2, 3, 5, "f32"),       # W = 96: no FFT of this width
+    (96, 40, (0, 1), (1,), 1, 16, 8, "bf16"),     # L < H/2
+    (24, 12, (0, 1), (0, 1), 2, 8, 8, "f32"),     # one latitude tile (H < 32)
+]
+
+
+@pytest.mark.parametrize("case", LAYERS, ids=[f"H{c[0]}L{c[1]}{c[7]}" for c in LAYERS])
+def test_layer_and_backward_at_widths_without_fft(case):
+    H, L, si, so, B, Ci, Co, dt = case
+    rng = np.random.default_rng(H + 7 * L)
+    x = round_to(O.inverse(syn.random_coefficients(rng, L, B, si, Ci, 1.0), H, H, si), dt)
+    K = round_to(syn.random_filters(rng, L, si, Ci, so, Co, 1.0 / Ci), dt)
+    gy = round_to(syn.complex_normal(rng, (B, len(so), Co, H, H)), dt)
+    plan = S.Plan(H, H, L, si, so, dt, longitude="matmul")
+    xd, Kd = to_device(x, dt), to_device(K, dt)
+    err = rel_l2(from_device(plan.conv(xd, Kd)), O.conv(x, K, L, si, so))
+    gx, gk = plan.conv_backward(xd, Kd, to_device(gy, dt))
+    rx, rk = O.conv_backward(x, K, gy, L, si, so)
+    ex, ek = rel_l2(from_device(gx), rx), rel_l2(from_device(gk), rk)
+    print(f"matmul layer {case}: conv {err:.2e}, grad_x {ex:.2e}, grad_filters {ek:.2e}")
+    assert err <= TOL[dt] and ex <= TOL[dt] and ek <= TOL[dt]
+    plan.close()
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_768_grid_forward_inverse_layer(dt):
+    """The largest grid of the paper's FFT-vs-DFT comparison (768 x 768,
+    bandlimit 384), whole outputs: forward, inverse and the layer."""
+    H, L, si, so, B, Ci, Co = 768, 384, (0, 1), (0, 1), 1, 4, 4
+    rng = np.random.default_rng(768)
+    a = syn.random_coefficients(rng, L, B, si, Ci, 1.0)
+    x = round_to(O.inverse(a, H, H, si), dt)
+    K = round_to(syn.random_filters(rng, L, si, Ci, so, Co, 1.0 / (2 * Ci)), dt)
+    plan = S.Plan(H, H, L, si, so, dt, longitude="matmul")
+    xd = to_device(x, dt)
+    coef = from_device(plan.forward(xd))
+    ref_a = O.forward(x, L, si)
+    e_f = rel_l2(coef, ref_a)
+    ac = round_to(a, dt)
+    e_i = rel_l2(from_device(plan.inverse(to_device(ac, dt))), O.inverse(ac, H, H, si))
+    e_c = rel_l2(from_device(plan.conv(xd, to_device(K, dt))),
+                 O.inverse(O.mix(ref_a, K, si, so), H, H, so))
+    print(f"768x768 {dt}: forward {e_f:.2e}, inverse {e_i:.2e}, conv {e_c:.2e}")
+    assert e_f <= TOL[dt] and e_i <= TOL[dt] and e_c <= TOL[dt]
     plan.close()
 
 
