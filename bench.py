@@ -103,7 +103,7 @@ def measured_traffic(kernel: str):
     return None if k is None else k.get("hbm_bytes_per_launch")
 
 
-STAGE_KERNELS = re.compile(r"(dft_fwd|dft_inv|lat_fwd|lat_inv|mix)(?:_dma)?_kernel")
+STAGE_KERNELS = re.compile(r"(dft_fwd|dft_inv|lat_fwd|lat_inv|mix)(?:_dma|_split)?_kernel")
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 COPY_BYTES = 1 << 30
 

@@ -17,6 +17,8 @@
 // transposed LDS read (ds_read_b64_tr_b16), two per fragment; B = table rows
 // j (K = l contiguous).  Each wave owns 64 x 64 outputs (2 x 2 MFMA
 // 32x32x16 tiles).
+#include <type_traits>
+
 #include "lds_dma.h"
 #include "mfma_tile.h"
 #include "swsft_internal.h"
@@ -147,39 +149,51 @@ __global__ void __launch_bounds__((FwdGeom<BK, RA, RB, ST>::NT))
   for (int s = 0; s < ST - 1; ++s)
     if (s < nk) issue(s, s);
   const int r32 = lane & 31, kh = lane >> 5;
-  for (int i = 0; i < nk; ++i) {
-    const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
-    wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
-    __builtin_amdgcn_s_barrier();  // step i landed for every wave; step i-1 is consumed
-    if (i + ST - 1 < nk) issue(i + ST - 1, (i + ST - 1) % ST);
-    const unsigned char* As = smem + (i % ST) * G::STAGE;
-    const unsigned char* Bs = As + RA * G::PITCH;
+  // The K loop for NL row blocks of 32 degrees that exist (l < L); blocks of
+  // the tile past the last degree (orders |m| near L leave most of a tile
+  // empty) issue neither operand reads nor MFMAs.  NL is wave-uniform.
+  auto k_loop = [&](auto nl) {
+    constexpr int NL = decltype(nl)::value;
+    for (int i = 0; i < nk; ++i) {
+      const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
+      wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
+      __builtin_amdgcn_s_barrier();  // step i landed for every wave; step i-1 is consumed
+      if (i + ST - 1 < nk) issue(i + ST - 1, (i + ST - 1) % ST);
+      if constexpr (NL > 0) {
+        const unsigned char* As = smem + (i % ST) * G::STAGE;
+        const unsigned char* Bs = As + RA * G::PITCH;
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int c = 2 * kk + kh;
-      v8bf a[2], b[2];
+        for (int kk = 0; kk < BK / 16; ++kk) {
+          const int c = 2 * kk + kh;
+          v8bf a[2], b[2];
 #pragma unroll
-      for (int ii = 0; ii < 2; ++ii) {
-        const int r = wm * 64 + ii * 32 + r32;
-        a[ii] = *reinterpret_cast<const v8bf*>(As + r * G::PITCH + swz<G::CPR>(r, c) * 16);
+          for (int ii = 0; ii < NL; ++ii) {
+            const int r = wm * 64 + ii * 32 + r32;
+            a[ii] = *reinterpret_cast<const v8bf*>(As + r * G::PITCH + swz<G::CPR>(r, c) * 16);
+          }
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj) {
+            const int r = wn * 64 + jj * 32 + r32;
+            b[jj] = *reinterpret_cast<const v8bf*>(Bs + r * G::PITCH + swz<G::CPR>(r, c) * 16);
+          }
+#pragma unroll
+          for (int ii = 0; ii < NL; ++ii)
+#pragma unroll
+            for (int jj = 0; jj < 2; ++jj)
+              acc[ii][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ii], b[jj], acc[ii][jj], 0, 0, 0);
+        }
       }
-#pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
-        const int r = wn * 64 + jj * 32 + r32;
-        b[jj] = *reinterpret_cast<const v8bf*>(Bs + r * G::PITCH + swz<G::CPR>(r, c) * 16);
-      }
-#pragma unroll
-      for (int ii = 0; ii < 2; ++ii)
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj)
-          acc[ii][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ii], b[jj], acc[ii][jj], 0, 0, 0);
     }
-  }
+  };
+  const int wrow = __builtin_amdgcn_readfirstlane(l_begin + wm * 64);
+  if (wrow + 32 < L) k_loop(std::integral_constant<int, 2>{});
+  else if (wrow < L) k_loop(std::integral_constant<int, 1>{});
+  else k_loop(std::integral_constant<int, 0>{});
   wait_vmcnt<0>();
   __syncthreads();
 
   // epilogue: rows l, columns n' = (b, c, re/im); 8 columns stay inside one
-  // b because 2C is a multiple of 8
+  // b because 2C is a multiple of 8 (rows past L are not stored)
   __bf16* cs = reinterpret_cast<__bf16*>(smem);
   acc_to_lds(acc, cs, G::LDC, wm, wn, lane);
   __syncthreads();
