@@ -305,7 +305,7 @@ struct MixGeomS {
   static_assert(ST >= 2 && (ST - 2) * PER_WAVE < 64, "stages");
 };
 
-template <int WM, int WN, int ST>
+template <int WM, int WN, int ST, bool REG>
 __global__ void __launch_bounds__((MixGeomS<WM, WN, ST>::NT))
     mix_split_kernel(const __bf16* __restrict__ coef, const __bf16* __restrict__ K,
                      __bf16* __restrict__ out, int L, int B, int Cin, int Cout, int Sin, int Sout,
@@ -374,6 +374,39 @@ __global__ void __launch_bounds__((MixGeomS<WM, WN, ST>::NT))
 #pragma unroll
     for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + koff, base + u * 1024);
   };
+  // Register-staged copies (REG): thread t moves the 16-byte chunks
+  // t + NT u of the stage [A rows; B rows] (8 consecutive threads one
+  // 128-byte row segment) through registers; global reads of step i + 2 are
+  // in flight while step i is multiplied and step i + 1 is written to LDS.
+  constexpr int NLD = REG ? (RA + RB) * G::CPR / G::NT : 1;
+  static_assert(!REG || ((RA + RB) * G::CPR) % G::NT == 0, "register staging");
+  const __bf16* rsrc[NLD];
+  int rdst[NLD];
+  v4u_t stg[NLD];
+  if constexpr (REG) {
+#pragma unroll
+    for (int u = 0; u < NLD; ++u) {
+      const int id = tid + G::NT * u, tr = id / G::CPR, c = id % G::CPR;
+      if (tr < RA) {
+        const int row = row0 + tr < Mrows ? row0 + tr : Mrows - 1;
+        rsrc[u] = A0 + (size_t)row * Kp + c * 8;
+      } else {
+        const int q = q0 + tr - RA < Nc ? q0 + tr - RA : Nc - 1;
+        rsrc[u] = K0 + (size_t)q * Kp + c * 8;
+      }
+      rdst[u] = tr * G::PITCH + swz<G::CPR>(tr, c) * 16;
+    }
+  }
+  auto rload = [&](int i) {
+    const int koff = live[i] * BK;
+#pragma unroll
+    for (int u = 0; u < NLD; ++u) stg[u] = *reinterpret_cast<const v4u_t*>(rsrc[u] + koff);
+  };
+  auto rstore = [&](int stage) {
+#pragma unroll
+    for (int u = 0; u < NLD; ++u)
+      *reinterpret_cast<v4u_t*>(smem + stage * G::STAGE + rdst[u]) = stg[u];
+  };
 
   v16f acc_re[TM][TN], acc_im[TM][TN];
 #pragma unroll
@@ -388,9 +421,19 @@ __global__ void __launch_bounds__((MixGeomS<WM, WN, ST>::NT))
 #pragma unroll
   for (int i = 0; i < TM; ++i) blk_live[i] = row0 + (wm * TM + i) * 32 < Mrows;
 
+  if constexpr (!REG) {
 #pragma unroll
-  for (int s = 0; s < ST - 1; ++s)
-    if (s < nk) issue(s, s);
+    for (int s = 0; s < ST - 1; ++s)
+      if (s < nk) issue(s, s);
+  } else {
+    static_assert(!REG || ST == 2, "register staging double-buffers");
+    if (nk > 0) {
+      rload(0);
+      rstore(0);
+    }
+    if (nk > 1) rload(1);
+    __syncthreads();
+  }
 
   const int r32 = lane & 31, kh = lane >> 5;
   // The K loop for NL live row blocks (0: the wave only copies and waits at
@@ -399,10 +442,12 @@ __global__ void __launch_bounds__((MixGeomS<WM, WN, ST>::NT))
   auto k_loop = [&](auto nl) {
     constexpr int NL = decltype(nl)::value;
     for (int i = 0; i < nk; ++i) {
-      const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
-      wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
-      __builtin_amdgcn_s_barrier();  // every wave's copies of step i landed; step i-1 is consumed
-      if (i + ST - 1 < nk) issue(i + ST - 1, (i + ST - 1) % ST);
+      if constexpr (!REG) {
+        const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
+        wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
+        __builtin_amdgcn_s_barrier();  // every wave's copies of step i landed; step i-1 is consumed
+        if (i + ST - 1 < nk) issue(i + ST - 1, (i + ST - 1) % ST);
+      }
       if constexpr (NL > 0) {
         const unsigned char* As = smem + (i % ST) * G::STAGE;
         const unsigned char* Bs = As + RA * G::PITCH;
@@ -448,6 +493,11 @@ __global__ void __launch_bounds__((MixGeomS<WM, WN, ST>::NT))
           }
         }
       }
+      if constexpr (REG) {
+        if (i + 1 < nk) rstore((i + 1) % 2);  // step i + 1 (its stage was consumed in step i - 1)
+        __syncthreads();                       // step i + 1 visible; step i consumed
+        if (i + 2 < nk) rload(i + 2);
+      }
     }
   };
   static_assert(TM == 2, "live-block dispatch");
@@ -484,7 +534,7 @@ __global__ void __launch_bounds__((MixGeomS<WM, WN, ST>::NT))
   }
 }
 
-template <int WM, int WN, int ST>
+template <int WM, int WN, int ST, bool REG>
 hipError_t launch_split(const Plan& p, int B, int Cin, int Cout, const void* coef, const void* K,
                         void* out, hipStream_t st) {
   using G = MixGeomS<WM, WN, ST>;
@@ -495,9 +545,9 @@ hipError_t launch_split(const Plan& p, int B, int Cin, int Cout, const void* coe
   for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + G::RA - 1) / G::RA;
   const int Nc = p.n_out * Cout;
   const long long blocks = tiles * ((Nc + G::RB - 1) / G::RB);
-  const hipError_t e = ensure_dynamic_lds((const void*)mix_split_kernel<WM, WN, ST>, G::SMEM);
+  const hipError_t e = ensure_dynamic_lds((const void*)mix_split_kernel<WM, WN, ST, REG>, G::SMEM);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((mix_split_kernel<WM, WN, ST>), dim3(xcd_grid(blocks)), dim3(G::NT), G::SMEM,
+  hipLaunchKernelGGL((mix_split_kernel<WM, WN, ST, REG>), dim3(xcd_grid(blocks)), dim3(G::NT), G::SMEM,
                      st, (const __bf16*)coef, (const __bf16*)K, (__bf16*)out, p.L, B, Cin, Cout,
                      p.n_in, p.n_out, si, so);
   return hipGetLastError();
@@ -754,6 +804,11 @@ hipError_t launch_geom_f32(const Plan& p, int B, int Cin, int Cout, const void* 
 #ifndef SWSFT_MIX_SPLIT_GEOM
 #define SWSFT_MIX_SPLIT_GEOM 2, 2, 2
 #endif
+// 1: the split kernel stages its operands through registers instead of
+// direct global -> LDS copies
+#ifndef SWSFT_MIX_SPLIT_REG
+#define SWSFT_MIX_SPLIT_REG 0
+#endif
 // float: WM, WN, ST, TN of MixGeomF
 #ifndef SWSFT_MIX_DMA_F32
 #define SWSFT_MIX_DMA_F32 2, 2, 4, 1
@@ -795,7 +850,8 @@ hipError_t launch_mix_dma(const Plan& p, int B, int Cin, int Cout, const void* c
   if (p.dtype == SWSFT_F32) return launch_geom_f32<SWSFT_MIX_DMA_F32>(p, B, Cin, Cout, coef, K, out, st);
 #if SWSFT_MIX_SPLIT
   if ((2 * Cin) % 64 == 0)
-    return launch_split<SWSFT_MIX_SPLIT_GEOM>(p, B, Cin, Cout, coef, K, out, st);
+    return launch_split<SWSFT_MIX_SPLIT_GEOM, SWSFT_MIX_SPLIT_REG != 0>(p, B, Cin, Cout, coef, K, out,
+                                                                        st);
 #endif
   if ((2 * Cin) % SWSFT_MIX_DMA_BK == 0)
     return launch_geom<SWSFT_MIX_DMA_BK, SWSFT_MIX_DMA_RA, SWSFT_MIX_DMA_RB, SWSFT_MIX_DMA_STAGES>(
