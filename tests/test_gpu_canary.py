@@ -116,6 +116,12 @@ def _all_calls(plan, B, Ci, Co, seed):
                                        st), "spin_sph_conv_forward_train")
     _run(Lib.spin_sph_conv_forward_train, [x, K, y, cx, w])
     cx.before = cx.raw[GUARD:GUARD + cx.n].clone()          # an input from now on
+    # the layer on the library's static workspace, where it fits (128 MiB)
+    if Lib.swsft_workspace_bytes(h, S.OP_CONV, B, Ci, Co) <= (128 << 20):
+        y = Guarded(sz["y"], "y")
+        ok(Lib.spin_sph_conv_forward_noalloc(h, B, Ci, Co, x.ptr, K.ptr, y.ptr, st),
+           "spin_sph_conv_forward_noalloc")
+        _run(Lib.spin_sph_conv_forward_noalloc, [x, K, y])
     # the backward pass: from x, and from the saved coefficients
     gy = Guarded(sz["y"], "grad_y", gen)
     for use_saved in (False, True):
