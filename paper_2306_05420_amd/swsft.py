@@ -236,7 +236,7 @@ class Plan:
         sh = _stream_handle(stream)
         ws = self.workspace(OP_FORWARD, B, C, 1, sh)
         _check(lib().swsft_forward(self._h, B, C, xr.data_ptr(), cr.data_ptr(), ws.data_ptr(),
-                                   ws.numel(), _stream_handle(stream)), "swsft_forward")
+                                   ws.numel(), sh), "swsft_forward")
         return coef
 
     def inverse(self, coef: torch.Tensor, y: torch.Tensor = None, stream=None) -> torch.Tensor:
@@ -251,7 +251,7 @@ class Plan:
         sh = _stream_handle(stream)
         ws = self.workspace(OP_INVERSE, B, 1, C, sh)
         _check(lib().swsft_inverse(self._h, B, C, cr.data_ptr(), yr.data_ptr(), ws.data_ptr(),
-                                   ws.numel(), _stream_handle(stream)), "swsft_inverse")
+                                   ws.numel(), sh), "swsft_inverse")
         return y
 
     def conv(self, x: torch.Tensor, filters: torch.Tensor, y: torch.Tensor = None,
@@ -275,7 +275,7 @@ class Plan:
         if coef_x is None or coef_x is False:
             _check(lib().spin_sph_conv_forward(self._h, B, Cin, Cout, xr.data_ptr(),
                                                kr.data_ptr(), yr.data_ptr(), ws.data_ptr(),
-                                               ws.numel(), _stream_handle(stream)),
+                                               ws.numel(), sh),
                    "spin_sph_conv_forward")
             return y
         if coef_x is True:
@@ -285,7 +285,7 @@ class Plan:
         _check(lib().spin_sph_conv_forward_train(self._h, B, Cin, Cout, xr.data_ptr(),
                                                  kr.data_ptr(), yr.data_ptr(), cr.data_ptr(),
                                                  ws.data_ptr(), ws.numel(),
-                                                 _stream_handle(stream)),
+                                                 sh),
                "spin_sph_conv_forward_train")
         return y, coef_x
 
@@ -334,7 +334,7 @@ class Plan:
         ws = self.workspace(OP_CONV_BACKWARD, B, Cin, Cout, sh)
         _check(lib().spin_sph_conv_backward(self._h, B, Cin, Cout, xr.data_ptr(), cx_ptr,
                                             kr.data_ptr(), gr.data_ptr(), gx_ptr, gk_ptr,
-                                            ws.data_ptr(), ws.numel(), _stream_handle(stream)),
+                                            ws.data_ptr(), ws.numel(), sh),
                "spin_sph_conv_backward")
         return grad_x, grad_filters
 
@@ -406,7 +406,7 @@ class Plan:
             None if beta is None else beta.data_ptr(), float(eps),
             None if var is None else var.data_ptr(), var_out.data_ptr(),
             None if sk is None else sk.data_ptr(), orr.data_ptr(), ws.data_ptr(), ws.numel(),
-            _stream_handle(stream)), "spin_sph_spectral_batch_norm")
+            sh), "spin_sph_spectral_batch_norm")
         return out, var_out
 
     # -- tables and timing -------------------------------------------------
@@ -512,6 +512,6 @@ class ResidualBlock:
         _check(lib().spin_sph_residual_block_forward(self.p_in._h, po._h, B, C, xr.data_ptr(),
                                                      ctypes.byref(prm), yr.data_ptr(),
                                                      ws.data_ptr(), ws.numel(),
-                                                     _stream_handle(stream)),
+                                                     sh),
                "spin_sph_residual_block_forward")
         return (y, v1, v2) if variances else y
