@@ -65,6 +65,12 @@ def stage_work(w):
         k = Ci * sum(1 for s in w.spins_in if abs(s) <= l)
         n = Co * sum(1 for t in w.spins_out if abs(t) <= l)
         mix += 8 * B * (2 * l + 1) * k * n
+    # the synthesis runs over batch ranges whose spectrum fits 128 MiB of the
+    # Infinity Cache (one range when the whole batch fits); each range's
+    # launch reads the whole table
+    per_item = So * M * Co * H * 2 * e
+    bc = max(1, min(B, (128 << 20) // per_item)) if (So * 2 * Co * e) % 16 == 0 else B
+    ranges = -(-B // bc)
     return {
         # small grids: whole transforms per map (the synthesis also mixes when
         # the layer runs without a separate mixing stage)
@@ -74,7 +80,7 @@ def stage_work(w):
         "dft_fwd": {"flops": 0, "bytes": x_b + X_b},
         "lat_fwd": {"flops": lat_f, "bytes": X_b + tab_i + a_b},
         "mix": {"flops": mix, "bytes": a_b + K_b + a2_b},
-        "lat_inv": {"flops": lat_i, "bytes": a2_b + tab_o + Y_b},
+        "lat_inv": {"flops": lat_i, "bytes": a2_b + ranges * tab_o + Y_b},
         "dft_inv": {"flops": 0, "bytes": Y_b + y_b},
     }
 
