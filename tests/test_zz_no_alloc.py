@@ -72,3 +72,51 @@ def test_noalloc_refuses_layers_above_the_static_workspace():
     assert "static workspace" in Lib.swsft_last_error().decode()
     torch.cuda.synchronize()
     plan.close()
+
+
+@pytest.mark.parametrize("name", ["mol", "wx128"])
+def test_noalloc_graph_replays_match_eager(name):
+    """The entry point captured in a HIP graph (the callers it is for): every
+    replay reproduces the eager call bit for bit, with an eager call of the
+    same entry point on another input between replays (it rewrites the
+    static workspace the replay then reuses)."""
+    w = syn.workload(name)
+    Lib = S.lib()
+    plan = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_out, w.dtype)
+    x, K = _inputs(plan, w, w.B, 3)
+    x2, _ = _inputs(plan, w, w.B, 4)
+    shape = (w.B, len(w.spins_out), w.C_out, w.H, w.W)
+    y, y2 = plan.empty(*shape), plan.empty(*shape)
+
+    def call(xx, yy):
+        st = torch.cuda.current_stream().cuda_stream
+        xr, kr, yr = (plan.real_view(t) for t in (xx, K, yy))
+        status = Lib.spin_sph_conv_forward_noalloc(plan._h, w.B, w.C_in, w.C_out, xr.data_ptr(),
+                                                   kr.data_ptr(), yr.data_ptr(), st)
+        assert status == S.OK, Lib.swsft_last_error().decode()
+
+    print(f"noalloc graph {name}", flush=True)
+    call(x, y)
+    call(x2, y2)
+    torch.cuda.synchronize()
+    ref, ref2 = y.clone(), y2.clone()
+    assert torch.equal(ref, plan.conv(x, K)) and torch.equal(ref2, plan.conv(x2, K))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call(x, y)
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call(x, y)
+    for rep in range(4):
+        y.zero_()
+        y2.zero_()
+        call(x2, y2)                         # eager, same static workspace
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, ref), (name, rep)
+        assert torch.equal(y2, ref2), (name, rep)
+    del g
+    plan.close()
