@@ -119,6 +119,25 @@ __device__ __forceinline__ void store_cplx(__bf16* p, size_t i, float2 v) {
   reinterpret_cast<uint32_t*>(p)[i] = pack_bf16x2(v.x, v.y);
 }
 
+typedef unsigned v4u_t __attribute__((ext_vector_type(4)));
+
+// LDS image of one pass's output rows of the inverse (W >= 64): WPC 32-bit
+// words per complex sample, rows padded by 64 (bf16) or 128 (float) bytes so
+// the rows one wave writes start in different banks.  The rows then leave as
+// 16-byte vectors, whole 128-byte lines, where storing each thread's samples
+// directly writes 64-byte pieces (W1 consecutive samples of a row).
+template <typename T, int W>
+struct OutStage {
+  static constexpr bool ON = W >= 64;
+  static constexpr int WPC = sizeof(T) == 2 ? 1 : 2;
+  static constexpr int PITCH = W * WPC + 16 * WPC;  // words per row
+  static constexpr int VPR = W * WPC / 4;           // 16-byte vectors per row
+  static __device__ __forceinline__ void put(uint32_t* row, int col, float2 v) {
+    if constexpr (WPC == 1) row[col] = pack_bf16x2(v.x, v.y);
+    else *reinterpret_cast<float2*>(row + 2 * col) = v;
+  }
+};
+
 // The NP values of rows NP*rr .. NP*rr+NP-1 at one stage position.
 template <typename T, int NP>
 struct StageVec;
@@ -316,7 +335,7 @@ __global__ void __launch_bounds__((DftGeom<W1, W2>::NT))
     dft_inv_kernel(const Tin* __restrict__ Y, Tout* __restrict__ y,
                    const float2* __restrict__ tw, int S, int C, int NB, int NBC, int L) {
   using G = DftGeom<W1, W2>;
-  constexpr int W = G::W, H = W, NP = G::NP, JB = G::JB, NT = G::NT;
+  constexpr int W = G::W, H = W, NP = G::NP, JB = G::JB, NT = G::NT, RPP_ = G::RPP;
   constexpr int SP = stage_pitch<Tin, JB>();
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x, t = tid % W1, rr = tid / W1;
@@ -368,6 +387,37 @@ __global__ void __launch_bounds__((DftGeom<W1, W2>::NT))
 #pragma unroll
     for (int k2 = 0; k2 < W2; ++k2) exr[k2 * (W1 + 1) + t] = v[p][k2];
     __syncthreads();
+    if constexpr (OutStage<Tout, W>::ON) {
+      // the pass's RPP rows are staged in LDS (over the exchange buffer, once
+      // every lane has read it) and leave as 16-byte vectors, whole rows
+      using O = OutStage<Tout, W>;
+      float2 uu[W2 / W1][W1];
+#pragma unroll
+      for (int i = 0; i < W2 / W1; ++i) {
+        const int k2 = t + W1 * i;
+#pragma unroll
+        for (int tp = 0; tp < W1; ++tp) uu[i][tp] = exr[k2 * (W1 + 1) + tp];
+        fft_reg<W1, +1>(uu[i]);
+      }
+      __syncthreads();  // every lane has read the exchange buffer
+      uint32_t* os = reinterpret_cast<uint32_t*>(smem);
+#pragma unroll
+      for (int i = 0; i < W2 / W1; ++i)
+#pragma unroll
+        for (int k1 = 0; k1 < W1; ++k1)
+          O::put(os + rr * O::PITCH, t + W1 * i + W2 * k1, uu[i][k1]);
+      __syncthreads();
+      uint32_t* yw = reinterpret_cast<uint32_t*>(y);
+      for (int idx = tid; idx < RPP_ * O::VPR; idx += NT) {
+        const int row = idx / O::VPR, vc = idx % O::VPR;
+        const v4u_t val = *reinterpret_cast<const v4u_t*>(os + row * O::PITCH + 4 * vc);
+        v4u_t* dst = reinterpret_cast<v4u_t*>(
+            yw + ((size_t)mb.map * H + mb.j0 + NP * row + p) * W * O::WPC + 4 * vc);
+        if constexpr (STREAM) __builtin_nontemporal_store(val, dst);
+        else *dst = val;
+      }
+      continue;
+    }
 #pragma unroll
     for (int i = 0; i < W2 / W1; ++i) {
       const int k2 = t + W1 * i;
@@ -423,7 +473,9 @@ hipError_t launch_inv_shape(const Plan& p, int S, int B, int C, const void* Y, v
                             hipStream_t st) {
   using G = DftGeom<W1, W2>;
   if (p.H != G::W || p.JT != G::JB) return hipErrorInvalidValue;
-  const size_t lds = dft_lds_bytes<Tin, G>(p.M);
+  size_t lds = dft_lds_bytes<Tin, G>(p.M);
+  using O = OutStage<Tout, G::W>;  // the output rows of a pass, staged over the same allocation
+  if (O::ON && (size_t)G::RPP * O::PITCH * 4 > lds) lds = (size_t)G::RPP * O::PITCH * 4;
   const size_t bytes = xy_elems(p, S, B, C) * sizeof(Tin) + (size_t)B * S * C * p.H * p.W * 2 * sizeof(Tout);
   auto kern = streams_past_caches<W1 * W2>(bytes) ? dft_inv_kernel<Tin, Tout, W1, W2, kHasStream<W1 * W2>>
                                                   : dft_inv_kernel<Tin, Tout, W1, W2, false>;
