@@ -374,6 +374,7 @@ def main(argv=None):
         "stages": r["stages"],
         "roofline": r["roofline"],
         "transforms": r["transforms"],
+        "plan_ms": r["plan_ms"],
     }
     for k in ("backward", "graph"):
         if k in r:
@@ -404,9 +405,35 @@ def measured_peaks() -> dict:
     c = torch.empty((n, n), device="cuda", dtype=torch.bfloat16)
     t_mm = _time_calls(lambda: torch.matmul(a, b, out=c), 10, 3)
     del a, b, c
-    return {"copy_GB/s": round(2 * (1 << 30) / t_copy / 1e9, 1),
-            "bf16_gemm_TFLOP/s": round(2.0 * n ** 3 / t_mm / 1e12, 1),
-            "gemm": f"torch.matmul bf16 {n}x{n}x{n}"}
+    out = {"copy_GB/s": round(2 * (1 << 30) / t_copy / 1e9, 1),
+           "bf16_gemm_TFLOP/s": round(2.0 * n ** 3 / t_mm / 1e12, 1),
+           "gemm": f"torch.matmul bf16 {n}x{n}x{n}"}
+    out.update(mfma_probe_rates())
+    return out
+
+
+def mfma_probe_rates() -> dict:
+    """The library's register-only MFMA probe (swsft_probe_mfma): 2,048 waves
+    (two per SIMD) of four independent MFMA chains, timed with events on the
+    stream it runs on; TFLOP/s for bf16 32x32x16 with random and with
+    constant operands, and for f32 32x32x2 with random operands."""
+    import torch
+
+    from paper_2306_05420_amd import swsft as S
+
+    n_waves = 2048
+    buf = torch.empty(64 * n_waves, dtype=torch.float32, device="cuda")
+    rates = {}
+    for key, dtype, rnd, iters in (("bf16_mfma_random_TFLOP/s", "bf16", True, 20000),
+                                   ("bf16_mfma_constant_TFLOP/s", "bf16", False, 20000),
+                                   ("f32_mfma_random_TFLOP/s", "f32", True, 10000)):
+        flops = S.probe_mfma(dtype, rnd, iters, n_waves, buf)  # warm-up
+        t = _time_calls(lambda: S.probe_mfma(dtype, rnd, iters, n_waves, buf), 5, 1)
+        if not bool(torch.isfinite(buf).all()):
+            raise RuntimeError("MFMA probe produced non-finite checksums")
+        rates[key] = round(flops / t / 1e12, 1)
+    rates["mfma_probe"] = f"{n_waves} waves x 4 register-only MFMA chains (swsft_probe_mfma)"
+    return rates
 
 
 def _time_calls(fn, steps: int, warmup: int):
@@ -458,7 +485,12 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
     from paper_2306_05420_amd import synthetic as syn
 
     w = syn.workload(name)
+    # plan creation (device tables and twiddles), outside every timed loop
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
     plan = S.Plan(w.H, w.W, w.L, w.spins_in, w.spins_out, w.dtype)
+    torch.cuda.synchronize()
+    plan_ms = (time.perf_counter() - t0) * 1e3
 
     # inputs: band-limited fields synthesised on the GPU from seeded
     # CN(0,1)/(l+1) coefficients by the library's own inverse transform
@@ -565,7 +597,7 @@ def measure(name: str, steps: int, warmup: int, dev, copy_calibration: bool = Fa
                              "TFLOP/s": round(fl / t / 1e12, 2)}
     r = {"w": w, "value": 1.0 / t_layer, "ms_per_step": t_layer * 1e3, "latency_us": latency,
          "tflops": useful / t_layer / 1e12, "useful": useful, "stages": stages,
-         "roofline": roof, "transforms": transforms}
+         "roofline": roof, "transforms": transforms, "plan_ms": round(plan_ms, 2)}
     if not extras:
         plan.close()
         return r

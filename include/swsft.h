@@ -405,6 +405,24 @@ const char* swsft_stage_name(int stage);
 swsft_status swsft_plan_table(swsft_plan p, int which, int spin_index, void* host_dst,
                               size_t bytes);
 
+/*
+ * Measurement helper, not part of the transform: enqueue on `stream` one
+ * kernel in which n_waves waves (a multiple of 4, 4 <= n_waves <= 2^20) each
+ * run `iters` (1 <= iters <= 2^24) rounds of four independent MFMAs with
+ * both operands held in registers and no memory traffic:
+ * v_mfma_f32_32x32x16_bf16 for dtype SWSFT_BF16, v_mfma_f32_32x32x2f32 for
+ * SWSFT_F32.  random_operands != 0 fills the operand registers with values
+ * of random sign and mantissa in [0.5, 2), 0 with ones (the chip's clock
+ * depends on the switching activity, so the two rates differ).  `out`
+ * (device, 64 n_waves floats, caller-owned) receives one checksum per lane.
+ * *flops_out (host, may be NULL) receives the MFMA flops the kernel issues:
+ * n_waves iters (4 x 2 x 32 x 32 x 16) for bf16, (4 x 2 x 32 x 32 x 2) for
+ * f32.  The caller times the kernel on its stream (e.g. with events) to get
+ * the sustained rate against which the contraction kernels are quoted.
+ */
+swsft_status swsft_probe_mfma(int dtype, int random_operands, long long iters, int n_waves,
+                              float* out, double* flops_out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1035,6 +1035,22 @@ int swsft_stage_times(swsft_plan p, double* ms, long long* launches, int n) {
   return swsft::kNumStages;
 }
 
+swsft_status swsft_probe_mfma(int dtype, int random_operands, long long iters, int n_waves,
+                              float* out, double* flops_out, void* stream) {
+  g_last_error[0] = 0;
+  if (dtype != SWSFT_F32 && dtype != SWSFT_BF16) return fail(SWSFT_E_INVALID, "dtype %d", dtype);
+  if (out == nullptr) return fail(SWSFT_E_INVALID, "out is NULL");
+  if (iters < 1 || iters > (1ll << 24)) return fail(SWSFT_E_INVALID, "iters = %lld", iters);
+  if (n_waves < 4 || n_waves > (1 << 20) || n_waves % 4 != 0)
+    return fail(SWSFT_E_INVALID, "n_waves = %d (a multiple of 4 in [4, 2^20])", n_waves);
+  if (flops_out != nullptr)
+    *flops_out = swsft::mfma_probe_flops_per_wave_round(dtype) * (double)n_waves * (double)iters;
+  const hipError_t e =
+      swsft::launch_mfma_probe(dtype, random_operands, iters, n_waves, out, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "mfma probe launch");
+  return SWSFT_OK;
+}
+
 swsft_status swsft_plan_table(swsft_plan p, int which, int spin_index, void* host_dst,
                               size_t bytes) {
   g_last_error[0] = 0;

@@ -196,5 +196,11 @@ int phase_collapse_max_channels(int n_spins);
 hipError_t launch_phase_collapse(const Plan& p, int B, int C, const void* x,
                                  const float2* W1, const float2* W2, const float2* bias,
                                  void* y, hipStream_t st);
+// Measurement helper (probe.hip): n_waves waves (a multiple of 4) each run
+// `iters` rounds of four register-only MFMAs of the dtype's shape; out holds
+// 64 n_waves floats.
+double mfma_probe_flops_per_wave_round(int dtype);
+hipError_t launch_mfma_probe(int dtype, int random, long long iters, int n_waves, float* out,
+                             hipStream_t st);
 
 }  // namespace swsft

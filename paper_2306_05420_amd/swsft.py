@@ -88,6 +88,8 @@ def lib() -> ctypes.CDLL:
                                   ctypes.POINTER(ctypes.c_longlong), i]),
         "swsft_stage_name": (ctypes.c_char_p, [i]),
         "swsft_plan_table": (i, [vp, i, i, vp, sz]),
+        "swsft_probe_mfma": (i, [i, i, ctypes.c_longlong, i, vp, ctypes.POINTER(ctypes.c_double),
+                                 vp]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(L, name)
@@ -119,6 +121,22 @@ def _check(status: int, what: str):
 def _stream_handle(stream) -> int:
     s = stream if stream is not None else torch.cuda.current_stream()
     return s.cuda_stream
+
+
+def probe_mfma(dtype: str, random_operands: bool, iters: int, n_waves: int, out: torch.Tensor,
+               stream=None) -> float:
+    """Enqueue the register-only MFMA probe (swsft_probe_mfma): n_waves waves
+    each run `iters` rounds of four MFMAs of the dtype's shape; `out` is a
+    float32 GPU tensor of 64 n_waves checksums.  Returns the flops the kernel
+    issues; the caller times it on its stream."""
+    _need(out, torch.float32, (64 * n_waves,), "out")
+    flops = ctypes.c_double(0.0)
+    if dtype not in ("f32", "bf16"):
+        raise ValueError("dtype must be 'f32' or 'bf16'")
+    _check(lib().swsft_probe_mfma(F32 if dtype == "f32" else BF16, int(bool(random_operands)),
+                                  int(iters), int(n_waves), out.data_ptr(), ctypes.byref(flops),
+                                  _stream_handle(stream)), "swsft_probe_mfma")
+    return flops.value
 
 
 class Plan:

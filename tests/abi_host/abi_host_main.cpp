@@ -227,6 +227,18 @@ int main() {
   block(SWSFT_F32);
   block(SWSFT_BF16);
   timing_from_threads();
+  {
+    // the MFMA probe writes exactly 64 floats per wave; bad arguments are refused
+    Buf out((size_t)8 * 64 * sizeof(float));
+    double flops = 0.0;
+    EXPECT(swsft_probe_mfma(SWSFT_BF16, 1, 10, 8, (float*)out.p, &flops, nullptr) == SWSFT_OK);
+    EXPECT(flops == 8.0 * 10 * 4 * 2 * 32 * 32 * 16);
+    EXPECT(swsft_probe_mfma(SWSFT_F32, 0, 10, 8, (float*)out.p, nullptr, nullptr) == SWSFT_OK);
+    EXPECT(swsft_probe_mfma(SWSFT_BF16, 1, 10, 6, (float*)out.p, nullptr, nullptr) == SWSFT_E_INVALID);
+    EXPECT(swsft_probe_mfma(SWSFT_BF16, 1, 0, 8, (float*)out.p, nullptr, nullptr) == SWSFT_E_INVALID);
+    EXPECT(swsft_probe_mfma(7, 1, 10, 8, (float*)out.p, nullptr, nullptr) == SWSFT_E_INVALID);
+    EXPECT(swsft_probe_mfma(SWSFT_BF16, 1, 10, 8, nullptr, nullptr, nullptr) == SWSFT_E_INVALID);
+  }
   std::printf("%lld stub launches\n", stub_launch_count());
   if (g_fail) {
     std::printf("%d expectation(s) failed\n", g_fail);

@@ -322,6 +322,14 @@ hipError_t launch_delta_theta_fwd(const Plan& p, int B, int C, const void* X, vo
   stub::wr("delta_theta_fwd CS", CS, delta_elems(p, p.n_in, B, C) * p.elem);
   return hipSuccess;
 }
+double mfma_probe_flops_per_wave_round(int dtype) {
+  return dtype == SWSFT_BF16 ? 4.0 * 2 * 32 * 32 * 16 : 4.0 * 2 * 32 * 32 * 2;
+}
+hipError_t launch_mfma_probe(int, int, long long, int n_waves, float* out, hipStream_t) {
+  stub::count();
+  stub::wr("mfma_probe out", out, (size_t)n_waves * 64 * sizeof(float));
+  return hipSuccess;
+}
 hipError_t launch_delta_theta_inv(const Plan& p, int B, int C, const void* G, void* Y,
                                   hipStream_t) {
   stub::count();

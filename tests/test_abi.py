@@ -16,7 +16,7 @@ def L():
 
 def test_exports_every_declared_function(L):
     names = S.header_functions()
-    assert len(names) == 21
+    assert len(names) == 22
     for n in names:
         assert hasattr(L, n), n
 
@@ -95,3 +95,16 @@ def test_status_strings_and_stage_names(L):
     assert L.swsft_status_string(99).decode() == "unknown swsft status"
     assert [L.swsft_stage_name(i).decode() for i in range(len(S.STAGES))] == list(S.STAGES)
     assert L.swsft_stage_name(len(S.STAGES)).decode() == ""
+
+
+def test_mfma_probe_validation(L):
+    # refused on the host before any launch: dtype, iteration and wave counts, NULL out
+    out = ctypes.c_void_p(1 << 20)
+    f = ctypes.c_double(0.0)
+    assert L.swsft_probe_mfma(7, 1, 10, 8, out, ctypes.byref(f), None) == S.E_INVALID
+    assert L.swsft_probe_mfma(S.BF16, 1, 0, 8, out, ctypes.byref(f), None) == S.E_INVALID
+    assert L.swsft_probe_mfma(S.BF16, 1, 1 << 25, 8, out, ctypes.byref(f), None) == S.E_INVALID
+    assert L.swsft_probe_mfma(S.BF16, 1, 10, 6, out, ctypes.byref(f), None) == S.E_INVALID
+    assert L.swsft_probe_mfma(S.F32, 1, 10, 0, out, ctypes.byref(f), None) == S.E_INVALID
+    assert L.swsft_probe_mfma(S.BF16, 1, 10, 8, None, ctypes.byref(f), None) == S.E_INVALID
+    assert L.swsft_last_error().decode() != ""
