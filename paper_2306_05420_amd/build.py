@@ -23,7 +23,7 @@ INCLUDE = os.path.join(os.path.dirname(PKG), "include")
 
 SOURCES = ["tables.hip", "delta.hip", "dft.hip", "dft_mm.hip", "gemm.hip", "mix_dma.hip", "lat_dma.hip",
            "phase_collapse.hip", "batch_norm.hip", "backward.hip", "small.hip", "noalloc.hip",
-           "probe.hip", "swsft_api.cpp"]
+           "probe.hip", "fused32.hip", "swsft_api.cpp"]
 ARCH = "gfx950"
 
 

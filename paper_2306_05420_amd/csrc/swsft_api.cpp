@@ -438,6 +438,9 @@ swsft_status forward_stages(Plan& p, int B, int C, const void* x, void* X, void*
   if (swsft::small_path(p, 1))
     return run_stage(p, swsft::kStageSmallFwd, st, "small_fwd",
                      [&] { return swsft::launch_small_fwd(p, B, C, x, coef, st); });
+  if (swsft::fused32_ok(p, C))
+    return run_stage(p, swsft::kStageSmallFwd, st, "small_fwd",
+                     [&] { return swsft::launch_fused32_fwd(p, B, C, x, coef, st); });
   SWSFT_TRY(run_stage(p, swsft::kStageDftFwd, st, "dft_fwd",
                       [&] { return swsft::launch_dft_fwd(p, p.n_in, B, C, x, X, st); }));
   if (!swsft::is_delta(p))
@@ -465,6 +468,9 @@ constexpr size_t kCacheResidentBytes = size_t(128) << 20;
 // the cache instead of HBM.
 swsft_status synthesis_stages(Plan& tp, const Plan& p, int B, int C, const void* coef, void* Y,
                               void* y, hipStream_t st) {
+  if (swsft::fused32_ok(p, C))  // the spectrum stays in LDS: one launch for the batch
+    return run_stage(tp, swsft::kStageSmallInv, st, "small_inv",
+                     [&] { return swsft::launch_fused32_inv(p, B, C, coef, y, st); });
   {
     const size_t per_item = swsft::xy_elems(p, p.n_out, 1, C) * p.elem;
     int bc = per_item == 0 ? B : (int)(kCacheResidentBytes / per_item);
@@ -744,11 +750,17 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
   syn.n_out = p->n_in;
   for (int i = 0; i < swsft::kMaxSpins; ++i) syn.spins_out[i] = p->spins_in[i];
 
-  SWSFT_TRY(run_stage(*p, swsft::kStageDftFwd, st, "dft_fwd", [&] {
-    return swsft::launch_dft_fwd(*p, p->n_out, B, C_out, grad_y, XY, st);
-  }));
-  SWSFT_TRY(run_stage(*p, swsft::kStageLatFwd, st, "lat_fwd",
-                      [&] { return swsft::launch_lat_fwd(ana, B, C_out, XY, g_out, st); }));
+  if (swsft::fused32_ok(ana, C_out)) {
+    SWSFT_TRY(run_stage(*p, swsft::kStageSmallFwd, st, "small_fwd", [&] {
+      return swsft::launch_fused32_fwd(ana, B, C_out, grad_y, g_out, st);
+    }));
+  } else {
+    SWSFT_TRY(run_stage(*p, swsft::kStageDftFwd, st, "dft_fwd", [&] {
+      return swsft::launch_dft_fwd(*p, p->n_out, B, C_out, grad_y, XY, st);
+    }));
+    SWSFT_TRY(run_stage(*p, swsft::kStageLatFwd, st, "lat_fwd",
+                        [&] { return swsft::launch_lat_fwd(ana, B, C_out, XY, g_out, st); }));
+  }
   if (grad_filters != nullptr) {
     const void* a = coef_x;  // F x as saved by the forward pass, or computed here
     if (a == nullptr) {

@@ -196,6 +196,20 @@ int phase_collapse_max_channels(int n_spins);
 hipError_t launch_phase_collapse(const Plan& p, int B, int C, const void* x,
                                  const float2* W1, const float2* W2, const float2* bias,
                                  void* y, hipStream_t st);
+// Whole transforms of 32 x 32 float grids in one launch per direction
+// (fused32.hip): the longitude spectrum stays in LDS.  C (maps per batch
+// item and spin) a multiple of 8.
+inline bool fused32_ok(const Plan& p, int C) {
+  return p.H == 32 && p.W == 32 && p.dtype == SWSFT_F32 && p.fft_ok &&
+         !(p.flags & SWSFT_PLAN_DFT_MATMUL) && !is_delta(p) && C % 8 == 0 && p.Hp == 32 &&
+         p.L <= 16 && p.Lp % 4 == 0;
+}
+// x [B][S_in][C][32][32] -> coef [L^2][B][S_in][C] with p.tab_fwd
+hipError_t launch_fused32_fwd(const Plan& p, int B, int C, const void* x, void* coef,
+                              hipStream_t st);
+// coef [L^2][Bc][S_out][C] (Bc = p.coef_ldb or B) -> y [B][S_out][C][32][32] with p.tab_inv
+hipError_t launch_fused32_inv(const Plan& p, int B, int C, const void* coef, void* y,
+                              hipStream_t st);
 // Measurement helper (probe.hip): n_waves waves (a multiple of 4) each run
 // `iters` rounds of four register-only MFMAs of the dtype's shape; out holds
 // 64 n_waves floats.

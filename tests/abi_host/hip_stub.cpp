@@ -322,6 +322,24 @@ hipError_t launch_delta_theta_fwd(const Plan& p, int B, int C, const void* X, vo
   stub::wr("delta_theta_fwd CS", CS, delta_elems(p, p.n_in, B, C) * p.elem);
   return hipSuccess;
 }
+hipError_t launch_fused32_fwd(const Plan& p, int B, int C, const void* x, void* coef,
+                              hipStream_t) {
+  stub::count();
+  stub::rd("fused32_fwd x", x, spatial(p, p.n_in, B, C));
+  stub::rd("fused32_fwd table", p.tab_fwd, p.n_in * p.fwd_table_elems() * p.elem);
+  stub::wr("fused32_fwd coef", coef, coefb(p, p.n_in, B, C));
+  return hipSuccess;
+}
+hipError_t launch_fused32_inv(const Plan& p, int B, int C, const void* coef, void* y,
+                              hipStream_t) {
+  stub::count();
+  const int ldb = p.coef_ldb > 0 ? p.coef_ldb : B;
+  const size_t row = (size_t)ldb * p.n_out * 2 * C * p.elem;  // one coefficient row (l, m)
+  stub::rd("fused32_inv coef", coef, ((size_t)p.L * p.L - 1) * row + (size_t)B * p.n_out * 2 * C * p.elem);
+  stub::rd("fused32_inv table", p.tab_inv, p.n_out * p.inv_table_elems() * p.elem);
+  stub::wr("fused32_inv y", y, spatial(p, p.n_out, B, C));
+  return hipSuccess;
+}
 double mfma_probe_flops_per_wave_round(int dtype) {
   return dtype == SWSFT_BF16 ? 4.0 * 2 * 32 * 32 * 16 : 4.0 * 2 * 32 * 32 * 2;
 }
