@@ -429,6 +429,21 @@ size_t swsft_workspace_bytes(swsft_plan p, int op, int B, int C_in, int C_out) {
 
 namespace {
 
+// The analysis x -> coef on the input spins of p with its table tab_fwd
+// (direct latitude route), stage times recorded on tp: one launch for 32 x 32
+// float grids (the spectrum stays in LDS), else the longitude DFT into X and
+// the latitude GEMM.
+swsft_status analysis_stages(Plan& tp, const Plan& p, int B, int C, const void* x, void* X,
+                             void* coef, hipStream_t st) {
+  if (swsft::fused32_ok(p, C))
+    return run_stage(tp, swsft::kStageSmallFwd, st, "small_fwd",
+                     [&] { return swsft::launch_fused32_fwd(p, B, C, x, coef, st); });
+  SWSFT_TRY(run_stage(tp, swsft::kStageDftFwd, st, "dft_fwd",
+                      [&] { return swsft::launch_dft_fwd(p, p.n_in, B, C, x, X, st); }));
+  return run_stage(tp, swsft::kStageLatFwd, st, "lat_fwd",
+                   [&] { return swsft::launch_lat_fwd(p, B, C, X, coef, st); });
+}
+
 // The forward transform x -> coef: longitude stage into X, then the latitude
 // stage directly (d tables) or by the Delta route (theta GEMM into D, then
 // the Delta contraction by the latitude kernels on a plan view whose "grid"
@@ -438,14 +453,9 @@ swsft_status forward_stages(Plan& p, int B, int C, const void* x, void* X, void*
   if (swsft::small_path(p, 1))
     return run_stage(p, swsft::kStageSmallFwd, st, "small_fwd",
                      [&] { return swsft::launch_small_fwd(p, B, C, x, coef, st); });
-  if (swsft::fused32_ok(p, C))
-    return run_stage(p, swsft::kStageSmallFwd, st, "small_fwd",
-                     [&] { return swsft::launch_fused32_fwd(p, B, C, x, coef, st); });
+  if (!swsft::is_delta(p)) return analysis_stages(p, p, B, C, x, X, coef, st);
   SWSFT_TRY(run_stage(p, swsft::kStageDftFwd, st, "dft_fwd",
                       [&] { return swsft::launch_dft_fwd(p, p.n_in, B, C, x, X, st); }));
-  if (!swsft::is_delta(p))
-    return run_stage(p, swsft::kStageLatFwd, st, "lat_fwd",
-                     [&] { return swsft::launch_lat_fwd(p, B, C, X, coef, st); });
   SWSFT_TRY(run_stage(p, swsft::kStageDeltaTheta, st, "delta_theta",
                       [&] { return swsft::launch_delta_theta_fwd(p, B, C, X, D, st); }));
   Plan v = p;
@@ -750,17 +760,7 @@ swsft_status spin_sph_conv_backward(swsft_plan p, int B, int C_in, int C_out, co
   syn.n_out = p->n_in;
   for (int i = 0; i < swsft::kMaxSpins; ++i) syn.spins_out[i] = p->spins_in[i];
 
-  if (swsft::fused32_ok(ana, C_out)) {
-    SWSFT_TRY(run_stage(*p, swsft::kStageSmallFwd, st, "small_fwd", [&] {
-      return swsft::launch_fused32_fwd(ana, B, C_out, grad_y, g_out, st);
-    }));
-  } else {
-    SWSFT_TRY(run_stage(*p, swsft::kStageDftFwd, st, "dft_fwd", [&] {
-      return swsft::launch_dft_fwd(*p, p->n_out, B, C_out, grad_y, XY, st);
-    }));
-    SWSFT_TRY(run_stage(*p, swsft::kStageLatFwd, st, "lat_fwd",
-                        [&] { return swsft::launch_lat_fwd(ana, B, C_out, XY, g_out, st); }));
-  }
+  SWSFT_TRY(analysis_stages(*p, ana, B, C_out, grad_y, XY, g_out, st));
   if (grad_filters != nullptr) {
     const void* a = coef_x;  // F x as saved by the forward pass, or computed here
     if (a == nullptr) {
@@ -939,38 +939,26 @@ swsft_status spin_sph_residual_block_forward(swsft_plan p_in, swsft_plan p_out, 
   auto f2 = [](const void* q) { return static_cast<const float2*>(q); };
 
   // stage timing is recorded on the output plan
-  SWSFT_TRY(run_stage(po, swsft::kStageDftFwd, st, "dft_fwd",
-                      [&] { return swsft::launch_dft_fwd(pi, S, B, C, x, XY, st); }));
-  SWSFT_TRY(run_stage(po, swsft::kStageLatFwd, st, "lat_fwd",
-                      [&] { return swsft::launch_lat_fwd(pi, B, C, XY, a, st); }));
+  SWSFT_TRY(analysis_stages(po, pi, B, C, x, XY, a, st));
   SWSFT_TRY(run_stage(po, swsft::kStageMix, st, "mix",
                       [&] { return swsft::launch_mix(po, B, C, C, a, prm->K1, h, st); }));
   SWSFT_TRY(run_stage(po, swsft::kStageBatchNorm, st, "batch_norm", [&] {
     return swsft::launch_batch_norm(po, B, C, h, prm->gamma1, f2(prm->beta1), prm->eps, nullptr,
                                     prm->var1_out, nullptr, h, bnws, st);
   }));
-  SWSFT_TRY(run_stage(po, swsft::kStageLatInv, st, "lat_inv",
-                      [&] { return swsft::launch_lat_inv(po, B, C, h, XY, st); }));
-  SWSFT_TRY(run_stage(po, swsft::kStageDftInv, st, "dft_inv",
-                      [&] { return swsft::launch_dft_inv(po, S, B, C, XY, z, st); }));
+  SWSFT_TRY(synthesis_stages(po, po, B, C, h, XY, z, st));
   SWSFT_TRY(run_stage(po, swsft::kStagePhaseCollapse, st, "phase_collapse", [&] {
     return swsft::launch_phase_collapse(po, B, C, z, f2(prm->pc1_W1), f2(prm->pc1_W2),
                                         f2(prm->pc1_b), z, st);
   }));
-  SWSFT_TRY(run_stage(po, swsft::kStageDftFwd, st, "dft_fwd",
-                      [&] { return swsft::launch_dft_fwd(po, S, B, C, z, XY, st); }));
-  SWSFT_TRY(run_stage(po, swsft::kStageLatFwd, st, "lat_fwd",
-                      [&] { return swsft::launch_lat_fwd(po, B, C, XY, h, st); }));
+  SWSFT_TRY(analysis_stages(po, po, B, C, z, XY, h, st));
   SWSFT_TRY(run_stage(po, swsft::kStageMix, st, "mix",
                       [&] { return swsft::launch_mix(po, B, C, C, h, prm->K2, g, st); }));
   SWSFT_TRY(run_stage(po, swsft::kStageBatchNorm, st, "batch_norm", [&] {
     return swsft::launch_batch_norm(po, B, C, g, prm->gamma2, f2(prm->beta2), prm->eps, nullptr,
                                     prm->var2_out, a, g, bnws, st);
   }));
-  SWSFT_TRY(run_stage(po, swsft::kStageLatInv, st, "lat_inv",
-                      [&] { return swsft::launch_lat_inv(po, B, C, g, XY, st); }));
-  SWSFT_TRY(run_stage(po, swsft::kStageDftInv, st, "dft_inv",
-                      [&] { return swsft::launch_dft_inv(po, S, B, C, XY, y, st); }));
+  SWSFT_TRY(synthesis_stages(po, po, B, C, g, XY, y, st));
   return run_stage(po, swsft::kStagePhaseCollapse, st, "phase_collapse", [&] {
     return swsft::launch_phase_collapse(po, B, C, y, f2(prm->pc2_W1), f2(prm->pc2_W2),
                                         f2(prm->pc2_b), y, st);
