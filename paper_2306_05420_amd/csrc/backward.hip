@@ -465,24 +465,34 @@ __global__ void __launch_bounds__(256) filter_grad_reduce_kernel(const float* __
   }
 }
 
-// ---------------------------------------------------------------- bf16 filter gradient, DMA
-// The same gradient as one real GEMM over the interleaved values as stored:
-//   P[(t',rho)][(s',sigma)] = sum_k g_rho[k][t'] a_sigma[k][s'],
-//   gK[t'][s'] = (P[re][re] + P[im][im], P[im][re] - P[re][im]),
-// rows from g and columns from a, both K-major (row k = one coefficient row
-// (m, b), channels contiguous), so their tiles are copied global -> LDS
-// unchanged ([k][cols], 16-byte chunks swizzled by k), fragments are read
-// with ds_read_b64_tr_b16 on both sides, and the 2 x 2 blocks are combined
-// in registers (rows 2q, 2q+1 are registers r, r+1 of a lane; columns
-// 2p, 2p+1 are neighbouring lanes).  Contraction rows past (2l+1) B are
-// copied from a clamped row and zeroed in LDS before use.
-template <int RA, int RB, int TN, int ST>
-struct GradDmaGeom {
-  static constexpr int BK = 32;  // contraction rows per K step
-  static constexpr int TM = 2;   // 32-row MFMA tiles per wave (64 rows)
-  static constexpr int WM = RA / (32 * TM), WN = RB / (32 * TN);
+// ---------------------------------------------------------------- bf16 filter gradient, split accumulators
+// The same gradient as a complex GEMM per degree with separate real and
+// imaginary accumulators, the contraction running over (k, rho):
+//   Re gK[t'][s'] = sum_k gr ar + gi ai   (g and a as stored, (re, im) per k),
+//   Im gK[t'][s'] = sum_k gi ar - gr ai   (each g pair turned into (gi, -gr) in registers).
+// Both operands are K-major (row k = one coefficient row (m, b), channels
+// contiguous); each tile is copied global -> LDS unchanged as [k][RA or RB
+// complex columns] (swz_k4 chunk order) and a lane gathers the 4 consecutive
+// contraction rows of its column as 4 dword reads, so one read of a g
+// fragment feeds a real and an imaginary MFMA.  A wave owns TM x TN blocks of
+// 32 x 32 complex outputs.  A real GEMM over the interleaved values, which
+// keeps all four real products of every complex output until its epilogue,
+// needs twice the accumulators per output; here the same registers hold
+// twice the outputs, so a 128 x 128 complex tile copies each row of g and of
+// a for 4 tiles (16 KB of copies per contraction row and degree at 512 x 512
+// channels, against 24 KB for 256 x 128 real tiles) and reads half the LDS
+// bytes per MFMA.  Contraction rows past (2l+1) B are copied from a clamped
+// row and zeroed in LDS before use.
+typedef unsigned v4u_t __attribute__((ext_vector_type(4)));
+
+template <int WM, int WN, int ST>
+struct GradSplitGeom {
+  static constexpr int BK = 32;            // contraction rows per K step
+  static constexpr int TM = 2, TN = 2;     // 32 x 32 complex blocks per wave
+  static constexpr int RA = 32 * TM * WM;  // complex rows t' per workgroup
+  static constexpr int RB = 32 * TN * WN;  // complex columns s' per workgroup
   static constexpr int NW = WM * WN, NT = 64 * NW;
-  static constexpr int PITCH_A = 2 * RA, PITCH_B = 2 * RB;  // bytes per k row
+  static constexpr int PITCH_A = 4 * RA, PITCH_B = 4 * RB;  // bytes per k row
   static constexpr int RPI_A = 1024 / PITCH_A, LPR_A = 64 / RPI_A;
   static constexpr int RPI_B = 1024 / PITCH_B, LPR_B = 64 / RPI_B;
   static constexpr int A_BYTES = BK * PITCH_A, B_BYTES = BK * PITCH_B;
@@ -490,55 +500,54 @@ struct GradDmaGeom {
   static constexpr int PER_WAVE = NI / NW;
   static constexpr int STAGE = A_BYTES + B_BYTES;
   static constexpr int SMEM = ST * STAGE;
-  static_assert(RA % 128 == 0 && RB % 128 == 0 && NI % NW == 0 && RPI_A >= 1 && RPI_B >= 1 &&
+  static_assert(PITCH_A <= 1024 && PITCH_B <= 1024 && 1024 % PITCH_A == 0 &&
+                    1024 % PITCH_B == 0 && PITCH_A >= 256 && PITCH_B >= 256 && NI % NW == 0 &&
                     ST >= 2 && (ST - 2) * PER_WAVE < 64,
                 "tile shape");
+  static_assert(RA * RB * 4 <= SMEM, "staged output tile");
 };
 
-__device__ __forceinline__ v4s tr_read_t(const unsigned char* tile, int pitch, int k, int col) {
-  const unsigned char* p = tile + k * pitch + swz_t(k, col >> 3) * 16 + (col & 7) * 2;
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) v4s*)((__attribute__((address_space(3))) unsigned char*)p));
-}
-
-template <int RA, int RB, int TN, int ST>
-__global__ void __launch_bounds__((GradDmaGeom<RA, RB, TN, ST>::NT))
-    filter_grad_dma_kernel(const __bf16* __restrict__ a, const __bf16* __restrict__ g,
-                           __bf16* __restrict__ gK, int L, int B, int Cin, int Cout, int n_in,
-                           int n_out, Spins sin_, Spins sout_, int tiles_r, int tiles_c) {
-  using G = GradDmaGeom<RA, RB, TN, ST>;
-  constexpr int BK = G::BK, TM = G::TM;
-  __shared__ __align__(16) unsigned char smem[G::SMEM];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / G::WN, wn = wave % G::WN;
+// (two workgroups per CU: at most 256 registers per lane)
+template <int WM, int WN, int ST>
+__global__ void __launch_bounds__((GradSplitGeom<WM, WN, ST>::NT), 2)
+    filter_grad_split_kernel(const __bf16* __restrict__ a, const __bf16* __restrict__ g,
+                             __bf16* __restrict__ gK, int L, int B, int Cin, int Cout, int n_in,
+                             int n_out, Spins sin_, Spins sout_, int tiles_r, int tiles_c) {
+  using G = GradSplitGeom<WM, WN, ST>;
+  constexpr int BK = G::BK, TM = G::TM, TN = G::TN, RA = G::RA, RB = G::RB;
+  extern __shared__ __align__(16) unsigned char smem[];  // the ring, then the output tile
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
   const int per_l = tiles_r * tiles_c;
   const int lb = xcd_logical_block();
   if (lb >= L * per_l) return;
   const int l = paired_degree(lb / per_l, L);
   const int tile = lb % per_l;
   const int Nc = n_out * Cout, Kc = n_in * Cin;
-  const int R2 = 2 * Nc, Q2 = 2 * Kc;  // real rows (from g) and columns (from a)
-  const int r0 = (tile / tiles_c) * RA, c0 = (tile % tiles_c) * RB;
+  const int r0 = (tile / tiles_c) * RA, c0 = (tile % tiles_c) * RB;  // first t', first s'
   const int Kl = (2 * l + 1) * B;
   const size_t row0 = (size_t)l * l * B;
 
   bool rows_dead = true, cols_dead = true;
-  for (int t = (r0 / 2) / Cout; t <= (min(r0 + RA, R2) / 2 - 1) / Cout; ++t)
+  for (int t = r0 / Cout; t <= (min(r0 + RA, Nc) - 1) / Cout; ++t)
     if (iabs_(sout_.s[t]) <= l) rows_dead = false;
-  for (int q = (c0 / 2) / Cin; q <= (min(c0 + RB, Q2) / 2 - 1) / Cin; ++q)
+  for (int q = c0 / Cin; q <= (min(c0 + RB, Kc) - 1) / Cin; ++q)
     if (iabs_(sin_.s[q]) <= l) cols_dead = false;
 
-  v16f acc[TM][TN];
+  v16f acc_re[TM][TN], acc_im[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      for (int r = 0; r < 16; ++r) acc_re[i][j][r] = acc_im[i][j][r] = 0.f;
 
   if (!rows_dead && !cols_dead) {
-    // copy u of this wave: g rows (A tile) for copy index < NI_A, else a rows;
-    // lane -> (k row of the step, 16-byte slot), source chunk swizzled by k
+    // copy u of this wave: g rows (A tile) for copy index < NI_A, else a
+    // rows; lane -> (k row of the step, 16-byte slot), the slot holding
+    // chunk swz_k4(k, slot) of the row (4 complex columns, clamped to the
+    // last whole chunk: those columns are never stored)
     const __bf16* src[G::PER_WAVE];
     int krow[G::PER_WAVE], pitch[G::PER_WAVE];
 #pragma unroll
@@ -546,17 +555,16 @@ __global__ void __launch_bounds__((GradDmaGeom<RA, RB, TN, ST>::NT))
       const int gi = wave * G::PER_WAVE + u;
       if (gi < G::NI_A) {
         const int k = gi * G::RPI_A + lane / G::LPR_A;
-        const int col = min(r0 + swz_t(k, lane % G::LPR_A) * 8, R2 - 8);
-        src[u] = g + col;
+        const int col = min(r0 + 4 * swz_k4(k, lane % G::LPR_A), Nc - 4);
+        src[u] = g + 2 * (size_t)col;
         krow[u] = k;
-        pitch[u] = R2;
+        pitch[u] = 2 * Nc;
       } else {
-        const int gb = gi - G::NI_A;
-        const int k = gb * G::RPI_B + lane / G::LPR_B;
-        const int col = min(c0 + swz_t(k, lane % G::LPR_B) * 8, Q2 - 8);
-        src[u] = a + col;
+        const int k = (gi - G::NI_A) * G::RPI_B + lane / G::LPR_B;
+        const int col = min(c0 + 4 * swz_k4(k, lane % G::LPR_B), Kc - 4);
+        src[u] = a + 2 * (size_t)col;
         krow[u] = k;
-        pitch[u] = Q2;
+        pitch[u] = 2 * Kc;
       }
     }
     const unsigned ring = lds_addr(smem);
@@ -570,117 +578,120 @@ __global__ void __launch_bounds__((GradDmaGeom<RA, RB, TN, ST>::NT))
     };
     const int nk = (Kl + BK - 1) / BK;
 #pragma unroll
-    for (int st = 0; st < ST - 1; ++st)
-      if (st < nk) issue(st, st);
-    const int kh = lane >> 5, q4 = (lane & 15) >> 2, c4 = 4 * (lane & 3);
-    const int rr0 = 16 * ((lane >> 4) & 1);
+    for (int s = 0; s < ST - 1; ++s)
+      if (s < nk) issue(s, s);
+    const int r32 = lane & 31, kh = lane >> 5;
+    // the 4 contraction rows 4c .. 4c + 3 of column col of a K-major tile
+    auto gather = [](const unsigned char* tile, int pitch_b, int c, int col) {
+      v4u_t y;
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        const int kr = 4 * c + d;
+        y[d] = *reinterpret_cast<const unsigned*>(tile + kr * pitch_b + swz_k4(kr, col >> 2) * 16 +
+                                                  (col & 3) * 4);
+      }
+      return y;
+    };
     for (int i = 0; i < nk; ++i) {
       const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
       wait_groups<ST - 2, G::PER_WAVE>(issued - i - 1);
-      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_s_barrier();  // every wave's copies of step i landed; step i-1 is consumed
       if (i + ST - 1 < nk) issue(i + ST - 1, (i + ST - 1) % ST);
       unsigned char* As = smem + (i % ST) * G::STAGE;
       unsigned char* Bs = As + G::A_BYTES;
       const int kv = Kl - i * BK;  // valid rows of this step
       if (kv < BK) {
         // the clamped rows of the last step hold other data: zero them
-        const int zb = (BK - kv) * G::PITCH_A, zc = (BK - kv) * G::PITCH_B;
-        for (int o = tid * 16; o < zb; o += G::NT * 16)
+        const int za = (BK - kv) * G::PITCH_A, zb = (BK - kv) * G::PITCH_B;
+        for (int o = tid * 16; o < za; o += G::NT * 16)
           *reinterpret_cast<uint4*>(As + kv * G::PITCH_A + o) = make_uint4(0, 0, 0, 0);
-        for (int o = tid * 16; o < zc; o += G::NT * 16)
+        for (int o = tid * 16; o < zb; o += G::NT * 16)
           *reinterpret_cast<uint4*>(Bs + kv * G::PITCH_B + o) = make_uint4(0, 0, 0, 0);
         __syncthreads();
       }
 #pragma unroll
-      for (int kk = 0; kk < BK / 16; ++kk) {
-        const int kbase = kk * 16 + 8 * kh + q4;
-        v8bf fa[TM], fb[TN];
+      for (int kk = 0; kk < BK / 8; ++kk) {  // MFMA K steps of 8 rows (4 per lane half)
+        const int c = 2 * kk + kh;
+        v8bf xb[TN];
+#pragma unroll
+        for (int jj = 0; jj < TN; ++jj)
+          xb[jj] = __builtin_bit_cast(v8bf, gather(Bs, G::PITCH_B, c, (wn * TN + jj) * 32 + r32));
 #pragma unroll
         for (int ii = 0; ii < TM; ++ii) {
-          const int col = wm * 32 * TM + ii * 32 + rr0 + c4;
-          const v4s lo4 = tr_read_t(As, G::PITCH_A, kbase, col);
-          const v4s hi4 = tr_read_t(As, G::PITCH_A, kbase + 4, col);
-          fa[ii] = __builtin_bit_cast(v8bf, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+          const v4u_t x = gather(As, G::PITCH_A, c, (wm * TM + ii) * 32 + r32);
+          v4u_t xi;
+#pragma unroll
+          for (int d = 0; d < 4; ++d)
+            xi[d] = __builtin_amdgcn_alignbit(x[d], x[d], 16u) ^ 0x80000000u;  // (gi, -gr)
+          const v8bf ar = __builtin_bit_cast(v8bf, x), ai = __builtin_bit_cast(v8bf, xi);
+#pragma unroll
+          for (int jj = 0; jj < TN; ++jj) {
+            acc_re[ii][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ar, xb[jj], acc_re[ii][jj], 0, 0, 0);
+            acc_im[ii][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ai, xb[jj], acc_im[ii][jj], 0, 0, 0);
+          }
         }
-#pragma unroll
-        for (int jj = 0; jj < TN; ++jj) {
-          const int col = wn * 32 * TN + jj * 32 + rr0 + c4;
-          const v4s lo4 = tr_read_t(Bs, G::PITCH_B, kbase, col);
-          const v4s hi4 = tr_read_t(Bs, G::PITCH_B, kbase + 4, col);
-          fb[jj] = __builtin_bit_cast(v8bf, __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
-        }
-#pragma unroll
-        for (int ii = 0; ii < TM; ++ii)
-#pragma unroll
-          for (int jj = 0; jj < TN; ++jj)
-            acc[ii][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ii], fb[jj], acc[ii][jj], 0, 0, 0);
       }
     }
     wait_vmcnt<0>();
   }
 
-  // epilogue: rows 2q, 2q+1 of a column are registers r, r+1 of one lane;
-  // columns 2p, 2p+1 are lanes 2p', 2p'+1: the even lane combines
-  //   re = P[2q][2p] + P[2q+1][2p+1],  im = P[2q+1][2p] - P[2q][2p+1]
-  // into one bf16 pair, staged in LDS as the tile's [t'][s'] block (row pitch
-  // padded by 16 bytes: the two row groups of a store hit different banks),
-  // then written by all threads as 16-byte chunks (4 outputs) along s'.
+  // epilogue: register r of a lane holds row 8 (r / 4) + 4 (lane / 32) + r % 4
+  // of its block, column lane % 32; the (re, im) bf16 pairs are staged in LDS
+  // as the tile's [t'][s'] block (16-byte chunks of rows with bit 2 set moved
+  // by 128 bytes), then written by all threads as 16-byte chunks along s'.
+  // Outputs of spins that do not exist at this degree are zero.
   typedef float f32x2 __attribute__((ext_vector_type(2)));
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  constexpr int OP = RB / 2 * 4 + 16;  // bytes per staged row
-  constexpr int CPRO = RB / 8;         // 16-byte chunks per staged row
-  static_assert(RA / 2 * OP <= G::SMEM, "staged output tile");
-  __syncthreads();  // every wave is done with the ring
+  constexpr int RP = RB * 4;    // bytes per staged row
+  constexpr int CPRO = RB / 4;  // 16-byte chunks per staged row
+  __syncthreads();              // every wave is done with the ring
+  const int col_l = lane & 31, row_l = 4 * (lane >> 5);
 #pragma unroll
-  for (int ii = 0; ii < TM; ++ii)
+  for (int jj = 0; jj < TN; ++jj) {
+    const int cl = (wn * TN + jj) * 32 + col_l;
+    const int sc = c0 + cl;
+    const bool col_live = sc < Kc && iabs_(sin_.s[(sc < Kc ? sc : 0) / Cin]) <= l;
 #pragma unroll
-    for (int jj = 0; jj < TN; ++jj) {
-      float x[16];
+    for (int ii = 0; ii < TM; ++ii)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) x[r] = __shfl_xor(acc[ii][jj][r], 1);
-      if (lane & 1) continue;
-      const int cl = wn * 32 * TN + jj * 32 + (lane & 31);  // even local column
-      const int sc = (c0 + cl) >> 1;
-      const bool col_live = sc < Kc && iabs_(sin_.s[sc / Cin]) <= l;
-#pragma unroll
-      for (int r = 0; r < 16; r += 2) {
-        const int rl = wm * 32 * TM + ii * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int tc = (r0 + rl) >> 1;
-        const bool live = col_live && tc < Nc && iabs_(sout_.s[tc / Cout]) <= l;
-        const float re = live ? acc[ii][jj][r] + x[r + 1] : 0.f;
-        const float im = live ? acc[ii][jj][r + 1] - x[r] : 0.f;
-        *reinterpret_cast<bf16x2*>(smem + (rl >> 1) * OP + (cl >> 1) * 4) =
-            __builtin_convertvector((f32x2){re, im}, bf16x2);
+      for (int r = 0; r < 16; ++r) {
+        const int rl = (wm * TM + ii) * 32 + 8 * (r >> 2) + row_l + (r & 3);
+        const int tc = r0 + rl;
+        const bool live = col_live && tc < Nc && iabs_(sout_.s[(tc < Nc ? tc : 0) / Cout]) <= l;
+        const f32x2 v = live ? (f32x2){acc_re[ii][jj][r], acc_im[ii][jj][r]} : (f32x2){0.f, 0.f};
+        *reinterpret_cast<bf16x2*>(smem + rl * RP + swz_k4(rl, cl >> 2) * 16 + (cl & 3) * 4) =
+            __builtin_convertvector(v, bf16x2);
       }
-    }
+  }
   __syncthreads();
   __bf16* out = gK + (size_t)l * Nc * Kc * 2;
-  for (int idx = tid; idx < RA / 2 * CPRO; idx += G::NT) {
+  for (int idx = tid; idx < RA * CPRO; idx += G::NT) {
     const int rl = idx / CPRO, ch = idx % CPRO;
-    const int tc = r0 / 2 + rl, sc = c0 / 2 + 4 * ch;  // Kc % 4 == 0: whole chunks
+    const int tc = r0 + rl, sc = c0 + 4 * ch;  // Kc % 4 == 0: whole chunks
     if (tc < Nc && sc < Kc)
       *reinterpret_cast<uint4*>(out + ((size_t)tc * Kc + sc) * 2) =
-          *reinterpret_cast<const uint4*>(smem + rl * OP + ch * 16);
+          *reinterpret_cast<const uint4*>(smem + rl * RP + swz_k4(rl, ch) * 16);
   }
 }
 
-// rows (from g) x columns (from a) per workgroup, 32-column MFMA tiles per
-// wave, stages: measured best of 256x256x4x2, 256x256x2x2, 256x256x4x3, 256x128x2x3
-#ifndef SWSFT_GRAD_DMA
-#define SWSFT_GRAD_DMA 256, 128, 2, 3
+// waves per workgroup (rows x columns of 64 x 64 complex wave tiles), stages
+#ifndef SWSFT_GRAD_SPLIT
+#define SWSFT_GRAD_SPLIT 2, 2, 2
 #endif
 
-template <int RA, int RB, int TN, int ST>
-hipError_t filter_grad_dma_t(const Plan& p, int B, int Cin, int Cout, const void* a,
-                             const void* g, void* gK, hipStream_t st) {
-  const int R2 = 2 * p.n_out * Cout, Q2 = 2 * p.n_in * Cin;
-  const int tiles_r = (R2 + RA - 1) / RA, tiles_c = (Q2 + RB - 1) / RB;
+template <int WM, int WN, int ST>
+hipError_t filter_grad_split_t(const Plan& p, int B, int Cin, int Cout, const void* a,
+                               const void* g, void* gK, hipStream_t st) {
+  using G = GradSplitGeom<WM, WN, ST>;
+  const int Nc = p.n_out * Cout, Kc = p.n_in * Cin;
+  const int tiles_r = (Nc + G::RA - 1) / G::RA, tiles_c = (Kc + G::RB - 1) / G::RB;
   const long long blocks = (long long)p.L * tiles_r * tiles_c;
-  hipLaunchKernelGGL((filter_grad_dma_kernel<RA, RB, TN, ST>), dim3(xcd_grid(blocks)),
-                     dim3(GradDmaGeom<RA, RB, TN, ST>::NT), 0, st, (const __bf16*)a,
-                     (const __bf16*)g, (__bf16*)gK, p.L, B, Cin, Cout, p.n_in, p.n_out,
-                     to_spins(p.spins_in, p.n_in), to_spins(p.spins_out, p.n_out), tiles_r,
-                     tiles_c);
+  const hipError_t e = ensure_dynamic_lds((const void*)filter_grad_split_kernel<WM, WN, ST>, G::SMEM);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((filter_grad_split_kernel<WM, WN, ST>), dim3(xcd_grid(blocks)), dim3(G::NT),
+                     G::SMEM, st, (const __bf16*)a, (const __bf16*)g, (__bf16*)gK, p.L, B, Cin,
+                     Cout, p.n_in, p.n_out, to_spins(p.spins_in, p.n_in),
+                     to_spins(p.spins_out, p.n_out), tiles_r, tiles_c);
   return hipGetLastError();
 }
 
@@ -694,7 +705,7 @@ hipError_t filter_grad_t(const Plan& p, int B, int Cin, int Cout, const void* a,
                          void* gK, void* part, hipStream_t st) {
   if constexpr (std::is_same<T, __bf16>::value) {
     if (grad_uses_dma(p, Cin, Cout))
-      return filter_grad_dma_t<SWSFT_GRAD_DMA>(p, B, Cin, Cout, a, g, gK, st);
+      return filter_grad_split_t<SWSFT_GRAD_SPLIT>(p, B, Cin, Cout, a, g, gK, st);
   }
   using G = GradGeom<T>;
   const int Nc = p.n_out * Cout, Kc = p.n_in * Cin;

@@ -54,4 +54,10 @@ __device__ __forceinline__ int swz(int r, int c) {
 // four different 64-byte windows.
 __device__ __forceinline__ int swz_t(int k, int c) { return c ^ ((k & 3) << 2); }
 
+// K-major tile read by dword gathers (a lane takes 4 consecutive rows of one
+// column, the two lane halves rows 4 apart; at least 16 chunks per row): the
+// chunks of alternate groups of 4 rows are moved by 128 bytes so that the two
+// halves of a wave hit different banks.  Self-inverse.
+__device__ __forceinline__ int swz_k4(int k, int c) { return c ^ (((k >> 2) & 1) << 3); }
+
 }  // namespace swsft

@@ -71,8 +71,6 @@ struct MixGeom {
   static_assert(ST >= 2 && (ST - 2) * PER_WAVE < 64, "stages");
 };
 
-// chunk position of the adjoint's filter tile (self-inverse)
-__device__ __forceinline__ int swz_adj(int k, int c) { return c ^ (((k >> 2) & 1) << 3); }
 
 // ADJ: the adjoint (Cin, Sin, sin_ describe the contraction side, i.e. the
 // forward's outputs; Cout, Sout, sout_ the results, the forward's inputs).
@@ -146,7 +144,7 @@ __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
       // contraction row kb of the step, 4 outputs per chunk; chunks past the
       // last output are clamped to it (their products are discarded)
       const int kb = (g - G::NI_A) * G::RPI_T + lane / G::LPR_T;
-      const int q = min(q0 + 4 * swz_adj(kb, lane % G::LPR_T), Nc - 4);
+      const int q = min(q0 + 4 * swz_k4(kb, lane % G::LPR_T), Nc - 4);
       gsrc[u] = K0 + (size_t)kb * (2 * Nc) + 2 * q;
     }
   }
@@ -211,7 +209,7 @@ __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
           for (int d = 0; d < 4; ++d) {
             const int kr = 4 * c + d;
             y[d] = *reinterpret_cast<const unsigned*>(Bs + kr * G::PITCH_T +
-                                                      swz_adj(kr, rb >> 2) * 16 + (rb & 3) * 4);
+                                                      swz_k4(kr, rb >> 2) * 16 + (rb & 3) * 4);
           }
           b[jj] = __builtin_bit_cast(v8bf, y);
         }
