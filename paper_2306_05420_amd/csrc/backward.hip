@@ -24,6 +24,7 @@
 #include "swsft_internal.h"
 #include "xcd.h"
 
+
 namespace swsft {
 namespace {
 
@@ -485,9 +486,19 @@ __global__ void __launch_bounds__(256) filter_grad_reduce_kernel(const float* __
 // row and zeroed in LDS before use.
 typedef unsigned v4u_t __attribute__((ext_vector_type(4)));
 
+// Contraction rows per K step and (waves per workgroup as rows x columns of
+// 64 x 64 complex wave tiles, stages); measured at 256^2, C = 256: 16 rows
+// with 4 stages 131 us, 32 with 2 136 us, 8 with 8 143 us.
+#ifndef SWSFT_GRAD_SPLIT_BK
+#define SWSFT_GRAD_SPLIT_BK 16
+#endif
+#ifndef SWSFT_GRAD_SPLIT
+#define SWSFT_GRAD_SPLIT 2, 2, 4
+#endif
+
 template <int WM, int WN, int ST>
 struct GradSplitGeom {
-  static constexpr int BK = 32;            // contraction rows per K step
+  static constexpr int BK = SWSFT_GRAD_SPLIT_BK;  // contraction rows per K step
   static constexpr int TM = 2, TN = 2;     // 32 x 32 complex blocks per wave
   static constexpr int RA = 32 * TM * WM;  // complex rows t' per workgroup
   static constexpr int RB = 32 * TN * WN;  // complex columns s' per workgroup
@@ -674,10 +685,6 @@ __global__ void __launch_bounds__((GradSplitGeom<WM, WN, ST>::NT), 2)
   }
 }
 
-// waves per workgroup (rows x columns of 64 x 64 complex wave tiles), stages
-#ifndef SWSFT_GRAD_SPLIT
-#define SWSFT_GRAD_SPLIT 2, 2, 2
-#endif
 
 template <int WM, int WN, int ST>
 hipError_t filter_grad_split_t(const Plan& p, int B, int Cin, int Cout, const void* a,
