@@ -20,17 +20,14 @@
 // Preconditions (checked by the launcher): K' = 2 S_in C_in with each input
 // spin's channel block a whole number of K steps; bf16 also C_out % 4 == 0.
 //
-// The bf16 kernel also computes the adjoint mixing of the backward pass
-// straight from the filters as stored (ADJ):
+// The adjoint mixing of the backward pass is computed straight from the
+// filters as stored (ADJ mode of the split kernel below and of the float
+// kernel):
 //   coef'[l][(m,b)][(s,c)] = sum_(t,c') g[l][(m,b)][(t,c')] conj(K[l][(t,c')][(s,c)]),
-// the contraction now running over the filter rows.  With g = a + ib and
-// K = c + id, Re = ac + bd and Im = bc - ad, so the expanded rows become
-// (a, b) and (b, -a) against the filter values as stored (c, d); the filter
-// tile is copied k-major ([32 contraction rows][RB outputs], 16-byte chunks
-// moved by 128 bytes on alternate groups of 4 rows so that the two K halves
-// of a wave read different banks) and a lane gathers its 4 consecutive
-// contraction rows of one output as 4 dword reads.  No conjugate-transposed
-// copy of the filters is made.
+// the contraction now running over the filter rows, so the filter tile is
+// copied k-major ([contraction rows][RB outputs]) and a lane gathers its
+// contraction rows of one output.  No conjugate-transposed copy of the
+// filters is made.
 #include <type_traits>
 
 #include "lds_dma.h"
@@ -59,10 +56,6 @@ struct MixGeom {
   static constexpr int LPR = 64 / RPI;               // lanes per row
   static constexpr int NI = (RA + RB) / RPI;         // copies per stage
   static constexpr int NI_A = RA / RPI;              // of which coefficient rows
-  // k-major filter tile of the adjoint: BK / 2 contraction rows of RB outputs
-  static constexpr int PITCH_T = 4 * RB;
-  static constexpr int RPI_T = PITCH_T <= 1024 ? 1024 / PITCH_T : 1;
-  static constexpr int LPR_T = 64 / RPI_T;
   static constexpr int PER_WAVE = NI / NW;
   static constexpr int STAGE = (RA + RB) * PITCH;
   static constexpr int SMEM = ST * STAGE;  // the ring (the epilogue needs no LDS)
@@ -71,18 +64,12 @@ struct MixGeom {
   static_assert(ST >= 2 && (ST - 2) * PER_WAVE < 64, "stages");
 };
 
-
-// ADJ: the adjoint (Cin, Sin, sin_ describe the contraction side, i.e. the
-// forward's outputs; Cout, Sout, sout_ the results, the forward's inputs).
-template <int BK, int RA, int RB, int ST, bool ADJ>
+template <int BK, int RA, int RB, int ST>
 __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
     mix_dma_kernel(const __bf16* __restrict__ coef, const __bf16* __restrict__ K,
                    __bf16* __restrict__ out, int L, int B, int Cin, int Cout, int Sin, int Sout,
                    Spins sin_, Spins sout_) {
   using G = MixGeom<BK, RA, RB, ST>;
-  static_assert(!ADJ || (G::PITCH_T <= 1024 && 1024 % G::PITCH_T == 0 &&
-                         (BK / 2) % G::RPI_T == 0 && (BK / 2) * G::PITCH_T == RB * G::PITCH),
-                "adjoint filter tile");
   __shared__ __align__(16) unsigned char smem[G::SMEM];
   __shared__ int live[G::MAX_KT];
   __shared__ int n_live_s;
@@ -136,24 +123,17 @@ __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
       const int tr = g * G::RPI + lane / G::LPR;  // row of the stage
       const int row = row0 + tr < Mrows ? row0 + tr : Mrows - 1;
       gsrc[u] = A0 + (size_t)row * Kp + swz<G::CPR>(tr, lane % G::LPR) * 8;
-    } else if (!ADJ) {
+    } else {
       const int rb = (g - G::NI_A) * G::RPI + lane / G::LPR;
       const int q = q0 + rb < Nc ? q0 + rb : Nc - 1;
       gsrc[u] = K0 + (size_t)q * Kp + swz<G::CPR>(rb, lane % G::LPR) * 8;
-    } else {
-      // contraction row kb of the step, 4 outputs per chunk; chunks past the
-      // last output are clamped to it (their products are discarded)
-      const int kb = (g - G::NI_A) * G::RPI_T + lane / G::LPR_T;
-      const int q = min(q0 + 4 * swz_k4(kb, lane % G::LPR_T), Nc - 4);
-      gsrc[u] = K0 + (size_t)kb * (2 * Nc) + 2 * q;
     }
   }
   auto issue = [&](int i, int stage) {
-    const int koff = live[i] * BK;                                   // along coefficient rows
-    const size_t koff_b = ADJ ? (size_t)live[i] * (BK / 2) * (2 * Nc) : (size_t)koff;
+    const int koff = live[i] * BK;  // along the rows of both operands
     const unsigned base = ring_base + stage * G::STAGE + wave * G::PER_WAVE * 1024;
 #pragma unroll
-    for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + (is_a[u] ? koff : koff_b), base + u * 1024);
+    for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + koff, base + u * 1024);
   };
 
   typedef unsigned v4u __attribute__((ext_vector_type(4)));
@@ -172,10 +152,9 @@ __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
 
   const int r32 = lane & 31, kh = lane >> 5;
   // odd expanded rows (im, re): rotate by 16 bits; even rows (re, -im): flip
-  // the high half's sign (the row parity is the lane parity).  Adjoint: even
-  // rows (re, im) as stored, odd rows (im, -re): rotate, then flip.
+  // the high half's sign (the row parity is the lane parity)
   const unsigned rot = (lane & 1) ? 16u : 0u;
-  const unsigned sgn = ((lane & 1) != 0) == ADJ ? 0x80000000u : 0u;
+  const unsigned sgn = (lane & 1) ? 0u : 0x80000000u;
   for (int i = 0; i < nk; ++i) {
     // K step i has landed once at most (issued - i - 1) steps are outstanding
     const int issued = nk < i + ST - 1 ? nk : i + ST - 1;
@@ -200,19 +179,7 @@ __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
 #pragma unroll
       for (int jj = 0; jj < 2; ++jj) {
         const int rb = wn * 64 + jj * 32 + r32;
-        if constexpr (!ADJ) {
-          b[jj] = *reinterpret_cast<const v8bf*>(Bs + rb * G::PITCH + swz<G::CPR>(rb, c) * 16);
-        } else {
-          // contraction rows 4c .. 4c + 3 of output rb: (re, im) each
-          v4u y;
-#pragma unroll
-          for (int d = 0; d < 4; ++d) {
-            const int kr = 4 * c + d;
-            y[d] = *reinterpret_cast<const unsigned*>(Bs + kr * G::PITCH_T +
-                                                      swz_k4(kr, rb >> 2) * 16 + (rb & 3) * 4);
-          }
-          b[jj] = __builtin_bit_cast(v8bf, y);
-        }
+        b[jj] = *reinterpret_cast<const v8bf*>(Bs + rb * G::PITCH + swz<G::CPR>(rb, c) * 16);
       }
 #pragma unroll
       for (int ii = 0; ii < 2; ++ii)
@@ -251,7 +218,7 @@ __global__ void __launch_bounds__((MixGeom<BK, RA, RB, ST>::NT))
   }
 }
 
-template <int BK, int RA, int RB, int ST, bool ADJ = false>
+template <int BK, int RA, int RB, int ST>
 hipError_t launch_geom(const Plan& p, int B, int Cin, int Cout, const void* coef, const void* K,
                        void* out, hipStream_t st) {
   using G = MixGeom<BK, RA, RB, ST>;
@@ -262,7 +229,7 @@ hipError_t launch_geom(const Plan& p, int B, int Cin, int Cout, const void* coef
   for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + RA - 1) / RA;
   const int Nc = p.n_out * Cout;
   const long long blocks = (long long)tiles * ((Nc + RB - 1) / RB);
-  hipLaunchKernelGGL((mix_dma_kernel<BK, RA, RB, ST, ADJ>), dim3(xcd_grid(blocks)), dim3(G::NT), 0,
+  hipLaunchKernelGGL((mix_dma_kernel<BK, RA, RB, ST>), dim3(xcd_grid(blocks)), dim3(G::NT), 0,
                      st, (const __bf16*)coef, (const __bf16*)K, (__bf16*)out, p.L, B, Cin, Cout,
                      p.n_in, p.n_out, si, so);
   return hipGetLastError();
@@ -299,17 +266,33 @@ struct MixGeomS {
   static constexpr int STAGE = (RA + RB) * PITCH;
   static constexpr int SMEM = ST * STAGE;
   static constexpr int MAX_KT = kMaxKp / BK;
+  // k-major filter tile of the adjoint: BK / 2 contraction rows of RB outputs
+  static constexpr int PITCH_T = 4 * RB;
+  static constexpr int RPI_T = PITCH_T <= 1024 ? 1024 / PITCH_T : 1;
+  static constexpr int LPR_T = 64 / RPI_T;
   static_assert(RA % RPI == 0 && NI % NW == 0, "tile shape");
   static_assert(ST >= 2 && (ST - 2) * PER_WAVE < 64, "stages");
 };
 
-template <int WM, int WN, int ST, bool REG>
+// ADJ: the adjoint mixing of the backward pass from the filters as stored
+// (Cin, Sin, sin_ describe the contraction side, i.e. the forward's outputs;
+// Cout, Sout, sout_ the results, the forward's inputs): the filter tile is
+// copied k-major ([32 contraction rows][RB outputs], swz_k4 chunk order) and
+// a lane gathers its 4 consecutive contraction rows of one output as 4 dword
+// reads; with g = (gr, gi) and K = (Kr, Ki), Re = gr Kr + gi Ki takes the
+// coefficient values as stored and Im = gi Kr - gr Ki takes them as
+// (gi, -gr).  (256^2, C = 256: 94 us against 101 us for the expanded-row
+// form with the same gathers, which issued 1.25x the MFMAs.)
+template <int WM, int WN, int ST, bool REG, bool ADJ = false>
 __global__ void __launch_bounds__((MixGeomS<WM, WN, ST>::NT))
     mix_split_kernel(const __bf16* __restrict__ coef, const __bf16* __restrict__ K,
                      __bf16* __restrict__ out, int L, int B, int Cin, int Cout, int Sin, int Sout,
                      Spins sin_, Spins sout_) {
   using G = MixGeomS<WM, WN, ST>;
   constexpr int TM = G::TM, TN = G::TN, RA = G::RA, RB = G::RB, BK = G::BK;
+  static_assert(!ADJ || (!REG && G::PITCH_T <= 1024 && 1024 % G::PITCH_T == 0 &&
+                         (BK / 2) % G::RPI_T == 0 && (BK / 2) * G::PITCH_T == RB * G::PITCH),
+                "adjoint filter tile");
   extern __shared__ __align__(16) unsigned char smem[];  // G::SMEM bytes: the ring, then the output tile
   __shared__ int live[G::MAX_KT];
   __shared__ int n_live_s;
@@ -360,17 +343,24 @@ __global__ void __launch_bounds__((MixGeomS<WM, WN, ST>::NT))
       const int tr = g * G::RPI + lane / G::LPR;
       const int row = row0 + tr < Mrows ? row0 + tr : Mrows - 1;
       gsrc[u] = A0 + (size_t)row * Kp + swz<G::CPR>(tr, lane % G::LPR) * 8;
-    } else {
+    } else if (!ADJ) {
       const int rb = (g - G::NI_A) * G::RPI + lane / G::LPR;
       const int q = q0 + rb < Nc ? q0 + rb : Nc - 1;
       gsrc[u] = K0 + (size_t)q * Kp + swz<G::CPR>(rb, lane % G::LPR) * 8;
+    } else {
+      // contraction row kb of the step, 4 outputs per chunk; chunks past the
+      // last output are clamped to it (their products are discarded)
+      const int kb = (g - G::NI_A) * G::RPI_T + lane / G::LPR_T;
+      const int q = min(q0 + 4 * swz_k4(kb, lane % G::LPR_T), Nc - 4);
+      gsrc[u] = K0 + (size_t)kb * (2 * Nc) + 2 * q;
     }
   }
   auto issue = [&](int i, int stage) {
-    const int koff = live[i] * BK;
+    const int koff = live[i] * BK;  // along coefficient rows
+    const size_t koff_b = ADJ ? (size_t)live[i] * (BK / 2) * (2 * Nc) : (size_t)koff;
     const unsigned base = ring_base + stage * G::STAGE + wave * G::PER_WAVE * 1024;
 #pragma unroll
-    for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + koff, base + u * 1024);
+    for (int u = 0; u < G::PER_WAVE; ++u) dma16(gsrc[u] + (is_a[u] ? koff : koff_b), base + u * 1024);
   };
   // Register-staged copies (REG): thread t moves the 16-byte chunks
   // t + NT u of the stage [A rows; B rows] (8 consecutive threads one
@@ -454,7 +444,19 @@ __global__ void __launch_bounds__((MixGeomS<WM, WN, ST>::NT))
 #pragma unroll
           for (int jj = 0; jj < TN; ++jj) {
             const int rb = (wn * TN + jj) * 32 + r32;
-            xb[jj] = *reinterpret_cast<const v8bf*>(Bs + rb * G::PITCH + swz<G::CPR>(rb, c) * 16);
+            if constexpr (!ADJ) {
+              xb[jj] = *reinterpret_cast<const v8bf*>(Bs + rb * G::PITCH + swz<G::CPR>(rb, c) * 16);
+            } else {
+              // contraction rows 4c .. 4c + 3 of output rb: (re, im) each
+              v4u_t y;
+#pragma unroll
+              for (int d = 0; d < 4; ++d) {
+                const int kr = 4 * c + d;
+                y[d] = *reinterpret_cast<const unsigned*>(Bs + kr * G::PITCH_T +
+                                                          swz_k4(kr, rb >> 2) * 16 + (rb & 3) * 4);
+              }
+              xb[jj] = __builtin_bit_cast(v8bf, y);
+            }
           }
 #pragma unroll
           for (int ii = 0; ii < NL; ++ii) {
@@ -473,8 +475,9 @@ __global__ void __launch_bounds__((MixGeomS<WM, WN, ST>::NT))
             v4u_t xr, xi;
 #pragma unroll
             for (int d = 0; d < 4; ++d) {
-              xr[d] = xa[ii][d] ^ 0x80000000u;                          // (re, -im)
-              xi[d] = __builtin_amdgcn_alignbit(xa[ii][d], xa[ii][d], 16u);  // (im, re)
+              const unsigned sw = __builtin_amdgcn_alignbit(xa[ii][d], xa[ii][d], 16u);
+              xr[d] = ADJ ? xa[ii][d] : xa[ii][d] ^ 0x80000000u;  // (re, im) / (re, -im)
+              xi[d] = ADJ ? sw ^ 0x80000000u : sw;                // (im, -re) / (im, re)
             }
             const v8bf ar = __builtin_bit_cast(v8bf, xr), ai = __builtin_bit_cast(v8bf, xi);
 #pragma unroll
@@ -573,7 +576,7 @@ __global__ void __launch_bounds__((MixGeomS<WM, WN, ST>::NT))
   }
 }
 
-template <int WM, int WN, int ST, bool REG>
+template <int WM, int WN, int ST, bool REG, bool ADJ = false>
 hipError_t launch_split(const Plan& p, int B, int Cin, int Cout, const void* coef, const void* K,
                         void* out, hipStream_t st) {
   using G = MixGeomS<WM, WN, ST>;
@@ -584,9 +587,9 @@ hipError_t launch_split(const Plan& p, int B, int Cin, int Cout, const void* coe
   for (int l = 0; l < p.L; ++l) tiles += ((2 * l + 1) * B + G::RA - 1) / G::RA;
   const int Nc = p.n_out * Cout;
   const long long blocks = tiles * ((Nc + G::RB - 1) / G::RB);
-  const hipError_t e = ensure_dynamic_lds((const void*)mix_split_kernel<WM, WN, ST, REG>, G::SMEM);
+  const hipError_t e = ensure_dynamic_lds((const void*)mix_split_kernel<WM, WN, ST, REG, ADJ>, G::SMEM);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((mix_split_kernel<WM, WN, ST, REG>), dim3(xcd_grid(blocks)), dim3(G::NT), G::SMEM,
+  hipLaunchKernelGGL((mix_split_kernel<WM, WN, ST, REG, ADJ>), dim3(xcd_grid(blocks)), dim3(G::NT), G::SMEM,
                      st, (const __bf16*)coef, (const __bf16*)K, (__bf16*)out, p.L, B, Cin, Cout,
                      p.n_in, p.n_out, si, so);
   return hipGetLastError();
@@ -878,7 +881,7 @@ hipError_t launch_mix_adj_dma(const Plan& p, int B, int Cin, int Cout, const voi
                               const void* K, void* out, hipStream_t st) {
   if (p.dtype == SWSFT_F32)
     return launch_geom_f32<SWSFT_MIX_DMA_F32, true>(p, B, Cin, Cout, coef, K, out, st);
-  return launch_geom<64, 128, 128, 2, true>(p, B, Cin, Cout, coef, K, out, st);
+  return launch_split<SWSFT_MIX_SPLIT_GEOM, false, true>(p, B, Cin, Cout, coef, K, out, st);
 }
 
 hipError_t launch_mix_dma(const Plan& p, int B, int Cin, int Cout, const void* coef,
