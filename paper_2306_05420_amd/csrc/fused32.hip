@@ -31,7 +31,17 @@ namespace {
 
 constexpr int kG = 32;      // grid size H = W
 constexpr int kMaps = 8;    // maps per workgroup
-constexpr int kNT = 256;    // one thread per (map, latitude row)
+constexpr int kRows = 256;  // (map, latitude row) pairs: one per thread in the FFTs
+#ifndef SWSFT_FUSED32_NT
+#define SWSFT_FUSED32_NT 512
+#endif
+// threads per workgroup: the FFTs use the first kRows; every wave takes
+// orders in the per-order GEMMs, so more waves shorten each wave's chain of
+// table (and coefficient) reads from L2 (molecule batch, 512 against 256
+// threads: forward 12.9 -> 11.8 us, inverse 14.4 -> 13.3 us; 1024 threads
+// would leave 64 registers per lane at two workgroups per CU and spill)
+constexpr int kNT = SWSFT_FUSED32_NT;
+constexpr int kWaves = kNT / 64;
 constexpr int kRP = 68;     // floats per staged grid row (64 + 4: row starts 4 banks apart)
 constexpr int kXP = 36;     // floats per (bin, column) row of the forward spectrum tile
 constexpr int kMapStride = kG * kRP + 4;  // staged rows of one map (inverse)
@@ -45,12 +55,12 @@ struct FSpins {
 __device__ __forceinline__ int fabs_i(int v) { return v < 0 ? -v : v; }
 
 // x [B][S][C][32][32] complex -> coef [L^2][B][S][C] complex (C % 8 == 0)
-__global__ void __launch_bounds__(kNT, 2)
+__global__ void __launch_bounds__(kNT, 2 * kNT / 256)
     fused32_fwd_kernel(const float* __restrict__ x, const float* __restrict__ tab,
                        float* __restrict__ coef, int L, int B, int S, int C) {
   // staged x rows [256][kRP], then the spectrum [32 bins][16 columns][kXP]
   __shared__ __align__(16) float sm[kG * 16 * kXP];
-  static_assert(kNT * kRP <= kG * 16 * kXP, "staged rows fit the spectrum tile");
+  static_assert(kRows * kRP <= kG * 16 * kXP, "staged rows fit the spectrum tile");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int M = 2 * L - 1;
   const int groups = C / kMaps;
@@ -60,29 +70,32 @@ __global__ void __launch_bounds__(kNT, 2)
 
   // the group's 8 maps (64 KiB, contiguous): 16-byte chunk c is row c / 16
   {
+    constexpr int NU = kRows * 16 / kNT;  // 16-byte chunks per thread
     const v4f* src = reinterpret_cast<const v4f*>(x + map0 * kG * kG * 2);
-    v4f buf[16];
+    v4f buf[NU];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) buf[u] = src[tid + kNT * u];
+    for (int u = 0; u < NU; ++u) buf[u] = src[tid + kNT * u];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
+    for (int u = 0; u < NU; ++u) {
       const int c = tid + kNT * u;
       *reinterpret_cast<v4f*>(sm + (c >> 4) * kRP + (c & 15) * 4) = buf[u];
     }
   }
   __syncthreads();
 
-  // thread tid = row (map = tid / 32, latitude j = tid % 32): X[k] = sum_q x[q] e^{-2 pi i q k / 32}
+  // thread tid < 256 = row (map = tid / 32, latitude j = tid % 32): X[k] = sum_q x[q] e^{-2 pi i q k / 32}
   float2 v[kG];
+  if (tid < kRows) {
 #pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const v4f q = *reinterpret_cast<const v4f*>(sm + tid * kRP + 4 * u);
-    v[2 * u] = make_float2(q[0], q[1]);
-    v[2 * u + 1] = make_float2(q[2], q[3]);
+    for (int u = 0; u < 16; ++u) {
+      const v4f q = *reinterpret_cast<const v4f*>(sm + tid * kRP + 4 * u);
+      v[2 * u] = make_float2(q[0], q[1]);
+      v[2 * u + 1] = make_float2(q[2], q[3]);
+    }
+    fft_reg<kG, -1>(v);
   }
-  fft_reg<kG, -1>(v);
   __syncthreads();  // every row is in registers before the spectrum overwrites it
-  {
+  if (tid < kRows) {
     const int map = tid >> 5, j = tid & 31;
 #pragma unroll
     for (int k = 0; k < kG; ++k) {
@@ -96,7 +109,7 @@ __global__ void __launch_bounds__(kNT, 2)
   // n = 2 map + re/im
   const int n = lane & 15, q = lane >> 4;
   const size_t row_stride = (size_t)S * C * 2;  // floats per coefficient row (l, m, b)
-  for (int mi = wave; mi < M; mi += 4) {
+  for (int mi = wave; mi < M; mi += kWaves) {
     const int m = mi - (L - 1);
     const int k = m & (kG - 1);
     v4f a0 = {0.f, 0.f, 0.f, 0.f}, a1 = a0;
@@ -125,7 +138,7 @@ __global__ void __launch_bounds__(kNT, 2)
 }
 
 // coef [L^2][Bc][S][C] complex (batch items 0 .. B-1 of Bc) -> y [B][S][C][32][32]
-__global__ void __launch_bounds__(kNT, 2)
+__global__ void __launch_bounds__(kNT, 2 * kNT / 256)
     fused32_inv_kernel(const float* __restrict__ coef, const float* __restrict__ tab,
                        float* __restrict__ y, int L, int Lp, int B, int Bc, int S, int C,
                        FSpins spins) {
@@ -142,7 +155,7 @@ __global__ void __launch_bounds__(kNT, 2)
   // per order m: D[j][n] = sum_l T'[m][j][l] coef[l][m][n], two blocks of 16 latitudes
   const int n = lane & 15, q = lane >> 4;
   const size_t row_stride = (size_t)S * C * 2;
-  for (int mi = wave; mi < M; mi += 4) {
+  for (int mi = wave; mi < M; mi += kWaves) {
     const int m = mi - (L - 1);
     const int k = m & (kG - 1);
     const int lo = fabs_i(m) > tabs ? fabs_i(m) : tabs;
@@ -171,29 +184,31 @@ __global__ void __launch_bounds__(kNT, 2)
   }
   __syncthreads();
 
-  // thread tid = row (map, j): bins with no order (L <= |m|) are zero;
+  // thread tid < 256 = row (map, j): bins with no order (L <= |m|) are zero;
   // y[q] = sum_k Y[k] e^{2 pi i q k / 32}
-  float* row = sm + (tid >> 5) * kMapStride + (tid & 31) * kRP;
-  float2 v[kG];
+  if (tid < kRows) {
+    float* row = sm + (tid >> 5) * kMapStride + (tid & 31) * kRP;
+    float2 v[kG];
 #pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const v4f w = *reinterpret_cast<const v4f*>(row + 4 * u);
-    v[2 * u] = make_float2(w[0], w[1]);
-    v[2 * u + 1] = make_float2(w[2], w[3]);
+    for (int u = 0; u < 16; ++u) {
+      const v4f w = *reinterpret_cast<const v4f*>(row + 4 * u);
+      v[2 * u] = make_float2(w[0], w[1]);
+      v[2 * u + 1] = make_float2(w[2], w[3]);
+    }
+#pragma unroll
+    for (int kk = 0; kk < kG; ++kk)
+      if (kk >= L && kk <= kG - L) v[kk] = make_float2(0.f, 0.f);
+    fft_reg<kG, 1>(v);
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      *reinterpret_cast<v4f*>(row + 4 * u) = (v4f){v[2 * u].x, v[2 * u].y, v[2 * u + 1].x, v[2 * u + 1].y};
   }
-#pragma unroll
-  for (int kk = 0; kk < kG; ++kk)
-    if (kk >= L && kk <= kG - L) v[kk] = make_float2(0.f, 0.f);
-  fft_reg<kG, 1>(v);
-#pragma unroll
-  for (int u = 0; u < 16; ++u)
-    *reinterpret_cast<v4f*>(row + 4 * u) = (v4f){v[2 * u].x, v[2 * u].y, v[2 * u + 1].x, v[2 * u + 1].y};
   __syncthreads();
 
   // the group's 8 output maps (64 KiB, contiguous)
   v4f* dst = reinterpret_cast<v4f*>(y + map0 * kG * kG * 2);
 #pragma unroll
-  for (int u = 0; u < 16; ++u) {
+  for (int u = 0; u < kRows * 16 / kNT; ++u) {
     const int c = tid + kNT * u, r = c >> 4;
     dst[c] = *reinterpret_cast<const v4f*>(sm + (r >> 5) * kMapStride + (r & 31) * kRP + (c & 15) * 4);
   }
